@@ -1,0 +1,156 @@
+/*
+ * dn.h -- C ABI of the deferred-normalization library (libdn.so), gfx950.
+ *
+ * Method: "LLM Inference Acceleration via Efficient Operation Fusion"
+ * (Salmani & Soloveychik, arXiv 2502.17728).  A LayerNorm or a Softmax that
+ * feeds a matrix product is split into an element-wise part, which becomes
+ * the product's operand, and a per-row collective part (the LayerNorm
+ * mean/variance, the softmax denominator), which is reduced concurrently and
+ * applied once after the product (Sec. II, Fig. 1; Eq. (5) and Eq. (8)).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensor pointers are DEVICE pointers (hipMalloc'd or equivalent), row-major
+ *   and contiguous, 16-byte aligned.  The caller owns all memory; the library
+ *   allocates nothing and keeps no state between calls.
+ * - Every call validates its arguments on the host BEFORE any HIP call; an
+ *   invalid call returns a status and enqueues nothing.  A valid call only
+ *   enqueues kernels on `stream` (NULL = the default stream) and returns; it
+ *   never synchronizes.  Buffers must stay alive until that work completes.
+ *   Calls on different streams are independent (reentrant).
+ * - Element types: DN_F32 (IEEE fp32) or DN_BF16 (bfloat16).  All accumulation
+ *   is fp32; outputs are rounded once, to nearest even, to the input type.
+ * - NaN/Inf inputs are not errors: they propagate as in the plain definition.
+ * - Sizes are int64 element counts; K and N (and d) must be multiples of 8.
+ * - Output ranges must not overlap input ranges (checked: DN_ERR_INVALID_ARG).
+ */
+#ifndef DN_H
+#define DN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DN_API __attribute__((visibility("default")))
+
+typedef enum { DN_F32 = 0, DN_BF16 = 1 } dn_dtype;
+
+typedef enum {
+    DN_OK = 0,
+    DN_ERR_INVALID_ARG = 1, /* NULL pointer, size < 1, bad eps, overlap, bad descriptor   */
+    DN_ERR_UNSUPPORTED = 2, /* valid request outside what the kernels implement            */
+    DN_ERR_MISALIGNED = 3,  /* a tensor pointer is not 16-byte aligned                     */
+    DN_ERR_HIP = 4          /* the HIP runtime reported an error when launching            */
+} dn_status;
+
+/* Human-readable name of a status code (static string; never NULL). */
+DN_API const char* dn_status_string(int status);
+
+/* Library version, (major << 16) | minor. */
+DN_API int dn_version(void);
+
+/* ======================================================================= */
+/* LayerNorm -> Linear, deferred (Sec. II-A, Eq. (1), (2), (4), (5))        */
+/* ======================================================================= */
+
+/*
+ * Static weights prepared once (the paper computes the static factors of
+ * Eq. (5) "at compile time", Sec. II-A; here once per weight set, off the
+ * per-token path).  From W[K][N] (the paper's F, n x m), gamma[K], beta[K]
+ * and an optional bias[N], ln_linear_prepare writes into `packed`:
+ *   Wt'[N][K] = (Diag(gamma) W)^T  rounded once to `dtype` (K contiguous),
+ *   c[N]      = sum_k W'[k][n]     over the ROUNDED W' (fp32),
+ *   b[N]      = sum_k beta[k] W[k][n] + bias[n]     (fp32; beta F of Eq. (5)).
+ * `packed` must be ln_linear_packed_bytes(K, N, dtype) bytes, 256-byte
+ * aligned, device memory; `*w_out` is filled on the host and is what
+ * ln_linear_deferred takes.  beta and bias may be NULL (treated as zero).
+ */
+typedef struct {
+    int64_t K, N;           /* normalized dim, output features                */
+    int32_t dtype;          /* dn_dtype of W' and of x/out                    */
+    int32_t layout_version; /* DN_LN_LAYOUT_VERSION when produced by prepare   */
+    void* packed;           /* device buffer holding Wt', c, b                */
+} ln_linear_weights;
+
+#define DN_LN_LAYOUT_VERSION 1
+
+/* Bytes of the packed buffer for (K, N, dtype); 0 if the request is invalid. */
+DN_API size_t ln_linear_packed_bytes(int64_t K, int64_t N, int dtype);
+
+DN_API dn_status ln_linear_prepare(const void* W, const void* gamma, const void* beta,
+                            const void* bias, int64_t K, int64_t N, int dtype,
+                            void* packed, size_t packed_bytes,
+                            ln_linear_weights* w_out, hipStream_t stream);
+
+/*
+ * out[M][N] = LayerNorm(x[M][K]) . W + bias, computed the deferred way:
+ * the MFMA product acc = x . W' runs on the un-normalized x while the row
+ * statistics (sum x, sum x^2) are reduced in the same workgroup, and the
+ * epilogue applies  out = rstd * (acc - mean * c) + b  once (Eq. (5) with the
+ * centering (I - E/n) applied as  x(I - E/n)W' = xW' - mean 1 W').
+ * mean and the biased variance follow Eq. (1); rstd = 1/sqrt(var + eps) as
+ * in Eq. (2).  eps must be finite and >= 0.  x and out have w->dtype.
+ */
+DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M,
+                             float eps, void* out, hipStream_t stream);
+
+/* ======================================================================= */
+/* Softmax -> P.V, deferred (Sec. II-B, Eq. (7), (8) and its footnote)      */
+/* ======================================================================= */
+
+/*
+ * out[BH][Lq][d] = softmax(S[BH][Lq][Lk]) . V[BH][Lk][d] per head, computed
+ * the deferred way: the MFMA consumes the un-normalized numerators
+ * exp(s - m) (rounded to bf16), the row max m (footnote of Eq. (7)) is kept
+ * online per key tile, the row sum l is accumulated concurrently, and the
+ * epilogue divides once: out = acc / l (Eq. (8)).
+ * causal = 1 keeps key j for query i iff j <= i (requires Lq == Lk); keys
+ * j > i are never read.  causal = 0 uses every key.  A row whose kept scores
+ * are all -inf gives NaN.  dtype must be DN_BF16; d must be 64 or 128.
+ */
+DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq,
+                              int64_t Lk, int64_t d, int causal, int dtype, void* out,
+                              hipStream_t stream);
+
+/* ======================================================================= */
+/* Unfused comparators: the conventional sub-graph of Fig. 1(a)             */
+/* ======================================================================= */
+
+/* y[M][K] = (x - mean)/sqrt(var + eps) * gamma + beta, Eq. (1)-(2).  beta may be NULL. */
+DN_API dn_status layernorm(const void* x, const void* gamma, const void* beta, int64_t M,
+                    int64_t K, float eps, int dtype, void* y, hipStream_t stream);
+
+/*
+ * P[BH][Lq][Lk] = softmax of each row of S (Eq. (7) with the max subtraction).
+ * causal = 0: every key.  causal = 1: keys j <= i, and P = 0 for j > i (dense,
+ * the conventional output).  causal = 2: keys j <= i, and only the aligned
+ * 8-element groups that contain some j <= i are written (entries j > i inside
+ * such a group are 0; the rest of the upper triangle is left untouched); this
+ * is the input gemm(a_causal = 1) expects.  causal != 0 requires Lq == Lk.
+ * dtype must be DN_BF16; Lk <= 16384.
+ */
+DN_API dn_status softmax(const void* S, int64_t BH, int64_t Lq, int64_t Lk, int causal,
+                  int dtype, void* P, hipStream_t stream);
+
+/*
+ * C[batch][M][N] = A[batch][M][K] . B (+ bias[N]), fp32 accumulation.
+ * b_layout = 0: B is [batch][K][N] (row-major, N contiguous).
+ * b_layout = 1: B is given transposed, [batch][N][K] (K contiguous) -- the
+ *               layout ln_linear_prepare uses for static weights.
+ * a_causal = 1: A is lower-triangular by contract (A[i][j] treated as 0 for
+ *               j > i, never read beyond the diagonal tile); requires M == K.
+ * bias may be NULL.  Same MFMA main loop as ln_linear_deferred.
+ */
+DN_API dn_status gemm(const void* A, const void* B, const void* bias, int64_t batch, int64_t M,
+               int64_t K, int64_t N, int b_layout, int a_causal, int dtype, void* C,
+               hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DN_H */

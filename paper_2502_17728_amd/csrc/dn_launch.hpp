@@ -1,0 +1,43 @@
+// dn_launch.hpp -- host-side launchers of the libdn kernels (internal; the
+// public C ABI in include/dn.h validates arguments and then calls these).
+// Every launcher only enqueues on `stream` and returns hipGetLastError().
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dn {
+
+// Byte offsets of the pieces of a prepared LN->Linear weight buffer.
+struct PackedLayout {
+    size_t wt_off, wt_bytes;  // Wt'[N][K] in the element type
+    size_t c_off, b_off;      // c[N], b[N] fp32
+    size_t total;
+};
+PackedLayout packed_layout(int64_t K, int64_t N, int dtype);
+
+hipError_t launch_ln_prepare(const void* W, const void* gamma, const void* beta, const void* bias,
+                             int64_t K, int64_t N, int dtype, void* packed, hipStream_t s);
+
+hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K,
+                                     int64_t N, int dtype, float eps, void* out, hipStream_t s);
+
+hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t batch, int64_t M,
+                       int64_t K, int64_t N, int b_layout, int a_causal, int dtype, void* C,
+                       hipStream_t s);
+
+hipError_t launch_softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq,
+                                      int64_t Lk, int64_t d, int causal, void* out, hipStream_t s);
+
+hipError_t launch_layernorm(const void* x, const void* gamma, const void* beta, int64_t M,
+                            int64_t K, float eps, int dtype, void* y, hipStream_t s);
+
+hipError_t launch_softmax(const void* S, int64_t BH, int64_t Lq, int64_t Lk, int causal, void* P,
+                          hipStream_t s);
+
+// Largest K (elements per row) the row-wise unfused kernels keep in registers.
+constexpr int64_t kMaxRowElemsBf16 = 16384;
+constexpr int64_t kMaxRowElemsF32 = 8192;
+
+}  // namespace dn

@@ -1,0 +1,183 @@
+"""Python binding of libdn (include/dn.h): argument marshalling only.
+
+Every function here has the name of the C entry point it calls, takes torch
+tensors that live on the GPU, passes their device pointers and sizes through
+ctypes, and launches on the current torch stream (or the one given).  All
+arithmetic happens in the HIP kernels; nothing here computes on the host, and
+there is no fallback: if ``libdn.so`` is missing the import fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdn.so")
+
+DN_F32, DN_BF16 = 0, 1
+DN_LN_LAYOUT_VERSION = 1
+STATUS = {0: "DN_OK", 1: "DN_ERR_INVALID_ARG", 2: "DN_ERR_UNSUPPORTED", 3: "DN_ERR_MISALIGNED", 4: "DN_ERR_HIP"}
+SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linear_prepare",
+           "ln_linear_deferred", "softmax_pv_deferred", "layernorm", "softmax", "gemm")
+
+
+class DNError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {STATUS.get(status, status)}")
+        self.status = status
+
+
+class LnLinearWeights(ctypes.Structure):
+    """Mirror of ``ln_linear_weights`` in dn.h."""
+    _fields_ = [("K", ctypes.c_int64), ("N", ctypes.c_int64), ("dtype", ctypes.c_int32),
+                ("layout_version", ctypes.c_int32), ("packed", ctypes.c_void_p)]
+
+
+def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
+    if not os.path.exists(path):
+        raise ImportError(f"libdn.so not found at {path}; build it with "
+                          f"`python -m paper_2502_17728_amd.build` (needs hipcc for gfx950)")
+    lib = ctypes.CDLL(path)
+    vp, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
+    lib.dn_status_string.argtypes, lib.dn_status_string.restype = [i32], ctypes.c_char_p
+    lib.dn_version.argtypes, lib.dn_version.restype = [], i32
+    lib.ln_linear_packed_bytes.argtypes, lib.ln_linear_packed_bytes.restype = [i64, i64, i32], ctypes.c_size_t
+    lib.ln_linear_prepare.argtypes = [vp, vp, vp, vp, i64, i64, i32, vp, ctypes.c_size_t,
+                                      ctypes.POINTER(LnLinearWeights), vp]
+    lib.ln_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
+    lib.softmax_pv_deferred.argtypes = [vp, vp, i64, i64, i64, i64, i32, i32, vp, vp]
+    lib.layernorm.argtypes = [vp, vp, vp, i64, i64, f32, i32, vp, vp]
+    lib.softmax.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp]
+    lib.gemm.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, i32, i32, vp, vp]
+    for f in ("ln_linear_prepare", "ln_linear_deferred", "softmax_pv_deferred", "layernorm", "softmax", "gemm"):
+        getattr(lib, f).restype = i32
+    return lib
+
+
+_lib = load_library()
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return DN_F32
+    if t.dtype == torch.bfloat16:
+        return DN_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _dev(t: Optional[torch.Tensor], name: str):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise DNError(fn, status)
+
+
+@dataclasses.dataclass
+class PreparedLinear:
+    """Prepared static weights: the packed device buffer and its descriptor."""
+    packed: torch.Tensor
+    desc: LnLinearWeights
+
+    @property
+    def K(self):
+        return self.desc.K
+
+    @property
+    def N(self):
+        return self.desc.N
+
+
+def ln_linear_packed_bytes(K: int, N: int, dtype: int) -> int:
+    return int(_lib.ln_linear_packed_bytes(K, N, dtype))
+
+
+def ln_linear_prepare(W: torch.Tensor, gamma: torch.Tensor, beta: Optional[torch.Tensor] = None,
+                      bias: Optional[torch.Tensor] = None, stream=None) -> PreparedLinear:
+    K, N = W.shape
+    dt = _dt(W)
+    nbytes = ln_linear_packed_bytes(K, N, dt)
+    if nbytes == 0:
+        raise DNError("ln_linear_packed_bytes", 1)
+    packed = torch.empty(nbytes, dtype=torch.uint8, device=W.device)
+    desc = LnLinearWeights()
+    _check("ln_linear_prepare", _lib.ln_linear_prepare(
+        _dev(W, "W"), _dev(gamma, "gamma"), _dev(beta, "beta"), _dev(bias, "bias"), K, N, dt,
+        _dev(packed, "packed"), nbytes, ctypes.byref(desc), _stream(stream)))
+    return PreparedLinear(packed, desc)
+
+
+def ln_linear_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
+                       out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    M = x.shape[0]
+    if out is None:
+        out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
+    if _dt(x) != w.desc.dtype:
+        raise TypeError("x dtype differs from the prepared weights")
+    _check("ln_linear_deferred", _lib.ln_linear_deferred(
+        _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def softmax_pv_deferred(S: torch.Tensor, V: torch.Tensor, causal: bool = False,
+                        out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    BH, Lq, Lk = S.shape
+    d = V.shape[-1]
+    if out is None:
+        out = torch.empty((BH, Lq, d), dtype=S.dtype, device=S.device)
+    _check("softmax_pv_deferred", _lib.softmax_pv_deferred(
+        _dev(S, "S"), _dev(V, "V"), BH, Lq, Lk, d, int(causal), _dt(S), _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def layernorm(x: torch.Tensor, gamma: torch.Tensor, beta: Optional[torch.Tensor] = None, eps: float = 1e-5,
+              out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    M, K = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    _check("layernorm", _lib.layernorm(_dev(x, "x"), _dev(gamma, "gamma"), _dev(beta, "beta"), M, K, eps,
+                                       _dt(x), _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def softmax(S: torch.Tensor, causal: int = 0, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    BH, Lq, Lk = S.shape
+    if out is None:
+        out = torch.empty_like(S)
+    _check("softmax", _lib.softmax(_dev(S, "S"), BH, Lq, Lk, int(causal), _dt(S), _dev(out, "out"),
+                                   _stream(stream)))
+    return out
+
+
+def gemm(A: torch.Tensor, B: torch.Tensor, bias: Optional[torch.Tensor] = None, b_layout: int = 0,
+         a_causal: bool = False, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    squeeze = A.dim() == 2
+    A3 = A.unsqueeze(0) if squeeze else A
+    B3 = B.unsqueeze(0) if B.dim() == 2 else B
+    batch, M, K = A3.shape
+    N = B3.shape[2] if b_layout == 0 else B3.shape[1]
+    if out is None:
+        out = torch.empty((batch, M, N), dtype=A.dtype, device=A.device)
+    _check("gemm", _lib.gemm(_dev(A3, "A"), _dev(B3, "B"), _dev(bias, "bias"), batch, M, K, N, int(b_layout),
+                             int(a_causal), _dt(A), _dev(out, "out"), _stream(stream)))
+    return out[0] if squeeze else out

@@ -1,0 +1,124 @@
+"""The C ABI on the host: the library loads, exports every entry point that
+include/dn.h declares, and rejects invalid calls before any HIP call (so
+these run without a GPU; every call below fails validation)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2502_17728_amd import ops
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+INVALID, UNSUPPORTED, MISALIGNED = 1, 2, 3
+P = 0x7F0000000000  # aligned fake device addresses: never dereferenced by validation
+P2 = P + (1 << 36)
+P3 = P + (2 << 36)
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "dn.h")).read()
+    return sorted(set(re.findall(r"DN_API\s+[\w\s\*]+?\b(\w+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_symbols() == sorted(ops.SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(ops.library_path())
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_version():
+    lib = ops._lib
+    assert [lib.dn_status_string(i).decode() for i in range(5)] == [ops.STATUS[i] for i in range(5)]
+    assert lib.dn_status_string(99) == b"DN_ERR_UNKNOWN"
+    assert lib.dn_version() >= 1
+
+
+def test_packed_bytes():
+    f = ops.ln_linear_packed_bytes
+    assert f(0, 8, 1) == 0 and f(8, 0, 1) == 0 and f(8, 8, 7) == 0
+    assert f(4096, 12288, 1) == 4096 * 12288 * 2 + 2 * 12288 * 4   # Wt' + c + b, 256-aligned pieces
+    assert f(768, 3072, 0) == 768 * 3072 * 4 + 2 * 3072 * 4
+    assert f(8, 8, 1) % 256 == 0
+
+
+def _w(K=64, N=64, dtype=1, version=1, packed=P3):
+    return ops.LnLinearWeights(K, N, dtype, version, packed)
+
+
+def test_ln_linear_deferred_validation():
+    f = ops._lib.ln_linear_deferred
+    w = _w()
+    assert f(None, ctypes.byref(w), 4, 1e-5, P2, None) == INVALID
+    assert f(P, None, 4, 1e-5, P2, None) == INVALID
+    assert f(P, ctypes.byref(w), 0, 1e-5, P2, None) == INVALID
+    assert f(P, ctypes.byref(w), 4, -1.0, P2, None) == INVALID
+    assert f(P, ctypes.byref(w), 4, float("nan"), P2, None) == INVALID
+    assert f(P, ctypes.byref(w), 4, float("inf"), P2, None) == INVALID
+    assert f(P, ctypes.byref(_w(version=0)), 4, 1e-5, P2, None) == INVALID
+    assert f(P, ctypes.byref(_w(packed=None)), 4, 1e-5, P2, None) == INVALID
+    assert f(P, ctypes.byref(_w(dtype=5)), 4, 1e-5, P2, None) == INVALID
+    assert f(P, ctypes.byref(_w(K=60)), 4, 1e-5, P2, None) == UNSUPPORTED
+    assert f(P + 8, ctypes.byref(w), 4, 1e-5, P2, None) == MISALIGNED
+    assert f(P, ctypes.byref(w), 4, 1e-5, P2 + 2, None) == MISALIGNED
+    assert f(P, ctypes.byref(_w(packed=P3 + 16)), 4, 1e-5, P2, None) == MISALIGNED
+    assert f(P, ctypes.byref(w), 4, 1e-5, P + 128, None) == INVALID          # out overlaps x
+    assert f(P, ctypes.byref(w), 4, 1e-5, P3 + 256, None) == INVALID         # out overlaps packed
+
+
+def test_ln_linear_prepare_validation():
+    f = ops._lib.ln_linear_prepare
+    w = ops.LnLinearWeights()
+    nb = ops.ln_linear_packed_bytes(64, 64, 1)
+    assert f(None, P2, None, None, 64, 64, 1, P3, nb, ctypes.byref(w), None) == INVALID
+    assert f(P, P2, None, None, 64, 64, 1, P3, nb - 1, ctypes.byref(w), None) == INVALID
+    assert f(P, P2, None, None, 64, 64, 1, P3, nb, None, None) == INVALID
+    assert f(P, P2, None, None, 64, 68, 1, P3, 1 << 20, ctypes.byref(w), None) == UNSUPPORTED
+    assert f(P, P2, None, None, 64, 64, 1, P3 + 16, nb, ctypes.byref(w), None) == MISALIGNED
+    assert f(P, P2, None, None, 64, 64, 1, P, nb, ctypes.byref(w), None) == INVALID   # packed overlaps W
+    assert w.layout_version == 0  # untouched on failure
+
+
+def test_softmax_pv_deferred_validation():
+    f = ops._lib.softmax_pv_deferred
+    assert f(None, P2, 1, 64, 64, 64, 0, 1, P3, None) == INVALID
+    assert f(P, P2, 1, 64, 64, 64, 2, 1, P3, None) == INVALID            # causal must be 0/1
+    assert f(P, P2, 1, 32, 64, 64, 1, 1, P3, None) == INVALID            # causal needs Lq == Lk
+    assert f(P, P2, 0, 64, 64, 64, 0, 1, P3, None) == INVALID
+    assert f(P, P2, 1, 64, 64, 64, 0, 0, P3, None) == UNSUPPORTED        # fp32 not implemented
+    assert f(P, P2, 1, 64, 64, 96, 0, 1, P3, None) == UNSUPPORTED        # d must be 64 or 128
+    assert f(P, P2, 1, 64, 60, 64, 0, 1, P3, None) == UNSUPPORTED        # Lk % 8
+    assert f(P, P2 + 4, 1, 64, 64, 64, 0, 1, P3, None) == MISALIGNED
+    assert f(P, P2, 1, 64, 64, 64, 0, 1, P + 64, None) == INVALID        # out overlaps S
+
+
+def test_unfused_validation():
+    ln, sm, gm = ops._lib.layernorm, ops._lib.softmax, ops._lib.gemm
+    assert ln(None, P2, None, 4, 64, 1e-5, 1, P3, None) == INVALID
+    assert ln(P, P2, None, 4, 64, -1e-5, 1, P3, None) == INVALID
+    assert ln(P, P2, None, 4, 20, 1e-5, 1, P3, None) == UNSUPPORTED
+    assert ln(P, P2, None, 4, 1 << 20, 1e-5, 1, P3, None) == UNSUPPORTED  # row kept in registers
+    assert ln(P, P2, P + 8, 4, 64, 1e-5, 1, P3, None) == MISALIGNED
+    assert ln(P, P2, None, 4, 64, 1e-5, 1, P, None) == INVALID           # in place not allowed
+    assert sm(P, 1, 64, 64, 3, 1, P2, None) == INVALID
+    assert sm(P, 1, 64, 32, 1, 1, P2, None) == INVALID
+    assert sm(P, 1, 64, 64, 0, 0, P2, None) == UNSUPPORTED
+    assert sm(P, 1, 64, 64, 0, 1, P, None) == INVALID
+    assert gm(P, P2, None, 1, 64, 64, 64, 2, 0, 1, P3, None) == INVALID   # b_layout
+    assert gm(P, P2, None, 1, 64, 32, 64, 0, 1, 1, P3, None) == INVALID   # causal needs M == K
+    assert gm(P, P2, None, 1, 64, 64, 60, 0, 0, 1, P3, None) == UNSUPPORTED
+    assert gm(P, P2, None, 1, 64, 64, 64, 0, 0, 0, P3, None) == UNSUPPORTED  # fp32 needs [N][K] B
+    assert gm(P, P2, None, 70000, 8, 8, 8, 1, 0, 1, P3, None) == UNSUPPORTED
+    assert gm(P, P2, None, 1, 64, 64, 64, 1, 0, 1, P2 + 64, None) == INVALID  # C overlaps B
+    assert gm(P, P2, P3 + 2, 1, 64, 64, 64, 1, 0, 1, P3 + 4096, None) == MISALIGNED
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        ops.layernorm(torch.zeros(4, 64, dtype=torch.bfloat16), torch.ones(64, dtype=torch.bfloat16),
+                      out=torch.zeros(4, 64, dtype=torch.bfloat16))

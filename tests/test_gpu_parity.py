@@ -1,0 +1,250 @@
+"""GPU parity: the HIP path, called through the C ABI, against the fp64 oracle.
+
+Small cases span several tiles and ragged tails; the named workloads run at
+full size in the bench's launch configuration and are checked on sampled
+rows the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2502_17728_amd import inputs as I
+from tests.parity import TOL, cuda, rowwise_rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ops():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2502_17728_amd import ops as _ops
+    return _ops
+
+
+def _ln_check(ops, case, rows=None, tol=None):
+    x, W = cuda(case["x"]), cuda(case["W"])
+    w = ops.ln_linear_prepare(W, cuda(case["gamma"]), cuda(case["beta"]), cuda(case["bias"]))
+    out = ops.ln_linear_deferred(x, w, case["eps"])
+    torch.cuda.synchronize()
+    xs = case["x"] if rows is None else case["x"][torch.as_tensor(rows)]
+    ref = oracle.ln_linear(xs, case["gamma"], case["beta"], case["W"], case["bias"], case["eps"])
+    got = out.cpu() if rows is None else out.cpu()[torch.as_tensor(rows)]
+    err = rowwise_rel_err(got, ref)
+    print(f"ln_linear_deferred {tuple(case['x'].shape)}x{tuple(case['W'].shape)} {case['x'].dtype}: err={err:.3e}")
+    assert err <= (tol or TOL[case["x"].dtype]), err
+    return out, w
+
+
+# ---------------------------------------------------------------------------- LN -> Linear
+def test_ln_linear_f32_workload(ops):
+    _ln_check(ops, I.make_ln(I.LN_F32_SMALL))
+
+
+@pytest.mark.parametrize("M,K,N", [(37, 104, 72), (1, 8, 8), (300, 512, 200)])
+def test_ln_linear_f32_ragged(ops, M, K, N):
+    _ln_check(ops, I.make_ln_case(M, K, N, "f32", seed=M))
+
+
+@pytest.mark.parametrize("M,K,N", [(17, 64, 136), (200, 520, 392), (257, 1024, 264), (300, 72, 8),
+                                   (128, 768, 3072), (1, 8, 8)])
+def test_ln_linear_bf16_ragged(ops, M, K, N):
+    _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M + K))
+
+
+@pytest.mark.parametrize("M", [1, 3, 4, 16])
+@pytest.mark.parametrize("K,N", [(1024, 520), (8200, 64)])
+def test_ln_linear_bf16_decode_shapes(ops, M, K, N):
+    _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M * 7 + 1, outliers=4))
+
+
+def test_ln_linear_bf16_outliers(ops):
+    _ln_check(ops, I.make_ln_case(96, 2048, 384, "bf16", seed=5, outliers=8))
+
+
+def test_ln_linear_mean_offset_stress(ops):
+    # rows with mean 4 and unit spread: the deferred form subtracts mean*c after
+    # the product, losing about (|mean|/std) * 2^-24 * sqrt(K) relative; well
+    # inside the bf16 bound, and documented as the method's cancellation limit
+    _ln_check(ops, I.make_ln_case(64, 1024, 256, "bf16", seed=9, mean_offset=4.0))
+
+
+def test_ln_linear_constant_rows_give_b(ops):
+    case = I.make_ln_case(20, 256, 136, "bf16", seed=11)
+    case["x"] = torch.full_like(case["x"], 0.75)
+    _ln_check(ops, case)
+
+
+def test_ln_linear_qkv_workload_sampled(ops):
+    w = I.LN_QKV
+    case = I.make_ln(w)
+    _ln_check(ops, case, rows=I.sample_rows(w.M, 24, seed=3))
+
+
+@pytest.mark.parametrize("t", [1, 4, 16])
+def test_ln_linear_ffn_decode_workload(ops, t):
+    _ln_check(ops, I.make_ln(I.ln_ffn_decode(t)))
+
+
+def test_ln_linear_deterministic(ops):
+    case = I.make_ln_case(130, 512, 256, "bf16", seed=2)
+    x = cuda(case["x"])
+    w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
+    a = ops.ln_linear_deferred(x, w)
+    b = ops.ln_linear_deferred(x, w)
+    assert torch.equal(a, b)
+
+
+def test_ln_linear_guard_band(ops):
+    case = I.make_ln_case(33, 256, 72, "bf16", seed=4)
+    w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
+    buf = torch.full((33 * 72 + 2 * 512,), 7.0, dtype=torch.bfloat16, device="cuda")
+    out = buf[512:512 + 33 * 72].view(33, 72)
+    ops.ln_linear_deferred(cuda(case["x"]), w, out=out)
+    torch.cuda.synchronize()
+    assert (buf[:512] == 7.0).all() and (buf[-512:] == 7.0).all()
+
+
+# ---------------------------------------------------------------------------- Softmax -> P.V
+def _sm_check(ops, case, rows=None):
+    S, V = case["S"], case["V"]
+    BH, L, _ = S.shape
+    causal = case["causal"]
+    out = ops.softmax_pv_deferred(cuda(S), cuda(V), causal=causal)
+    torch.cuda.synchronize()
+    if rows is None:
+        rows = np.arange(BH * L)
+    rows = np.asarray(rows)
+    head, q = rows // L, rows % L
+    S_rows = S.reshape(BH * L, L)[torch.as_tensor(rows)]
+    ref = oracle.softmax_pv(S_rows, V, head=head, qpos=q if causal else None)
+    got = out.cpu().reshape(BH * L, -1)[torch.as_tensor(rows)]
+    err = rowwise_rel_err(got, ref)
+    print(f"softmax_pv_deferred {tuple(S.shape)} d={V.shape[-1]} causal={causal}: err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
+    return out
+
+
+def test_softmax_pv_small_workload(ops):
+    _sm_check(ops, I.make_sm(I.SM_BF16_SMALL))
+
+
+@pytest.mark.parametrize("BH,L,d,causal", [(3, 200, 64, True), (2, 136, 128, False), (2, 8, 64, True),
+                                           (1, 392, 128, True), (5, 64, 64, False), (2, 520, 128, False)])
+def test_softmax_pv_ragged(ops, BH, L, d, causal):
+    _sm_check(ops, I.make_sm_case(BH, L, d, causal, seed=L, from_qk=causal))
+
+
+def test_softmax_pv_causal_workload_sampled(ops):
+    w = I.SM_CAUSAL
+    case = I.make_sm(w)
+    rows = I.sample_rows(w.BH * w.L, 48, seed=5)
+    _sm_check(ops, case, rows=rows)
+
+
+def test_softmax_pv_causal_row0_exact(ops):
+    case = I.make_sm_case(2, 256, 128, True, seed=3)
+    out = ops.softmax_pv_deferred(cuda(case["S"]), cuda(case["V"]), causal=True)
+    assert torch.equal(out[:, 0].cpu(), case["V"][:, 0])
+
+
+def test_softmax_pv_causal_flag_matches_premasked(ops):
+    case = I.make_sm_case(2, 264, 64, True, seed=8, from_qk=True)   # S carries -inf above the diagonal
+    S, V = cuda(case["S"]), cuda(case["V"])
+    a = ops.softmax_pv_deferred(S, V, causal=True)
+    b = ops.softmax_pv_deferred(S, V, causal=False)
+    assert torch.equal(a, b)
+
+
+def test_softmax_pv_fully_masked_row_is_nan(ops):
+    case = I.make_sm_case(1, 64, 64, False, seed=1)
+    case["S"][0, 5, :] = float("-inf")
+    out = _sm_check(ops, case)
+    assert torch.isnan(out[0, 5].float()).all()
+
+
+def test_softmax_pv_deterministic(ops):
+    case = I.make_sm_case(2, 296, 128, True, seed=6)
+    S, V = cuda(case["S"]), cuda(case["V"])
+    assert torch.equal(ops.softmax_pv_deferred(S, V, causal=True), ops.softmax_pv_deferred(S, V, causal=True))
+
+
+def test_softmax_pv_rejects_ragged_key_length(ops):
+    case = I.make_sm_case(1, 300, 64, False, seed=6)
+    with pytest.raises(ops.DNError) as e:
+        ops.softmax_pv_deferred(cuda(case["S"]), cuda(case["V"]))
+    assert e.value.status == 2  # DN_ERR_UNSUPPORTED: Lk must be a multiple of 8
+
+
+# ---------------------------------------------------------------------------- unfused comparators
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layernorm_unfused(ops, dtype):
+    case = I.make_ln_case(77, 1032, 8, dtype, seed=3, outliers=2)
+    y = ops.layernorm(cuda(case["x"]), cuda(case["gamma"]), cuda(case["beta"]), case["eps"])
+    ref = oracle.layernorm(case["x"], case["gamma"], case["beta"], case["eps"])
+    err = rowwise_rel_err(y.cpu(), ref)
+    assert err <= TOL[case["x"].dtype] / (4 if dtype == "bf16" else 1), err
+
+
+@pytest.mark.parametrize("causal", [0, 1])
+def test_softmax_unfused(ops, causal):
+    case = I.make_sm_case(2, 136, 64, bool(causal), seed=4)
+    P = ops.softmax(cuda(case["S"]), causal=causal)
+    L = 136
+    ref = oracle.softmax(case["S"].reshape(-1, L), np.tile(np.arange(L), 2) if causal else None)
+    assert rowwise_rel_err(P.cpu().reshape(-1, L), ref) <= 1e-2
+
+
+@pytest.mark.parametrize("b_layout", [0, 1])
+def test_gemm_unfused(ops, b_layout):
+    g = torch.Generator().manual_seed(1)
+    A = torch.randn(3, 136, 200, generator=g).to(torch.bfloat16)
+    B = torch.randn(3, 200, 72, generator=g).to(torch.bfloat16)
+    bias = torch.randn(72, generator=g).to(torch.bfloat16)
+    Bd = B if b_layout == 0 else B.transpose(1, 2).contiguous()
+    C = ops.gemm(cuda(A), cuda(Bd), cuda(bias), b_layout=b_layout)
+    ref = oracle.linear(A, B, bias)
+    assert rowwise_rel_err(C.cpu().reshape(-1, 72), ref.reshape(-1, 72)) <= TOL[torch.bfloat16]
+
+
+def test_gemm_unfused_f32(ops):
+    g = torch.Generator().manual_seed(2)
+    A, B = torch.randn(70, 96, generator=g), torch.randn(96, 40, generator=g)
+    C = ops.gemm(cuda(A), cuda(B.t().contiguous()), b_layout=1)
+    assert rowwise_rel_err(C.cpu(), oracle.linear(A, B)) <= TOL[torch.float32]
+
+
+def test_gemm_causal_matches_dense_lower_triangular(ops):
+    g = torch.Generator().manual_seed(3)
+    L, d = 264, 64
+    A = torch.tril(torch.rand(2, L, L, generator=g)).to(torch.bfloat16)
+    V = torch.randn(2, L, d, generator=g).to(torch.bfloat16)
+    junk = A.clone()
+    junk[:, torch.triu(torch.ones(L, L, dtype=torch.bool), 1)] = float("nan")   # never used
+    C = ops.gemm(cuda(junk), cuda(V), a_causal=True)
+    ref = oracle.linear(A, V)
+    assert rowwise_rel_err(C.cpu().reshape(-1, d), ref.reshape(-1, d)) <= TOL[torch.bfloat16]
+
+
+def test_unfused_chains_match_deferred(ops):
+    case = I.make_ln_case(150, 512, 264, "bf16", seed=12)
+    x = cuda(case["x"])
+    w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
+    fused = ops.ln_linear_deferred(x, w)
+    y = ops.layernorm(x, cuda(case["gamma"]), cuda(case["beta"]))
+    unfused = ops.gemm(y, cuda(case["W"]).t().contiguous(), b_layout=1)
+    ref = oracle.ln_linear(case["x"], case["gamma"], case["beta"], case["W"], None, case["eps"])
+    assert rowwise_rel_err(unfused.cpu(), ref) <= TOL[torch.bfloat16]
+    assert rowwise_rel_err(fused.cpu(), oracle.to_f64(unfused.cpu())) <= TOL[torch.bfloat16]
+    sm = I.make_sm_case(2, 256, 128, True, seed=13)
+    S, V = cuda(sm["S"]), cuda(sm["V"])
+    P = ops.softmax(S, causal=2)
+    o2 = ops.gemm(P, V, a_causal=True)
+    o1 = ops.softmax(S, causal=1)
+    o1 = ops.gemm(o1, V)
+    fused = ops.softmax_pv_deferred(S, V, causal=True)
+    ref = oracle.softmax_pv(sm["S"].reshape(-1, 256), sm["V"], head=np.repeat([0, 1], 256),
+                            qpos=np.tile(np.arange(256), 2))
+    for o in (o1, o2, fused):
+        assert rowwise_rel_err(o.cpu().reshape(-1, 128), ref) <= TOL[torch.bfloat16]
