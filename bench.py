@@ -1,0 +1,281 @@
+"""Benchmark of deferred normalization on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+the deferred LayerNorm -> Linear (Sec. II-A, Eq. (5)) and the deferred
+Softmax -> P.V (Sec. II-B, Eq. (8)).  The default workload is a 7B-class
+Transformer layer's two fusion sites: LN -> QKV projection, x[4096, 4096] .
+W[4096, 12288], and causal Softmax -> P.V over 32 heads, 8192 keys, d = 128.
+
+Prints ONE JSON line.  `value` is whole-step throughput (TFLOP/s, algorithmic
+FLOP of both products) with inputs already resident in HBM; per-kernel times
+come from HIP events recorded on the stream the kernels are launched on.  The
+unfused comparators (LayerNorm + GEMM; Softmax + GEMM) run in the same process
+on the same inputs.  `cpu_baseline` times the fp64 oracle on a bounded row
+sample of the same workload on this host's cores and extrapolates by work.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "TFLOP/s fused LN→GEMM & softmax→PV, % MFMA peak, speedup vs unfused"
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 flop/clk (dense bf16 MFMA)
+PEAK_F32_TFLOPS = 157.3     # fp32 MFMA / vector
+PEAK_HBM_GBS = 8000.0       # HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="layer",
+                    choices=["layer", "small", "ln_qkv", "causal_softmax_pv", "ffn_prefill",
+                             "ffn_decode_t1", "ffn_decode_t4", "ffn_decode_t16"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=None)
+    return ap.parse_args()
+
+
+# ------------------------------------------------------------------------------ workloads
+def ln_bytes(w) -> float:
+    """Algorithmic bytes of deferred LN->Linear: read x and W' (+c, b), write out."""
+    es = 4 if w.dtype == "f32" else 2
+    return es * (w.M * w.K + w.K * w.N + w.M * w.N) + 8.0 * w.N
+
+
+def sm_bytes(w) -> float:
+    """Algorithmic bytes of deferred Softmax->P.V: the kept scores, V, and the output."""
+    return 2.0 * (w.pairs() + 2.0 * w.BH * w.L * w.d)
+
+
+class LNSite:
+    def __init__(self, ops, I, w):
+        self.w = w
+        self.case = I.make_ln(w)
+        c = self.case
+        self.x = c["x"].cuda()
+        self.W = c["W"].cuda()
+        self.prep = ops.ln_linear_prepare(self.W, c["gamma"].cuda(), c["beta"].cuda(),
+                                          None if c["bias"] is None else c["bias"].cuda())
+        self.out = torch.empty((w.M, w.N), dtype=self.x.dtype, device="cuda")
+        # unfused comparator: static weights pre-transposed once, like W' for the deferred path
+        self.Wt = self.W.t().contiguous()
+        self.g, self.b = c["gamma"].cuda(), c["beta"].cuda()
+        self.bias = None if c["bias"] is None else c["bias"].cuda()
+        self.y = torch.empty_like(self.x)
+        self.ops = ops
+        torch.cuda.synchronize()
+
+    def fused(self):
+        self.ops.ln_linear_deferred(self.x, self.prep, self.w.eps, out=self.out)
+
+    def unfused(self):
+        self.ops.layernorm(self.x, self.g, self.b, self.w.eps, out=self.y)
+        self.ops.gemm(self.y, self.Wt, self.bias, b_layout=1, out=self.out.view(1, self.w.M, self.w.N))
+
+    def flops(self):
+        return self.w.flops()
+
+    def bytes(self):
+        return ln_bytes(self.w)
+
+    def peak_tflops(self):
+        return PEAK_F32_TFLOPS if self.w.dtype == "f32" else PEAK_BF16_TFLOPS
+
+    def oracle_sample(self, oracle, I, threads, rows):
+        idx = I.sample_rows(self.w.M, rows, seed=7)
+        c = self.case
+        xs = c["x"][torch.as_tensor(idx)]
+        t0 = time.perf_counter()
+        oracle.ln_linear(xs, c["gamma"], c["beta"], c["W"], c["bias"], c["eps"], nthreads=threads)
+        dt = time.perf_counter() - t0
+        return dt, len(idx) / self.w.M, f"{len(idx)} of {self.w.M} LayerNorm->Linear rows"
+
+
+class SMSite:
+    def __init__(self, ops, I, w):
+        self.w = w
+        self.case = I.make_sm(w)
+        self.S = self.case["S"].cuda()
+        self.V = self.case["V"].cuda()
+        self.out = torch.empty((w.BH, w.L, w.d), dtype=torch.bfloat16, device="cuda")
+        self.P = torch.empty_like(self.S)
+        self.ops = ops
+        torch.cuda.synchronize()
+
+    def fused(self):
+        self.ops.softmax_pv_deferred(self.S, self.V, causal=self.w.causal, out=self.out)
+
+    def unfused(self):
+        # strongest conventional pair: softmax writes the kept triangle, the GEMM skips masked tiles
+        self.ops.softmax(self.S, causal=2 if self.w.causal else 0, out=self.P)
+        self.ops.gemm(self.P, self.V, a_causal=self.w.causal, out=self.out)
+
+    def unfused_dense(self):
+        # the eager conventional pair: dense probabilities (zeros above the diagonal), dense GEMM
+        self.ops.softmax(self.S, causal=1 if self.w.causal else 0, out=self.P)
+        self.ops.gemm(self.P, self.V, out=self.out)
+
+    def flops(self):
+        return self.w.flops()
+
+    def bytes(self):
+        return sm_bytes(self.w)
+
+    def peak_tflops(self):
+        return PEAK_BF16_TFLOPS
+
+    def oracle_sample(self, oracle, I, threads, rows):
+        w = self.w
+        idx = I.sample_rows(w.BH * w.L, rows, seed=8)
+        head, q = idx // w.L, idx % w.L
+        S_rows = self.case["S"].reshape(w.BH * w.L, w.L)[torch.as_tensor(idx)]
+        t0 = time.perf_counter()
+        oracle.softmax_pv(S_rows, self.case["V"], head=head, qpos=q if w.causal else None, nthreads=threads)
+        dt = time.perf_counter() - t0
+        kept = float(np.sum(q + 1)) if w.causal else float(len(idx) * w.L)
+        return dt, kept / w.pairs(), f"{len(idx)} of {w.BH * w.L} Softmax->P.V rows"
+
+
+def build_sites(ops, I, name):
+    if name == "layer":
+        return [LNSite(ops, I, I.LN_QKV), SMSite(ops, I, I.SM_CAUSAL)], \
+            "llama7b-class layer: LN->QKV x[4096,4096].W[4096,12288] + causal softmax->PV 32h x 8192 x 8192, d128"
+    if name == "small":
+        return [LNSite(ops, I, I.LN_F32_SMALL), SMSite(ops, I, I.SM_BF16_SMALL)], \
+            "small: LN->Linear fp32 x[128,768].W[768,3072] + softmax->PV 12h x 512 x 512, d64"
+    if name == "ln_qkv":
+        return [LNSite(ops, I, I.LN_QKV)], I.LN_QKV.name
+    if name == "causal_softmax_pv":
+        return [SMSite(ops, I, I.SM_CAUSAL)], I.SM_CAUSAL.name
+    if name == "ffn_prefill":
+        return [LNSite(ops, I, I.LN_FFN_PREFILL)], I.LN_FFN_PREFILL.name
+    t = int(name.rsplit("t", 1)[1])
+    w = I.ln_ffn_decode(t)
+    return [LNSite(ops, I, w)], w.name
+
+
+# ------------------------------------------------------------------------------ timing
+def time_steps(fns, steps, warmup):
+    """Run `fns` in order per step; per-fn HIP-event durations and the total, in ms."""
+    for _ in range(warmup):
+        for f in fns:
+            f()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(steps)]
+    t_begin = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_begin.record(stream)
+    for s in range(steps):
+        ev[s][0].record(stream)
+        for i, f in enumerate(fns):
+            f()
+            ev[s][i + 1].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    per = [sum(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(steps)) / steps for i in range(len(fns))]
+    total = t_begin.elapsed_time(t_end) / steps
+    return per, total
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    from paper_2502_17728_amd import inputs as I
+    from paper_2502_17728_amd import ops
+
+    t_setup = time.perf_counter()
+    sites, wl_name = build_sites(ops, I, args.workload)
+    setup_s = time.perf_counter() - t_setup
+
+    per, total = time_steps([s.fused for s in sites], args.steps, args.warmup)
+    flops = sum(s.flops() for s in sites)
+    value = flops / (total * 1e-3) / 1e12
+
+    kernels = {}
+    dom = max(range(len(sites)), key=lambda i: per[i])
+    for i, s in enumerate(sites):
+        name = "ln_linear_deferred" if isinstance(s, LNSite) else "softmax_pv_deferred"
+        tf = s.flops() / (per[i] * 1e-3) / 1e12
+        gbs = s.bytes() / (per[i] * 1e-3) / 1e9
+        k = {"workload": s.w.name, "ms": round(per[i], 4), "tflops": round(tf, 2),
+             "frac_mfma_peak": round(tf / s.peak_tflops(), 4), "gbs": round(gbs, 1),
+             "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "alg_gflop": round(s.flops() / 1e9, 3),
+             "alg_mbytes": round(s.bytes() / 1e6, 2)}
+        if not args.no_unfused:
+            (u,), _ = time_steps([s.unfused], max(3, args.steps // 2), 2)
+            k["unfused_ms"] = round(u, 4)
+            k["speedup_vs_unfused"] = round(u / per[i], 3)
+            if isinstance(s, SMSite) and s.w.causal:
+                (ud,), _ = time_steps([s.unfused_dense], max(3, args.steps // 4), 1)
+                k["unfused_dense_ms"] = round(ud, 4)
+                k["speedup_vs_unfused_dense"] = round(ud / per[i], 3)
+        kernels[name] = k
+
+    d = sites[dom]
+    dname = list(kernels)[dom]
+    hbm_bound = isinstance(d, SMSite) or (isinstance(d, LNSite) and d.w.M <= 16)
+    if hbm_bound:
+        ach = d.bytes() / (per[dom] * 1e-3) / 1e9
+        roof = {"kernel": dname, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+    else:
+        ach = d.flops() / (per[dom] * 1e-3) / 1e12
+        pk = d.peak_tflops()
+        roof = {"kernel": dname, "bound": "mfma", "achieved": round(ach, 2), "peak": pk,
+                "unit": "TFLOP/s", "frac": round(ach / pk, 4), "traffic": None}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))
+        t_cpu, frac_cpu, descs = 0.0, 0.0, []
+        extrap = 0.0
+        for s in sites:
+            rows = 16 if isinstance(s, LNSite) and s.w.K * s.w.N > 1e8 else 64
+            if isinstance(s, LNSite) and s.w.M <= 16:
+                rows = s.w.M
+            if isinstance(s, SMSite):
+                rows = 1024 if s.w.L >= 4096 else 2048
+            dt, frac, desc = s.oracle_sample(oracle, I, threads, rows)
+            extrap += dt / frac
+            descs.append(desc)
+        cpu = {"value": round(flops / extrap / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+               "sample": "; ".join(descs) + f"; time extrapolated by work to the whole step "
+                         f"({extrap:.1f} s per step on {threads} threads)"}
+
+    line = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(total, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32" if all(getattr(s.w, "dtype", "bf16") == "f32" for s in sites) else "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl_name},
+        "roofline": roof, "cpu_baseline": cpu, "kernels": kernels,
+        "frac_mfma_peak_step": round(value / PEAK_BF16_TFLOPS, 4), "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
