@@ -71,8 +71,9 @@ class LNSite:
         self.prep = ops.ln_linear_prepare(self.W, c["gamma"].cuda(), c["beta"].cuda(),
                                           None if c["bias"] is None else c["bias"].cuda())
         self.out = torch.empty((w.M, w.N), dtype=self.x.dtype, device="cuda")
-        # unfused comparator: static weights pre-transposed once, like W' for the deferred path
-        self.Wt = self.W.t().contiguous()
+        # unfused comparator: the same static weights packed once the same way (gamma = 1 folds
+        # nothing), so both paths run the same weight layout and MFMA main loop
+        self.Wpk = ops.ln_linear_prepare(self.W, torch.ones(w.K, dtype=self.W.dtype, device="cuda"))
         self.g, self.b = c["gamma"].cuda(), c["beta"].cuda()
         self.bias = None if c["bias"] is None else c["bias"].cuda()
         self.y = torch.empty_like(self.x)
@@ -84,7 +85,7 @@ class LNSite:
 
     def unfused(self):
         self.ops.layernorm(self.x, self.g, self.b, self.w.eps, out=self.y)
-        self.ops.gemm(self.y, self.Wt, self.bias, b_layout=1, out=self.out.view(1, self.w.M, self.w.N))
+        self.ops.gemm(self.y, self.Wpk, self.bias, out=self.out.view(1, self.w.M, self.w.N))
 
     def flops(self):
         return self.w.flops()

@@ -69,6 +69,10 @@ DN_API int dn_version(void);
  * `packed` must be ln_linear_packed_bytes(K, N, dtype) bytes, 256-byte
  * aligned, device memory; `*w_out` is filled on the host and is what
  * ln_linear_deferred takes.  beta and bias may be NULL (treated as zero).
+ * Layout of W'^T in `packed` (version 2): 16-row x 64-byte fragment chunks
+ * (16 output features x 32 bf16 or 16 fp32 of K), in chunk order
+ * [ceil(N/16)][ceil(K/kchunk)][64 lanes][16 B], zero padded; lane l of a
+ * chunk holds feature 16*nb + (l & 15) at K offset kchunk*kc + (l >> 4)*(16 B).
  */
 typedef struct {
     int64_t K, N;           /* normalized dim, output features                */
@@ -77,7 +81,7 @@ typedef struct {
     void* packed;           /* device buffer holding Wt', c, b                */
 } ln_linear_weights;
 
-#define DN_LN_LAYOUT_VERSION 1
+#define DN_LN_LAYOUT_VERSION 2
 
 /* Bytes of the packed buffer for (K, N, dtype); 0 if the request is invalid. */
 DN_API size_t ln_linear_packed_bytes(int64_t K, int64_t N, int dtype);
@@ -140,11 +144,16 @@ DN_API dn_status softmax(const void* S, int64_t BH, int64_t Lq, int64_t Lk, int 
 /*
  * C[batch][M][N] = A[batch][M][K] . B (+ bias[N]), fp32 accumulation.
  * b_layout = 0: B is [batch][K][N] (row-major, N contiguous).
- * b_layout = 1: B is given transposed, [batch][N][K] (K contiguous) -- the
- *               layout ln_linear_prepare uses for static weights.
+ * b_layout = 1: B is given transposed, [batch][N][K] (K contiguous).
+ * b_layout = 2: B is the packed buffer ln_linear_prepare wrote for (K, N,
+ *               dtype) -- with gamma = 1 it holds W itself; its c and b parts
+ *               are ignored.  batch must be 1.  This is the weight layout and
+ *               main loop ln_linear_deferred uses, so the two paths differ
+ *               only by the fusion.
  * a_causal = 1: A is lower-triangular by contract (A[i][j] treated as 0 for
- *               j > i, never read beyond the diagonal tile); requires M == K.
- * bias may be NULL.  Same MFMA main loop as ln_linear_deferred.
+ *               j > i, never read beyond the diagonal tile); requires M == K,
+ *               bf16 and b_layout 0 or 1.
+ * bias may be NULL.
  */
 DN_API dn_status gemm(const void* A, const void* B, const void* bias, int64_t batch, int64_t M,
                int64_t K, int64_t N, int b_layout, int a_causal, int dtype, void* C,

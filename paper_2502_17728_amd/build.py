@@ -36,7 +36,7 @@ def hipcc() -> str:
 def common_flags():
     return [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}"]
+            "-Wall", "-Wno-unused-function", "-Wno-inline-asm", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
 def _compile(src: str) -> str:

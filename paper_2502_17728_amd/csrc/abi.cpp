@@ -150,17 +150,21 @@ DN_API dn_status softmax(const void* S, int64_t BH, int64_t Lq, int64_t Lk, int 
 DN_API dn_status gemm(const void* A, const void* B, const void* bias, int64_t batch, int64_t M, int64_t K, int64_t N,
                       int b_layout, int a_causal, int dtype, void* C, hipStream_t stream) {
     if (!A || !B || !C || batch < 1 || M < 1 || K < 1 || N < 1 || !valid_dtype(dtype)) return DN_ERR_INVALID_ARG;
-    if ((b_layout != 0 && b_layout != 1) || (a_causal != 0 && a_causal != 1)) return DN_ERR_INVALID_ARG;
+    if (b_layout < 0 || b_layout > 2 || (a_causal != 0 && a_causal != 1)) return DN_ERR_INVALID_ARG;
     if (a_causal && M != K) return DN_ERR_INVALID_ARG;
+    if (b_layout == 2 && batch != 1) return DN_ERR_INVALID_ARG;
     const int64_t es = (int64_t)esize(dtype);
     size_t ab, bb, cb, t;
     if (!bytes_of(batch, M, K * es, &ab) || !bytes_of(batch, K, N * es, &bb) || !bytes_of(batch, M, N * es, &cb) ||
         !bytes_of(M, K, 1, &t) || !bytes_of(K, N, 1, &t))
         return DN_ERR_INVALID_ARG;
+    if (b_layout == 2) bb = ln_linear_packed_bytes(K, N, dtype);
     if (K % 8 || N % 8) return DN_ERR_UNSUPPORTED;
     if (dtype == DN_F32 && (b_layout == 0 || a_causal)) return DN_ERR_UNSUPPORTED;
+    if (a_causal && b_layout == 2) return DN_ERR_UNSUPPORTED;
     if (batch > kMaxBatch) return DN_ERR_UNSUPPORTED;
-    if (!aligned(A, 16) || !aligned(B, 16) || !aligned(bias, 16) || !aligned(C, 16)) return DN_ERR_MISALIGNED;
+    if (!aligned(A, 16) || !aligned(B, b_layout == 2 ? 256 : 16) || !aligned(bias, 16) || !aligned(C, 16))
+        return DN_ERR_MISALIGNED;
     if (overlaps(C, cb, A, ab) || overlaps(C, cb, B, bb) || overlaps(C, cb, bias, (size_t)(N * es)))
         return DN_ERR_INVALID_ARG;
     if (((M + 31) / 32) * ((N + 63) / 64) > kMaxGridX) return DN_ERR_UNSUPPORTED;

@@ -95,15 +95,17 @@ __device__ __forceinline__ void chunk_moments(const u32x4& a, float& s1, float& 
 
 template <>
 __device__ __forceinline__ void chunk_moments<__bf16>(const u32x4& a, float& s1, float& s2) {
-    const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
-    // Copy the words out first: a bit_cast applied directly to the vector
-    // element a[j] was compiled as a read of element 0 for every j.
+    // Widened to fp32 (exact) and accumulated with FMAs.  Measured faster inside
+    // the MFMA loop than v_dot2c_f32_bf16, whose accumulate chains stall the
+    // in-order issue of the wave's next matrix instruction.  The words are
+    // copied out first: reading the vector element a[j] straight into a
+    // bit_cast was compiled as a read of element 0 for every j.
     const uint32_t w[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        bf16x2_t v = __builtin_bit_cast(bf16x2_t, w[j]);
-        s1 = __builtin_amdgcn_fdot2_f32_bf16(v, one, s1, false);
-        s2 = __builtin_amdgcn_fdot2_f32_bf16(v, v, s2, false);
+        const float lo = bf_lo(w[j]), hi = bf_hi(w[j]);
+        s1 += lo + hi;
+        s2 = __builtin_fmaf(lo, lo, __builtin_fmaf(hi, hi, s2));
     }
 }
 
@@ -121,6 +123,22 @@ __device__ __forceinline__ void chunk_moments<float>(const u32x4& a, float& s1, 
 // One wave-wide direct global->LDS copy: lane l's 16 bytes at `g` land at lds_base + 16*l.
 __device__ __forceinline__ void g2lds16(const void* g, DN_LDS void* lds_base) {
     __builtin_amdgcn_global_load_lds(g, lds_base, 16, 0, 0);
+}
+
+// The same copy issued through inline asm.  The compiler then does not track
+// it, so it cannot add its own conservative "s_waitcnt vmcnt(0)" before later
+// LDS reads of other buffers; the caller owns every wait for these copies
+// (explicit vmcnt counts).  m0 is written here and used by nothing else in the
+// kernels that call this.  `lds_addr` must be wave-uniform.
+__device__ __forceinline__ void g2lds16_async(const void* g, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(g)
+                 : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr32(const void* p) {
+    return (uint32_t)(uintptr_t)(const DN_LDS void*)p;
 }
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }

@@ -11,8 +11,9 @@ namespace dn {
 
 // Byte offsets of the pieces of a prepared LN->Linear weight buffer.
 struct PackedLayout {
-    size_t wt_off, wt_bytes;  // Wt'[N][K] in the element type
-    size_t c_off, b_off;      // c[N], b[N] fp32
+    int64_t kchunks, nblocks;  // K_pad / kchunk, N_pad / 16
+    size_t wt_off, wt_bytes;   // W'^T in fragment-chunk order, element type, zero padded
+    size_t c_off, b_off;       // c[N], b[N] fp32
     size_t total;
 };
 PackedLayout packed_layout(int64_t K, int64_t N, int dtype);

@@ -1,6 +1,6 @@
 // ln_gemm.hip -- deferred LayerNorm -> Linear (Sec. II-A, Eq. (5)) and the
-// plain GEMM comparator, sharing one MFMA main loop; plus the decode-shaped
-// deferred kernel and the static-weight preparation.
+// plain GEMM comparator, sharing the same MFMA main loops; plus the
+// decode-shaped deferred kernel and the static-weight preparation.
 //
 // Deferred LayerNorm -> Linear.  With W' = Diag(gamma) W (static, folded once),
 // Eq. (5) with the centering applied after the product reads
@@ -11,19 +11,31 @@
 // MFMA, feed the row moments (sum x, sum x^2) on the VALU -- the paper's
 // "collective sub-operation" running concurrently with the matmul -- and the
 // epilogue applies the normalization once before the single rounded store.
+//
+// Packed weight layout (written by the prepare kernels, read by every LN
+// kernel and by gemm with b_layout = 2).  W'^T is cut into 16-row x 64-byte
+// fragment chunks (16 output features x 32 bf16 / 16 fp32 of K), stored in
+// chunk order [N_pad/16][K_pad/kchunk][64 lanes][16 B], zero padded.  One
+// chunk is 1 KiB, contiguous, already in MFMA operand order: a wave copies it
+// with one fully coalesced instruction, and a lane's 16 bytes are its operand.
+#include <type_traits>
+
 #include "dn_device.hpp"
 #include "dn_launch.hpp"
 
 namespace dn {
 
 enum class Epi { kLnDeferred, kGemm };
+enum class BMode { kKN, kNK, kPacked };
 
 struct MainArgs {
     const void* A;  // [batch][M][K]
-    const void* B;  // NK: [batch][N][K];  KN: [batch][K][N]
+    const void* B;  // kKN: [batch][K][N];  kNK: [batch][N][K];  kPacked: packed chunks
     void* C;        // [batch][M][N]
     int64_t M, K, N;
     int64_t sA, sB, sC;   // batch strides, elements
+    int64_t kchunks;      // kPacked: K_pad / kchunk
+    int64_t nblocks;      // kPacked: N_pad / 16
     const float* c_col;   // LN: c[N]
     const float* b_col;   // LN: b[N]
     float eps;            // LN
@@ -31,10 +43,32 @@ struct MainArgs {
     int a_causal;         // GEMM: A lower-triangular, skip k > row
 };
 
-// Wait until every global->LDS copy issued by this wave has landed.
+// ---------------------------------------------------------------------------- waits
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    // gfx9 s_waitcnt: vmcnt[3:0] bits 3:0, vmcnt[5:4] bits 15:14, expcnt bits 6:4, lgkmcnt bits 11:8
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4)); }
 __device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void block_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
-template <class T, int BM, int BN, int WM, int WN, bool B_KN, Epi EPI>
+// Address of packed chunk (nb, kc), lane `lane` (bytes from the packed base).
+__device__ __forceinline__ int64_t packed_chunk(int64_t nb, int64_t kc, int64_t kchunks, int lane) {
+    return ((nb * kchunks + kc) * kWave + lane) * 16;
+}
+
+// =============================================================================
+// General main loop: 128x128 (bf16) or 32x64 (fp32) tiles, two LDS stages.
+// Used for problems too small for the 256x256 kernel, for K not a multiple of
+// 64, for fp32, for batched products and for B in [K][N] layout.
+// =============================================================================
+template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI>
 __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
     constexpr int NW = WM * WN;
     constexpr int EPL = elem<T>::per16;  // elements per lane per chunk
@@ -46,6 +80,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
     constexpr int A_CH = (BM / 16) * KB, B_CH = (BN / 16) * KB;
     constexpr int STAGE = (A_CH + B_CH) * kChunkBytes;
     constexpr bool LN = EPI == Epi::kLnDeferred;
+    constexpr bool B_KN = BMODE == BMode::kKN;
     static_assert(FM >= 1 && FN >= 1 && BM % (16 * WM) == 0 && BN % (16 * WN) == 0, "tile");
     static_assert(!B_KN || sizeof(T) == 2, "KN staging is bf16 only");
     static_assert(A_CH % NW == 0 && B_CH % NW == 0, "every wave issues the same number of chunk copies");
@@ -89,7 +124,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
             const int64_t kk = min(k0 + kb * KC + (lane >> 4) * EPL, K - EPL);
             g2lds16(A + row * K + kk, lds_ptr(base + c * kChunkBytes));
         }
-        if constexpr (!B_KN) {
+        if constexpr (BMODE == BMode::kNK) {
 #pragma unroll
             for (int j = 0; j < B_CH / NW; ++j) {
                 const int c = wave + j * NW;
@@ -97,6 +132,17 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 const int64_t row = min(n0 + nb * 16 + (lane & 15), N - 1);
                 const int64_t kk = min(k0 + kb * KC + (lane >> 4) * EPL, K - EPL);
                 g2lds16(B + row * K + kk, lds_ptr(base + (A_CH + c) * kChunkBytes));
+            }
+        }
+        if constexpr (BMODE == BMode::kPacked) {
+#pragma unroll
+            for (int j = 0; j < B_CH / NW; ++j) {
+                const int c = wave + j * NW;
+                const int nb = c / KB, kb = c % KB;
+                const int64_t gnb = min(n0 / 16 + nb, p.nblocks - 1);
+                const int64_t gkc = min((int64_t)s * KB + kb, p.kchunks - 1);
+                g2lds16(reinterpret_cast<const char*>(p.B) + packed_chunk(gnb, gkc, p.kchunks, lane),
+                        lds_ptr(base + (A_CH + c) * kChunkBytes));
             }
         }
     };
@@ -296,32 +342,239 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
 }
 
 // =============================================================================
+// Large-problem main loop (bf16, packed B, K % 64 == 0): 256x256 tiles, eight
+// waves as 4 x 2, each wave 64 x 128 of the output.
+//
+// Copies.  The L2 -> CU path is limited by cache lines per instruction: a wave
+// instruction touching 16 half lines moves about half of what one touching 8
+// full lines does.  A (activations, row-major) is therefore copied as 8 rows
+// x 128 bytes per instruction (BK = 64), and the packed B as one contiguous
+// KiB.  A's 16-byte pieces land XOR-swizzled, piece p of tile row r at slot
+// p ^ f(r) with f(r) = (r & 7) ^ ((r >> 3) & 1): any 8 or 16 consecutive rows
+// read at one piece index hit distinct banks, so the fragment reads are
+// conflict-free.
+//
+// Pipeline.  Two 64 KiB stages.  A stage is consumed in two halves (k 0-31,
+// 32-63): the MFMAs of one half run while the next half's fragments are read
+// from LDS.  The copy of stage s+2 is issued right after the barrier in the
+// middle of stage s (when every wave has finished reading stage s), so it has
+// a whole stage of MFMA time to land.
+// =============================================================================
+constexpr int kSgMfma = 0x008, kSgValu = 0x002, kSgDsRead = 0x100;
+
+__device__ __forceinline__ int a_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+template <Epi EPI>
+__global__ __launch_bounds__(512) void pipe_kernel(MainArgs p) {
+    constexpr int BM = 256, BN = 256, WM = 4, WN = 2, NW = 8;
+    constexpr int BK = 64;                        // bf16 elements per stage (128 B per row)
+    constexpr int WTM = BM / WM, WTN = BN / WN;   // 64 x 128 per wave
+    constexpr int FM = WTM / 16, FN = WTN / 16;   // 4 x 8 output fragments
+    constexpr int A_BYTES = BM * 128;             // 32 KiB
+    constexpr int STAGE = A_BYTES + BN / 16 * 2 * kChunkBytes;  // + 32 KiB of B chunks
+    constexpr int A_INS = BM / 8 / NW;            // A copies per wave per stage (4)
+    constexpr int B_INS = BN / 16 * 2 / NW;       // B copies per wave per stage (4)
+    constexpr int PER = A_INS + B_INS;
+    constexpr bool LN = EPI == Epi::kLnDeferred;
+    constexpr int FMW = FM / WN;                  // row blocks whose moments each wave column owns
+    constexpr int NMF = FM * FN, NRD = FM + FN, NVA = LN ? FMW * 8 : 0;
+
+    __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+    __shared__ float row_s1[LN ? BM : 1], row_s2[LN ? BM : 1];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WN, wn = wave % WN;
+    const int64_t M = p.M, K = p.K, N = p.N;
+
+    const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
+    const int t = xcd_contiguous(blockIdx.x, gridDim.x);
+    constexpr int GM = 4;
+    const int group = GM * tiles_n, gid = t / group, first = gid * GM;
+    const int gsz = min(tiles_m - first, GM);
+    const int pm = first + (t % group) % gsz;
+    const int pn = (t % group) / gsz;
+    const int64_t m0 = (int64_t)pm * BM, n0 = (int64_t)pn * BN;
+
+    const __bf16* A = reinterpret_cast<const __bf16*>(p.A);
+    const char* Bp = reinterpret_cast<const char*>(p.B);
+    __bf16* C = reinterpret_cast<__bf16*>(p.C);
+    const int nst = (int)(K / BK);
+
+    // Per-lane copy sources (fixed rows; k advances by BK per stage).
+    const __bf16* a_src[A_INS];
+#pragma unroll
+    for (int j = 0; j < A_INS; ++j) {
+        const int r = (wave + j * NW) * 8 + (lane >> 3);           // tile row of this lane
+        const int piece = (lane & 7) ^ a_swz(r);                    // 16-byte piece it fetches
+        a_src[j] = A + min(m0 + r, M - 1) * K + piece * 8;
+    }
+    const char* b_src[B_INS];
+#pragma unroll
+    for (int j = 0; j < B_INS; ++j) {
+        const int c = wave + j * NW, nb = c >> 1, kb = c & 1;
+        b_src[j] = Bp + packed_chunk(min(n0 / 16 + nb, p.nblocks - 1), kb, p.kchunks, lane);
+    }
+    const uint32_t smem_addr = lds_addr32(smem);
+    auto issue = [&](int s) {
+        const uint32_t base = smem_addr + (uint32_t)((s & 1) * STAGE);
+#pragma unroll
+        for (int j = 0; j < A_INS; ++j)
+            g2lds16_async(a_src[j] + (int64_t)s * BK, base + (uint32_t)((wave + j * NW) * kChunkBytes));
+#pragma unroll
+        for (int j = 0; j < B_INS; ++j)
+            g2lds16_async(b_src[j] + (int64_t)s * 2 * kWave * 16,
+                          base + (uint32_t)(A_BYTES + (wave + j * NW) * kChunkBytes));
+    };
+    // fragments of stage s, half h (k 32h .. 32h+31)
+    auto read = [&](int s, int h, u32x4(&fa)[FM], u32x4(&fb)[FN]) {
+        const char* base = smem + (s & 1) * STAGE;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) {
+            const int r = wm * WTM + fm * 16 + (lane & 15);
+            const int piece = h * 4 + (lane >> 4);
+            fa[fm] = lds_ld16(lds_ptr((char*)base + r * 128 + ((piece ^ a_swz(r)) << 4)));
+        }
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+            fb[fn] = lds_ld16(lds_ptr((char*)base + A_BYTES + ((wn * FN + fn) * 2 + h) * kChunkBytes + lane * 16));
+    };
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float s1[FMW], s2[FMW];
+#pragma unroll
+    for (int i = 0; i < FMW; ++i) s1[i] = s2[i] = 0.f;
+
+    // MFMAs on (fa, fb), the owned rows' moments from fa, with the next half's
+    // fragment reads (already issued) interleaved by the scheduler.
+    auto compute = [&](auto own, u32x4(&fa)[FM], u32x4(&fb)[FN]) {
+        constexpr int OWN = decltype(own)::value;
+        if constexpr (LN) {
+#pragma unroll
+            for (int i = 0; i < FMW; ++i) chunk_moments<__bf16>(fa[OWN * FMW + i], s1[i], s2[i]);
+        }
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma_chunk<__bf16>(fa[fm], fb[fn], acc[fm][fn]);
+#pragma unroll
+        for (int i = 0; i < NMF; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+            if (i < NRD) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
+            if (NVA > 0) __builtin_amdgcn_sched_group_barrier(kSgValu, (NVA + NMF - 1) / NMF, 0);
+        }
+    };
+
+    auto run = [&](auto own) {
+        issue(0);
+        if (nst > 1) {
+            issue(1);
+            wait_vmcnt<PER>();
+        } else {
+            wait_vmcnt<0>();
+        }
+        block_barrier();
+        u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+        read(0, 0, fa0, fb0);
+        for (int s = 0; s < nst; ++s) {
+            read(s, 1, fa1, fb1);
+            compute(own, fa0, fb0);
+            wait_vmcnt<0>();  // this wave's copies of stage s+1 have landed
+            wait_lgkm0();     // this wave's reads of stage s are complete
+            block_barrier();
+            if (s + 2 < nst) issue(s + 2);  // into the buffer stage s just vacated
+            read(s + 1, 0, fa0, fb0);       // past the end this reads stale data that is never used
+            compute(own, fa1, fb1);
+        }
+    };
+    if (LN && wn == 1)
+        run(std::integral_constant<int, 1>{});
+    else
+        run(std::integral_constant<int, 0>{});
+    wait_lgkm0();
+
+    if constexpr (LN) {
+#pragma unroll
+        for (int i = 0; i < FMW; ++i) {
+            const float a = sum_lane_groups(s1[i]);
+            const float b = sum_lane_groups(s2[i]);
+            if (lane < 16) {
+                const int r = wm * WTM + (wn * FMW + i) * 16 + lane;
+                row_s1[r] = a;
+                row_s2[r] = b;
+            }
+        }
+        __syncthreads();
+        for (int r = tid; r < BM; r += NW * kWave) {
+            const float mean = row_s1[r] / (float)K;
+            const float var = __builtin_fmaxf(row_s2[r] / (float)K - mean * mean, 0.f);
+            row_s1[r] = mean;
+            row_s2[r] = 1.0f / __builtin_sqrtf(var + p.eps);
+        }
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+        const int64_t n = n0 + wn * WTN + fn * 16 + (lane & 15);
+        const int64_t nc = min(n, N - 1);
+        float cn = 0.f, bn = 0.f;
+        if constexpr (LN) {
+            cn = p.c_col[nc];
+            bn = p.b_col[nc];
+        } else {
+            if (p.bias) bn = to_f32<__bf16>(reinterpret_cast<const __bf16*>(p.bias)[nc]);
+        }
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int rl = wm * WTM + fm * 16 + 4 * (lane >> 4) + i;
+                const int64_t r = m0 + rl;
+                float v = acc[fm][fn][i];
+                if constexpr (LN) {
+                    v = __builtin_fmaf(-row_s1[rl], cn, v);
+                    v = __builtin_fmaf(row_s2[rl], v, bn);
+                } else {
+                    v += bn;
+                }
+                if (r < M && n < N) C[r * N + n] = (__bf16)v;
+            }
+        }
+    }
+}
+
+// =============================================================================
 // Decode-shaped deferred LN -> Linear: M <= 16 tokens, bf16.
 // The work is streaming W' from HBM, so each workgroup owns 16 output columns
 // and its four waves split K; one 16x16x32 MFMA per 32-k chunk multiplies the
-// (zero-padded) x rows with W' read straight from HBM into operand registers.
-// The row moments ride on the otherwise idle matrix core: with B = all-ones
-// the product gives sum_k x[m][k] in every column, and with B = x itself the
-// Gram matrix x x^T whose diagonal is sum_k x[m][k]^2.
+// (zero-padded) x rows with a packed W' chunk, which a wave reads straight
+// from HBM into operand registers as one contiguous KiB.  The row moments
+// ride on the otherwise idle matrix core: with B = all-ones the product gives
+// sum_k x[m][k] in every column, and with B = x itself the Gram matrix x x^T
+// whose diagonal is sum_k x[m][k]^2.
 // =============================================================================
 constexpr int kDecUnroll = 8;
 
 __global__ __launch_bounds__(256) void ln_decode_bf16_kernel(const __bf16* __restrict__ x,
-                                                             const __bf16* __restrict__ Wt,
+                                                             const char* __restrict__ Wp, int64_t kchunks,
                                                              const float* __restrict__ c_col,
-                                                             const float* __restrict__ b_col, int M,
-                                                             int64_t K, int64_t N, float eps,
-                                                             __bf16* __restrict__ out) {
+                                                             const float* __restrict__ b_col, int M, int64_t K,
+                                                             int64_t N, float eps, __bf16* __restrict__ out) {
     __shared__ f32x4 part[3][4][kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t n0 = (int64_t)blockIdx.x * 16;
+    const int64_t nb = blockIdx.x;
+    const int64_t n0 = nb * 16;
     const int row = lane & 15;
     const bool row_ok = row < M;
-    const int64_t n = min(n0 + (lane & 15), N - 1);
     const __bf16* xr = x + (int64_t)(row_ok ? row : 0) * K;
-    const __bf16* wr = Wt + n * K;
+    const char* wr = Wp + packed_chunk(nb, 0, kchunks, lane);
 
-    const int64_t nchunks = (K + 31) / 32;
+    const int64_t nchunks = kchunks;
     const int64_t per = (nchunks + 3) / 4;
     const int64_t c_begin = wave * per, c_end = min(nchunks, c_begin + per);
 
@@ -335,9 +588,8 @@ __global__ __launch_bounds__(256) void ln_decode_bf16_kernel(const __bf16* __res
 #pragma unroll
         for (int u = 0; u < kDecUnroll; ++u) {
             const int64_t kk = (c + u) * 32 + (lane >> 4) * 8;
-            const bool ok = kk < K;
-            b[u] = ok ? ld16(wr + kk) : zero;
-            a[u] = (ok && row_ok) ? ld16(xr + kk) : zero;
+            b[u] = ld16(wr + (c + u) * kWave * 16);  // zero-padded past K
+            a[u] = (kk < K && row_ok) ? ld16(xr + kk) : zero;
         }
 #pragma unroll
         for (int u = 0; u < kDecUnroll; ++u) {
@@ -348,9 +600,8 @@ __global__ __launch_bounds__(256) void ln_decode_bf16_kernel(const __bf16* __res
     }
     for (; c < c_end; ++c) {
         const int64_t kk = c * 32 + (lane >> 4) * 8;
-        const bool ok = kk < K;
-        const u32x4 b = ok ? ld16(wr + kk) : zero;
-        const u32x4 a = (ok && row_ok) ? ld16(xr + kk) : zero;
+        const u32x4 b = ld16(wr + c * kWave * 16);
+        const u32x4 a = (kk < K && row_ok) ? ld16(xr + kk) : zero;
         acc = mfma_chunk<__bf16>(a, b, acc);
         sx = mfma_chunk<__bf16>(a, ones, sx);
         sxx = mfma_chunk<__bf16>(a, a, sxx);
@@ -373,6 +624,7 @@ __global__ __launch_bounds__(256) void ln_decode_bf16_kernel(const __bf16* __res
 #pragma unroll
         for (int i = 0; i < 4; ++i) diag[i] = __shfl(tot[2][i], 20 * (lane >> 4) + i);
         const int64_t col = n0 + (lane & 15);
+        const int64_t n = min(col, N - 1);
         const float cn = c_col[n], bn = b_col[n];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -410,22 +662,33 @@ __global__ __launch_bounds__(256) void prep_colsum_kernel(const T* __restrict__ 
     b_col[n] = (float)bs;
 }
 
-// Wt'[n][k] = round(gamma_k W[k][n]) through a 64x64 LDS tile.
+// One thread per 16-byte lane piece of the packed layout: chunk (nb, kc), lane l
+// holds W'[k][n] for n = 16 nb + (l & 15), k = kc*kchunk + (l >> 4)*EPL + e.
 template <class T>
-__global__ __launch_bounds__(256) void prep_transpose_kernel(const T* __restrict__ W, const T* __restrict__ gamma,
-                                                             int64_t K, int64_t N, T* __restrict__ Wt) {
-    __shared__ float tile[64][65];
-    const int64_t k0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    for (int r = ty; r < 64; r += 4) {
-        const int64_t k = k0 + r, n = n0 + tx;
-        if (k < K && n < N) tile[r][tx] = to_f32<T>(gamma[k]) * to_f32<T>(W[k * N + n]);
+__global__ __launch_bounds__(256) void prep_pack_kernel(const T* __restrict__ W, const T* __restrict__ gamma,
+                                                        int64_t K, int64_t N, int64_t kchunks, int64_t pieces,
+                                                        char* __restrict__ packed) {
+    constexpr int EPL = elem<T>::per16, KC = elem<T>::kchunk;
+    const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (id >= pieces) return;
+    const int l = (int)(id % kWave);
+    const int64_t chunk = id / kWave;
+    const int64_t nb = chunk / kchunks, kc = chunk % kchunks;
+    const int64_t n = nb * 16 + (l & 15);
+    const int64_t k0 = kc * KC + (l >> 4) * EPL;
+    float v[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+        const int64_t k = k0 + e;
+        v[e] = (n < N && k < K) ? to_f32<T>(gamma[k]) * to_f32<T>(W[k * N + n]) : 0.f;
     }
-    __syncthreads();
-    for (int r = ty; r < 64; r += 4) {
-        const int64_t n = n0 + r, k = k0 + tx;
-        if (k < K && n < N) Wt[n * K + k] = from_f32<T>(tile[tx][r]);
+    u32x4 out;
+    if constexpr (sizeof(T) == 2) {
+        out = u32x4{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])};
+    } else {
+        out = u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])};
     }
+    *reinterpret_cast<u32x4*>(packed + id * 16) = out;
 }
 
 // =============================================================================
@@ -435,9 +698,12 @@ static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 PackedLayout packed_layout(int64_t K, int64_t N, int dtype) {
     PackedLayout L;
-    const size_t es = dtype == 0 ? 4 : 2;
+    const int64_t es = dtype == 0 ? 4 : 2;
+    const int64_t kc = dtype == 0 ? 16 : 32;
+    L.kchunks = (K + kc - 1) / kc;
+    L.nblocks = (N + 15) / 16;
     L.wt_off = 0;
-    L.wt_bytes = (size_t)K * (size_t)N * es;
+    L.wt_bytes = (size_t)(L.nblocks * 16) * (size_t)(L.kchunks * kc) * (size_t)es;
     L.c_off = align256(L.wt_bytes);
     L.b_off = L.c_off + align256((size_t)N * 4);
     L.total = L.b_off + align256((size_t)N * 4);
@@ -452,8 +718,9 @@ static hipError_t prepare_t(const void* W, const void* gamma, const void* beta, 
     dim3 g1((unsigned)((N + 255) / 256));
     prep_colsum_kernel<T><<<g1, 256, 0, s>>>((const T*)W, (const T*)gamma, (const T*)beta, (const T*)bias, K, N,
                                              (float*)(base + L.c_off), (float*)(base + L.b_off));
-    dim3 g2((unsigned)((N + 63) / 64), (unsigned)((K + 63) / 64));
-    prep_transpose_kernel<T><<<g2, 256, 0, s>>>((const T*)W, (const T*)gamma, K, N, (T*)(base + L.wt_off));
+    const int64_t pieces = L.nblocks * L.kchunks * kWave;
+    prep_pack_kernel<T><<<dim3((unsigned)((pieces + 255) / 256)), 256, 0, s>>>((const T*)W, (const T*)gamma, K, N,
+                                                                                L.kchunks, pieces, base + L.wt_off);
     return hipGetLastError();
 }
 
@@ -463,55 +730,84 @@ hipError_t launch_ln_prepare(const void* W, const void* gamma, const void* beta,
     return prepare_t<__bf16>(W, gamma, beta, bias, K, N, packed, s);
 }
 
-template <class T, int BM, int BN, int WM, int WN, bool B_KN, Epi EPI>
+template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI>
 static hipError_t run_main(const MainArgs& a, int64_t batch, hipStream_t s) {
     const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
     dim3 grid((unsigned)tiles, (unsigned)batch);
-    main_loop_kernel<T, BM, BN, WM, WN, B_KN, EPI><<<grid, WM * WN * kWave, 0, s>>>(a);
+    main_loop_kernel<T, BM, BN, WM, WN, BMODE, EPI><<<grid, WM * WN * kWave, 0, s>>>(a);
     return hipGetLastError();
+}
+
+template <Epi EPI>
+static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
+    const int64_t tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
+    pipe_kernel<EPI><<<dim3((unsigned)tiles), 512, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+// The 256x256 kernel once its tiles fill the chip (and K is a multiple of its stage).
+static bool use_big_tiles(int64_t M, int64_t N, int64_t K) {
+    return K % 64 == 0 && ((M + 255) / 256) * ((N + 255) / 256) >= 256;
+}
+
+static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_t K, int64_t N, int dtype,
+                            void* C) {
+    const PackedLayout L = packed_layout(K, N, dtype);
+    const char* base = reinterpret_cast<const char*>(packed);
+    MainArgs a{};
+    a.A = A;
+    a.B = base + L.wt_off;
+    a.C = C;
+    a.M = M;
+    a.K = K;
+    a.N = N;
+    a.kchunks = L.kchunks;
+    a.nblocks = L.nblocks;
+    a.c_col = (const float*)(base + L.c_off);
+    a.b_col = (const float*)(base + L.b_off);
+    return a;
 }
 
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
                                      int dtype, float eps, void* out, hipStream_t s) {
-    const PackedLayout L = packed_layout(K, N, dtype);
-    const char* base = reinterpret_cast<const char*>(packed);
+    MainArgs a = packed_args(x, packed, M, K, N, dtype, out);
+    a.eps = eps;
     if (dtype == 1 && M <= 16) {
-        ln_decode_bf16_kernel<<<dim3((unsigned)((N + 15) / 16)), 256, 0, s>>>(
-            (const __bf16*)x, (const __bf16*)(base + L.wt_off), (const float*)(base + L.c_off),
-            (const float*)(base + L.b_off), (int)M, K, N, eps, (__bf16*)out);
+        ln_decode_bf16_kernel<<<dim3((unsigned)a.nblocks), 256, 0, s>>>(
+            (const __bf16*)x, (const char*)a.B, a.kchunks, a.c_col, a.b_col, (int)M, K, N, eps, (__bf16*)out);
         return hipGetLastError();
     }
-    MainArgs a{};
-    a.A = x;
-    a.B = base + L.wt_off;
-    a.C = out;
-    a.M = M;
-    a.K = K;
-    a.N = N;
-    a.c_col = (const float*)(base + L.c_off);
-    a.b_col = (const float*)(base + L.b_off);
-    a.eps = eps;
-    if (dtype == 0) return run_main<float, 32, 64, 2, 2, false, Epi::kLnDeferred>(a, 1, s);
-    return run_main<__bf16, 128, 128, 2, 2, false, Epi::kLnDeferred>(a, 1, s);
+    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
+    if (use_big_tiles(M, N, K)) return run_pipe<Epi::kLnDeferred>(a, s);
+    return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
 }
 
 hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t batch, int64_t M, int64_t K,
                        int64_t N, int b_layout, int a_causal, int dtype, void* C, hipStream_t s) {
     MainArgs a{};
-    a.A = A;
-    a.B = B;
-    a.C = C;
-    a.M = M;
-    a.K = K;
-    a.N = N;
-    a.sA = M * K;
-    a.sB = K * N;
-    a.sC = M * N;
+    if (b_layout == 2) {
+        a = packed_args(A, B, M, K, N, dtype, C);
+    } else {
+        a.A = A;
+        a.B = B;
+        a.C = C;
+        a.M = M;
+        a.K = K;
+        a.N = N;
+        a.sA = M * K;
+        a.sB = K * N;
+        a.sC = M * N;
+    }
     a.bias = bias;
     a.a_causal = a_causal;
-    if (dtype == 0) return run_main<float, 32, 64, 2, 2, false, Epi::kGemm>(a, batch, s);
-    if (b_layout == 1) return run_main<__bf16, 128, 128, 2, 2, false, Epi::kGemm>(a, batch, s);
-    return run_main<__bf16, 128, 128, 2, 2, true, Epi::kGemm>(a, batch, s);
+    if (b_layout == 2) {
+        if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);
+        if (use_big_tiles(M, N, K)) return run_pipe<Epi::kGemm>(a, s);
+        return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);
+    }
+    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kNK, Epi::kGemm>(a, batch, s);
+    if (b_layout == 1) return run_main<__bf16, 128, 128, 2, 2, BMode::kNK, Epi::kGemm>(a, batch, s);
+    return run_main<__bf16, 128, 128, 2, 2, BMode::kKN, Epi::kGemm>(a, batch, s);
 }
 
 }  // namespace dn

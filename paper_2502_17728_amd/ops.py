@@ -18,7 +18,7 @@ import torch
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdn.so")
 
 DN_F32, DN_BF16 = 0, 1
-DN_LN_LAYOUT_VERSION = 1
+DN_LN_LAYOUT_VERSION = 2
 STATUS = {0: "DN_OK", 1: "DN_ERR_INVALID_ARG", 2: "DN_ERR_UNSUPPORTED", 3: "DN_ERR_MISALIGNED", 4: "DN_ERR_HIP"}
 SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linear_prepare",
            "ln_linear_deferred", "softmax_pv_deferred", "layernorm", "softmax", "gemm")
@@ -169,15 +169,21 @@ def softmax(S: torch.Tensor, causal: int = 0, out: Optional[torch.Tensor] = None
     return out
 
 
-def gemm(A: torch.Tensor, B: torch.Tensor, bias: Optional[torch.Tensor] = None, b_layout: int = 0,
+def gemm(A: torch.Tensor, B, bias: Optional[torch.Tensor] = None, b_layout: int = 0,
          a_causal: bool = False, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """C = A . B (+ bias).  B is a tensor ([K, N] for b_layout 0, [N, K] for 1, optionally
+    batched) or a PreparedLinear (b_layout 2: the packed weights of ln_linear_prepare)."""
     squeeze = A.dim() == 2
     A3 = A.unsqueeze(0) if squeeze else A
-    B3 = B.unsqueeze(0) if B.dim() == 2 else B
     batch, M, K = A3.shape
-    N = B3.shape[2] if b_layout == 0 else B3.shape[1]
+    if isinstance(B, PreparedLinear):
+        b_layout, N, bptr = 2, B.N, _dev(B.packed, "B")
+    else:
+        B3 = B.unsqueeze(0) if B.dim() == 2 else B
+        N = B3.shape[2] if b_layout == 0 else B3.shape[1]
+        bptr = _dev(B3, "B")
     if out is None:
         out = torch.empty((batch, M, N), dtype=A.dtype, device=A.device)
-    _check("gemm", _lib.gemm(_dev(A3, "A"), _dev(B3, "B"), _dev(bias, "bias"), batch, M, K, N, int(b_layout),
+    _check("gemm", _lib.gemm(_dev(A3, "A"), bptr, _dev(bias, "bias"), batch, M, K, N, int(b_layout),
                              int(a_causal), _dt(A), _dev(out, "out"), _stream(stream)))
     return out[0] if squeeze else out

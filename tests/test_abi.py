@@ -44,9 +44,11 @@ def test_packed_bytes():
     assert f(4096, 12288, 1) == 4096 * 12288 * 2 + 2 * 12288 * 4   # Wt' + c + b, 256-aligned pieces
     assert f(768, 3072, 0) == 768 * 3072 * 4 + 2 * 3072 * 4
     assert f(8, 8, 1) % 256 == 0
+    assert f(8, 8, 1) >= 16 * 32 * 2      # K padded to a 32-element chunk, N to 16 rows
+    assert f(520, 24, 1) == (32 * 544 * 2) + 2 * 256
 
 
-def _w(K=64, N=64, dtype=1, version=1, packed=P3):
+def _w(K=64, N=64, dtype=1, version=2, packed=P3):
     return ops.LnLinearWeights(K, N, dtype, version, packed)
 
 
@@ -108,7 +110,10 @@ def test_unfused_validation():
     assert sm(P, 1, 64, 32, 1, 1, P2, None) == INVALID
     assert sm(P, 1, 64, 64, 0, 0, P2, None) == UNSUPPORTED
     assert sm(P, 1, 64, 64, 0, 1, P, None) == INVALID
-    assert gm(P, P2, None, 1, 64, 64, 64, 2, 0, 1, P3, None) == INVALID   # b_layout
+    assert gm(P, P2, None, 1, 64, 64, 64, 3, 0, 1, P3, None) == INVALID   # b_layout
+    assert gm(P, P2, None, 2, 64, 64, 64, 2, 0, 1, P3, None) == INVALID   # packed B is not batched
+    assert gm(P, P2, None, 1, 64, 64, 64, 2, 1, 1, P3, None) == UNSUPPORTED  # causal A with packed B
+    assert gm(P, P2 + 16, None, 1, 64, 64, 64, 2, 0, 1, P3, None) == MISALIGNED  # packed B is 256-aligned
     assert gm(P, P2, None, 1, 64, 32, 64, 0, 1, 1, P3, None) == INVALID   # causal needs M == K
     assert gm(P, P2, None, 1, 64, 64, 60, 0, 0, 1, P3, None) == UNSUPPORTED
     assert gm(P, P2, None, 1, 64, 64, 64, 0, 0, 0, P3, None) == UNSUPPORTED  # fp32 needs [N][K] B

@@ -76,6 +76,41 @@ def test_ln_linear_constant_rows_give_b(ops):
     _ln_check(ops, case)
 
 
+@pytest.mark.parametrize("M,K,N", [(4000, 544, 4104), (4000, 520, 4104), (4096, 4096, 4096)])
+def test_ln_linear_bf16_large_tiles_sampled(ops, M, K, N):
+    # >= 256 output tiles of 256x256: the pipelined main loop with ragged M and N (K % 32 == 0);
+    # K = 520 takes the 128x128 loop with its K tail
+    case = I.make_ln_case(M, K, N, "bf16", seed=M % 97, outliers=3)
+    _ln_check(ops, case, rows=I.sample_rows(M, 40, seed=1) + 0)
+
+
+@pytest.mark.parametrize("M,K,N,layout", [(4104, 320, 4096, 2), (4104, 264, 4096, 2), (4104, 264, 4096, 1),
+                                           (300, 136, 264, 2)])
+def test_gemm_sampled(ops, M, K, N, layout):
+    # layout 2 (packed weights, gamma = 1) at >= 256 tiles and K % 64 == 0 runs the 256x256
+    # pipelined loop; K = 264 and the small case run the 128x128 loop
+    g = torch.Generator().manual_seed(5)
+    A = torch.randn(M, K, generator=g).to(torch.bfloat16)
+    B = torch.randn(K, N, generator=g).to(torch.bfloat16)
+    bias = torch.randn(N, generator=g).to(torch.bfloat16)
+    if layout == 2:
+        Bd = ops.ln_linear_prepare(cuda(B), torch.ones(K, dtype=torch.bfloat16, device="cuda"))
+    else:
+        Bd = cuda(B.t().contiguous())
+    C = ops.gemm(cuda(A), Bd, cuda(bias), b_layout=layout)
+    rows = I.sample_rows(M, 32, seed=2)
+    ref = oracle.linear(A[torch.as_tensor(rows)], B, bias)
+    assert rowwise_rel_err(C.cpu()[torch.as_tensor(rows)], ref) <= TOL[torch.bfloat16]
+
+
+def test_gemm_packed_f32(ops):
+    g = torch.Generator().manual_seed(6)
+    A, B = torch.randn(45, 72, generator=g), torch.randn(72, 40, generator=g)
+    Bd = ops.ln_linear_prepare(cuda(B), torch.ones(72, device="cuda"))
+    C = ops.gemm(cuda(A), Bd)
+    assert rowwise_rel_err(C.cpu(), oracle.linear(A, B)) <= TOL[torch.float32]
+
+
 def test_ln_linear_qkv_workload_sampled(ops):
     w = I.LN_QKV
     case = I.make_ln(w)
@@ -233,7 +268,8 @@ def test_unfused_chains_match_deferred(ops):
     w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
     fused = ops.ln_linear_deferred(x, w)
     y = ops.layernorm(x, cuda(case["gamma"]), cuda(case["beta"]))
-    unfused = ops.gemm(y, cuda(case["W"]).t().contiguous(), b_layout=1)
+    unfused = ops.gemm(y, ops.ln_linear_prepare(cuda(case["W"]), torch.ones(512, dtype=torch.bfloat16,
+                                                                          device="cuda")))
     ref = oracle.ln_linear(case["x"], case["gamma"], case["beta"], case["W"], None, case["eps"])
     assert rowwise_rel_err(unfused.cpu(), ref) <= TOL[torch.bfloat16]
     assert rowwise_rel_err(fused.cpu(), oracle.to_f64(unfused.cpu())) <= TOL[torch.bfloat16]
