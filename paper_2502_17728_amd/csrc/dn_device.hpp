@@ -151,16 +151,29 @@ __device__ __forceinline__ DN_LDS char* lds_ptr(char* p) { return (DN_LDS char*)
 
 // ----------------------------------------------------------------- cross-lane
 // Sum / max over the four lanes that share (l & 15): l, l^16, l^32, l^48.
-__device__ __forceinline__ float sum_lane_groups(float v) {
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 32);
-    return v;
+// v_permlane{16,32}_swap with both operands = v leaves lane l holding the pair
+// {v[l], v[l ^ 16]} (resp. l ^ 32), so one VALU op per level, no LDS traffic.
+// v_max_f32 directly (fmaxf on bit-cast values gets canonicalizing maxes added).
+// The compiler's hazard pass does not guard inline assembly that consumes a
+// just-written VGPR, so the s_nop supplies the wait state a permlane-swap or
+// transcendental result may need.
+__device__ __forceinline__ float vmax2(float a, float b) {
+    float d;
+    asm("s_nop 0\n\tv_max_f32 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
+    return d;
 }
-__device__ __forceinline__ float max_lane_groups(float v) {
-    v = __builtin_fmaxf(v, __shfl_xor(v, 16));
-    v = __builtin_fmaxf(v, __shfl_xor(v, 32));
-    return v;
+__device__ __forceinline__ float xor16_pair_op(float v, bool is_max) {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    const float a = __uint_as_float(p[0]), b = __uint_as_float(p[1]);
+    return is_max ? vmax2(a, b) : a + b;
 }
+__device__ __forceinline__ float xor32_pair_op(float v, bool is_max) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    const float a = __uint_as_float(p[0]), b = __uint_as_float(p[1]);
+    return is_max ? vmax2(a, b) : a + b;
+}
+__device__ __forceinline__ float sum_lane_groups(float v) { return xor32_pair_op(xor16_pair_op(v, false), false); }
+__device__ __forceinline__ float max_lane_groups(float v) { return xor32_pair_op(xor16_pair_op(v, true), true); }
 
 // ----------------------------------------------------------------- 8x8 bf16 transpose
 // in[r] holds 8 bf16 (columns 0..7) of row r; out[c] gets column c (rows 0..7).
