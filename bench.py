@@ -34,6 +34,39 @@ PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 flop/clk (dense bf16 MFMA)
 PEAK_F32_TFLOPS = 157.3     # fp32 MFMA / vector
 PEAK_HBM_GBS = 8000.0       # HBM3E
 
+# HBM traffic per launch, from two rocprofv3 --pmc runs of this script (FETCH_SIZE, then WRITE_SIZE,
+# KiB per dispatch, averaged over the timed launches), each scaled by what the same counter reads for
+# a plain device copy of 1 GiB in the same run (--calib-copy-mib 1024): FETCH_SIZE reads 524311 KiB
+# for its 1048576 KiB (x 1.99994), WRITE_SIZE reads 1048576 KiB (x 1.0).  A figure is only valid for
+# the kernel source it was taken on: each entry carries the sha256 of its kernel's source files, and
+# the bench reports null once they differ.
+KERNEL_SOURCES = {"softmax_pv_deferred": ("softmax_pv.hip", "dn_device.hpp"),
+                  "ln_linear_deferred": ("ln_gemm.hip", "dn_device.hpp")}
+TRAFFIC = {
+    ("softmax_pv_deferred", "causal_softmax_pv_bf16_32x8192x8192_d128"): {
+        "sha256": ("830e39f50b3cb6ed5d8273774baaaf434a22f74e4b0409c59d583f9dbbb9400b",
+                   "c35d8f3810277d81e077facfe856e3842bb3f13625be6e4a3a221ae5265716ef"),
+        "fetch_kib": 1171836, "fetch_scale": 1.99994, "write_kib": 65841, "write_scale": 1.0},
+    ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
+        "sha256": ("53cdcfa75a5a7fe78d29af953808b597f6c1ce75eb14ca21f165ad784c3e3dfb",
+                   "c35d8f3810277d81e077facfe856e3842bb3f13625be6e4a3a221ae5265716ef"),
+        "fetch_kib": 300864, "fetch_scale": 1.99994, "write_kib": 178678, "write_scale": 1.0},
+}
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the counter table, or None when absent or taken on other sources."""
+    import hashlib
+    t = TRAFFIC.get((kernel, workload))
+    if t is None:
+        return None
+    csrc = os.path.join(ROOT, "paper_2502_17728_amd", "csrc")
+    now = tuple(hashlib.sha256(open(os.path.join(csrc, f), "rb").read()).hexdigest()
+                for f in KERNEL_SOURCES[kernel])
+    if now != t["sha256"]:
+        return None
+    return 1024.0 * (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"])
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -46,6 +79,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the timed steps, copy a buffer of this many MiB twice (a plain copy "
+                         "kernel of known size, to scale hardware traffic counters)")
     return ap.parse_args()
 
 
@@ -211,6 +247,13 @@ def main():
     setup_s = time.perf_counter() - t_setup
 
     per, total = time_steps([s.fused for s in sites], args.steps, args.warmup)
+    if args.calib_copy_mib > 0:
+        src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     flops = sum(s.flops() for s in sites)
     value = flops / (total * 1e-3) / 1e12
 
@@ -224,6 +267,8 @@ def main():
              "frac_mfma_peak": round(tf / s.peak_tflops(), 4), "gbs": round(gbs, 1),
              "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "alg_gflop": round(s.flops() / 1e9, 3),
              "alg_mbytes": round(s.bytes() / 1e6, 2)}
+        tr = measured_traffic(name, s.w.name)
+        k["hbm_traffic_mbytes"] = None if tr is None else round(tr / 1e6, 2)
         if not args.no_unfused:
             (u,), _ = time_steps([s.unfused], max(3, args.steps // 2), 2)
             k["unfused_ms"] = round(u, 4)
@@ -240,12 +285,14 @@ def main():
     if hbm_bound:
         ach = d.bytes() / (per[dom] * 1e-3) / 1e9
         roof = {"kernel": dname, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                "traffic": kernels[dname]["hbm_traffic_mbytes"] and round(kernels[dname]["hbm_traffic_mbytes"] * 1e6)}
     else:
         ach = d.flops() / (per[dom] * 1e-3) / 1e12
         pk = d.peak_tflops()
         roof = {"kernel": dname, "bound": "mfma", "achieved": round(ach, 2), "peak": pk,
-                "unit": "TFLOP/s", "frac": round(ach / pk, 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(ach / pk, 4),
+                "traffic": kernels[dname]["hbm_traffic_mbytes"] and round(kernels[dname]["hbm_traffic_mbytes"] * 1e6)}
 
     cpu = None
     if not args.no_cpu_baseline:
