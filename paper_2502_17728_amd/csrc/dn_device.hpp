@@ -137,6 +137,22 @@ __device__ __forceinline__ void g2lds16_async(const void* g, uint32_t lds_addr) 
                  : "memory", "m0");
 }
 
+// Scalar-base form: the wave-uniform 64-bit base sits in SGPRs and each lane
+// supplies only a 32-bit byte offset, which saves two VGPRs and a 64-bit add
+// per copy stream.  `offset` must be below 2^32.
+__device__ __forceinline__ uint64_t uniform_u64(const void* p) {
+    const uint64_t v = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ void g2lds16_async_sb(uint64_t sbase, uint32_t offset, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(offset), "s"(sbase)
+                 : "memory", "m0");
+}
+
 __device__ __forceinline__ uint32_t lds_addr32(const void* p) {
     return (uint32_t)(uintptr_t)(const DN_LDS void*)p;
 }

@@ -401,30 +401,37 @@ __global__ __launch_bounds__(512) void pipe_kernel(MainArgs p) {
     __bf16* C = reinterpret_cast<__bf16*>(p.C);
     const int nst = (int)(K / BK);
 
-    // Per-lane copy sources (fixed rows; k advances by BK per stage).
-    const __bf16* a_src[A_INS];
+    // Copy sources: a wave-uniform base per operand (this tile's first row of
+    // x, its first packed chunk column of W') advanced by one stage at a time,
+    // and fixed per-lane byte offsets from it (rows or chunks; k advances only
+    // the base).  The host guarantees 256 K-element rows and the chunk panel
+    // stay below 4 GiB of offset.
+    uint32_t a_off[A_INS];
 #pragma unroll
     for (int j = 0; j < A_INS; ++j) {
         const int r = (wave + j * NW) * 8 + (lane >> 3);           // tile row of this lane
         const int piece = (lane & 7) ^ a_swz(r);                    // 16-byte piece it fetches
-        a_src[j] = A + min(m0 + r, M - 1) * K + piece * 8;
+        a_off[j] = (uint32_t)(((min(m0 + r, M - 1) - m0) * K + piece * 8) * 2);
     }
-    const char* b_src[B_INS];
+    uint32_t b_off[B_INS];
+    const int64_t nb0 = n0 / 16;
 #pragma unroll
     for (int j = 0; j < B_INS; ++j) {
         const int c = wave + j * NW, nb = c >> 1, kb = c & 1;
-        b_src[j] = Bp + packed_chunk(min(n0 / 16 + nb, p.nblocks - 1), kb, p.kchunks, lane);
+        b_off[j] = (uint32_t)packed_chunk(min(nb0 + nb, p.nblocks - 1) - nb0, kb, p.kchunks, lane);
     }
+    const uint64_t a_base = uniform_u64(A + m0 * K);
+    const uint64_t b_base = uniform_u64(Bp + packed_chunk(nb0, 0, p.kchunks, 0));
     const uint32_t smem_addr = lds_addr32(smem);
     auto issue = [&](int s) {
         const uint32_t base = smem_addr + (uint32_t)((s & 1) * STAGE);
+        const uint64_t ab = a_base + (uint64_t)s * (BK * 2), bb = b_base + (uint64_t)s * (2 * kChunkBytes);
 #pragma unroll
         for (int j = 0; j < A_INS; ++j)
-            g2lds16_async(a_src[j] + (int64_t)s * BK, base + (uint32_t)((wave + j * NW) * kChunkBytes));
+            g2lds16_async_sb(ab, a_off[j], base + (uint32_t)((wave + j * NW) * kChunkBytes));
 #pragma unroll
         for (int j = 0; j < B_INS; ++j)
-            g2lds16_async(b_src[j] + (int64_t)s * 2 * kWave * 16,
-                          base + (uint32_t)(A_BYTES + (wave + j * NW) * kChunkBytes));
+            g2lds16_async_sb(bb, b_off[j], base + (uint32_t)(A_BYTES + (wave + j * NW) * kChunkBytes));
     };
     // fragments of stage s, half h (k 32h .. 32h+31)
     auto read = [&](int s, int h, u32x4(&fa)[FM], u32x4(&fb)[FN]) {
@@ -747,7 +754,9 @@ static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
 
 // The 256x256 kernel once its tiles fill the chip (and K is a multiple of its stage).
 static bool use_big_tiles(int64_t M, int64_t N, int64_t K) {
-    return K % 64 == 0 && ((M + 255) / 256) * ((N + 255) / 256) >= 256;
+    // K < 2^22 keeps the 32-bit copy offsets of a 256-row panel (256 K bf16) and of a
+    // 16-chunk-column W' panel (16 x K/32 KiB) below 4 GiB.
+    return K % 64 == 0 && K < (int64_t(1) << 22) && ((M + 255) / 256) * ((N + 255) / 256) >= 256;
 }
 
 static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_t K, int64_t N, int dtype,
