@@ -377,7 +377,7 @@ __global__ __launch_bounds__(512) void pipe_kernel(MainArgs p) {
     constexpr int PER = A_INS + B_INS;
     constexpr bool LN = EPI == Epi::kLnDeferred;
     constexpr int FMW = FM / WN;                  // row blocks whose moments each wave column owns
-    constexpr int NMF = FM * FN, NRD = FM + FN, NVA = LN ? FMW * 8 : 0;
+    constexpr int NMF = FM * FN, NRD = FM + FN;
 
     __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
     __shared__ float row_s1[LN ? BM : 1], row_s2[LN ? BM : 1];
@@ -472,7 +472,6 @@ __global__ __launch_bounds__(512) void pipe_kernel(MainArgs p) {
         for (int i = 0; i < NMF; ++i) {
             __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
             if (i < NRD) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
-            if (NVA > 0) __builtin_amdgcn_sched_group_barrier(kSgValu, (NVA + NMF - 1) / NMF, 0);
         }
     };
 
@@ -525,33 +524,64 @@ __global__ __launch_bounds__(512) void pipe_kernel(MainArgs p) {
         __syncthreads();
     }
 
+    // Per-lane epilogue operands, loaded once: the column terms c_n, b_n (or
+    // the bias) of the lane's 8 columns and the row terms mean_m, rstd_m of
+    // its 16 rows.
+    const int lc = wn * WTN + (lane & 15), lr = wm * WTM + 4 * (lane >> 4);  // lane's first column / row in the tile
+    float cn[FN], bn[FN];
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
-        const int64_t n = n0 + wn * WTN + fn * 16 + (lane & 15);
-        const int64_t nc = min(n, N - 1);
-        float cn = 0.f, bn = 0.f;
+        const int64_t nc = min(n0 + lc + fn * 16, N - 1);
+        cn[fn] = 0.f;
+        bn[fn] = 0.f;
         if constexpr (LN) {
-            cn = p.c_col[nc];
-            bn = p.b_col[nc];
+            cn[fn] = p.c_col[nc];
+            bn[fn] = p.b_col[nc];
         } else {
-            if (p.bias) bn = to_f32<__bf16>(reinterpret_cast<const __bf16*>(p.bias)[nc]);
+            if (p.bias) bn[fn] = to_f32<__bf16>(reinterpret_cast<const __bf16*>(p.bias)[nc]);
         }
+    }
+    float mu[FM][4], rs[FM][4];
 #pragma unroll
-        for (int fm = 0; fm < FM; ++fm) {
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            mu[fm][i] = LN ? row_s1[lr + fm * 16 + i] : 0.f;
+            rs[fm][i] = LN ? row_s2[lr + fm * 16 + i] : 1.f;
+        }
+    auto value = [&](int fm, int fn, int i) {
+        const float v = acc[fm][fn][i];
+        if constexpr (LN)
+            return __builtin_fmaf(rs[fm][i], __builtin_fmaf(-mu[fm][i], cn[fn], v), bn[fn]);
+        else
+            return v + bn[fn];
+    };
+    if (m0 + BM <= M && n0 + BN <= N) {
+        // whole tile in range: no per-element checks; the row offsets are
+        // uniform (scalar) and the lane's offset from the tile base is fixed
+        // (32 bits: 256 rows of N elements)
+        __bf16* Ct = C + m0 * N + n0;
+        const uint32_t lo = (uint32_t)(lr * N + lc);
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int rl = wm * WTM + fm * 16 + 4 * (lane >> 4) + i;
-                const int64_t r = m0 + rl;
-                float v = acc[fm][fn][i];
-                if constexpr (LN) {
-                    v = __builtin_fmaf(-row_s1[rl], cn, v);
-                    v = __builtin_fmaf(row_s2[rl], v, bn);
-                } else {
-                    v += bn;
-                }
-                if (r < M && n < N) C[r * N + n] = (__bf16)v;
+                __bf16* Cr = Ct + (int64_t)(fm * 16 + i) * N;
+#pragma unroll
+                for (int fn = 0; fn < FN; ++fn) Cr[lo + fn * 16] = (__bf16)value(fm, fn, i);
             }
-        }
+    } else {
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t r = m0 + lr + fm * 16 + i;
+#pragma unroll
+                for (int fn = 0; fn < FN; ++fn) {
+                    const int64_t n = n0 + lc + fn * 16;
+                    if (r < M && n < N) C[r * N + n] = (__bf16)value(fm, fn, i);
+                }
+            }
     }
 }
 

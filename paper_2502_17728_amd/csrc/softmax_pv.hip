@@ -20,16 +20,24 @@
 // product used and keeps the VALU -- the second bottleneck after HBM -- free of
 // the additions.
 //
-// Data movement.  One workgroup owns NW x 32 queries of one head (NW waves of 32).
-// Per step it copies the S tile (BQ rows x 128 bytes, 8 rows of full cache
-// lines per wave instruction) and the V tile (64 keys x d, contiguous in
-// memory, one KiB per instruction) into an NS-deep LDS ring with global->LDS
-// copies issued NS-1 steps ahead.  S pieces are XOR-swizzled (rows of
-// one fragment read hit distinct banks).  V stays in its row-major [key][d]
-// layout, pieces XOR-swizzled per key row, and the V^T operand -- eight
-// consecutive keys of one d per lane -- is read with two transposing LDS reads
-// (ds_read_b64_tr_b16: within a 16-lane group, lane j, slot t receives element
-// j & 3 of the 8 bytes read by lane 4t + (j >> 2)).
+// Data movement.  One workgroup owns NW x QW x 16 queries of one head (NW
+// waves, QW 16-query fragments each) and walks the keys in steps of 64.
+// Scores are private to a wave, so each wave streams its own rows into a
+// ring of PF LDS slots that only it reads: global->LDS copies of whole
+// 128-byte lines (8 rows per instruction), 16-byte pieces XOR-swizzled so that
+// the fragment reads are bank-conflict free, and no barrier.  V is shared by
+// all waves and goes through an NS-slot ring with one barrier per step; it
+// stays in its row-major [key][d] layout, pieces XOR-swizzled per key row, and
+// the V^T operand -- eight consecutive keys of one d per lane -- is read with
+// two transposing LDS reads (ds_read_b64_tr_b16: within a 16-lane group, lane
+// j, slot t receives element j & 3 of the 8 bytes read by lane 4t + (j >> 2)).
+// Every copy is issued from inline assembly and waited on with hand-counted
+// vmcnt values.
+//
+// Schedule.  Iteration s issues the products of step s (numerators computed in
+// iteration s-1) and computes the numerators of step s+1: independent work in
+// one basic block, which the compiler interleaves, so the exponentials of one
+// step run beside the matrix instructions of the previous one.
 #include <type_traits>
 
 #include "dn_device.hpp"
@@ -46,6 +54,14 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4)); }
+// vmcnt wait that also orders the compiler's memory operations: every memory
+// operation of the main loop is issued from inline assembly, so every wait on
+// them is written by hand.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_asm() {
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 __device__ __forceinline__ void block_barrier() {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
@@ -58,15 +74,6 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
     float d;
     asm("v_max3_f32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
     return d;
-}
-// Scale a 4-float accumulator in place (tied operands keep it in its registers).
-// alpha is the result of v_exp_f32; a transcendental result needs one wait
-// state before a non-transcendental VALU reads it, and the compiler's hazard
-// pass does not insert it in front of inline assembly -- hence the s_nop.
-__device__ __forceinline__ void scale_inplace(f32x4& a, float alpha) {
-    asm volatile("s_nop 0\n\tv_mul_f32 %0, %0, %4\n\tv_mul_f32 %1, %1, %4\n\tv_mul_f32 %2, %2, %4\n\tv_mul_f32 %3, %3, %4"
-                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3])
-                 : "v"(alpha));
 }
 __device__ __forceinline__ int s_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }  // 128-byte S rows
 // V pieces: the transposing read is serviced 32 lanes at a time, covering 8 key
@@ -86,29 +93,33 @@ __device__ __forceinline__ uint2 lds_tr16(const char* p) {
 }
 }  // namespace sm
 
-template <int D, int NW, int NS>
+template <int D, int NW, int QW, int NS, int PF>
 __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __restrict__ S,
                                                          const __bf16* __restrict__ V, int BH,
                                                          int64_t Lq, int64_t Lk, int causal, int nqb,
                                                          __bf16* __restrict__ out) {
     using namespace sm;
-    constexpr int QW = 2;                  // 16-query fragments per wave
-    constexpr int BQ = NW * QW * 16;       // queries per workgroup
+    constexpr int BQ = NW * QW * 16;       // queries per workgroup (QW 16-query fragments per wave)
     constexpr int BKV = 64;                // keys per step
-    constexpr int S_BYTES = BQ * BKV * 2;
     constexpr int VROW = D * 2;            // bytes per V row
-    constexpr int V_BYTES = BKV * VROW;
-    constexpr int STAGE = S_BYTES + V_BYTES;
-    constexpr int S_INS = BQ / 8 / NW;     // S copies per wave per step
-    constexpr int V_INS = V_BYTES / kChunkBytes / NW;
-    constexpr int PER = S_INS + V_INS;
+    constexpr int V_BYTES = BKV * VROW;    // one V ring slot
+    constexpr int V_INS = V_BYTES / kChunkBytes / NW;  // V copies per wave per step
+    constexpr int WROWS = QW * 16;         // score rows per wave
+    constexpr int S_SLOT = WROWS * BKV * 2;  // one step of a wave's scores
+    constexpr int S_LD = WROWS / 8;        // S copies per wave per step (8 rows x 128 B each)
     constexpr int VPR = VROW / 16;         // 16-byte pieces per V row
     constexpr int VRPI = kChunkBytes / VROW;  // V rows per copy instruction
     constexpr int DB = D / 16;
     static_assert(V_BYTES % (kChunkBytes * NW) == 0, "V tile split evenly over the waves");
-    static_assert(NS == 2 || NS == 3, "ring depth");
+    static_assert(NS >= 2 && NS <= 4 && PF >= 2 && PF >= NS - 2 && PF <= NS, "ring depths the counts assume");
+    // Memory-op order per iteration j: [top] V copies of step j+NS-1, [middle] S copies of step
+    // j+1+PF.  At the top of iteration s the wave needs S(s+1) and V(s); the ops issued after each:
+    constexpr int AFTER_S = (PF - 1) * (V_INS + S_LD);
+    constexpr int AFTER_V = S_LD + (NS - 2) * (V_INS + S_LD);
+    constexpr int WAIT_N = AFTER_S < AFTER_V ? AFTER_S : AFTER_V;
+    constexpr int AHEAD = PF + 1 > NS - 1 ? PF + 1 : NS - 1;  // prologue length
 
-    __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
+    __shared__ __attribute__((aligned(1024))) char smem[NS * V_BYTES + NW * PF * S_SLOT];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -124,20 +135,59 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     const __bf16* Vh = V + (int64_t)h * Lk * D;
     __bf16* Oh = out + (int64_t)h * Lq * D;
 
-    const int64_t qw0 = q0 + wave * QW * 16;  // first query of this wave
+    const int64_t qw0 = q0 + wave * WROWS;  // first query of this wave
+    const int G = lane >> 4, i = lane & 15;
     int64_t qrow[QW];
 #pragma unroll
-    for (int f = 0; f < QW; ++f) qrow[f] = qw0 + f * 16 + (lane & 15);
+    for (int f = 0; f < QW; ++f) qrow[f] = qw0 + f * 16 + i;
+    const uint32_t smem_addr = lds_addr32(smem);
 
-    // ---- copy sources.  S: instruction i covers tile rows 8i..8i+7; V: piece i covers rows VRPI*i..
-    const __bf16* s_row[S_INS];
-    int s_piece[S_INS];
+    // ---- S: each score row belongs to one wave, so it goes through a ring
+    // private to that wave (PF steps deep) and needs no barrier.  Copies move
+    // whole 128-byte lines (8 rows per instruction); lane l fetches piece
+    // (l & 7) ^ s_swz(row) of row 8j + (l >> 3), so piece c of a row sits in
+    // 16-byte slot c ^ s_swz(row), which makes the fragment reads below
+    // bank-conflict free.  Offsets from the head's base fit 32 bits
+    // (Lq * Lk <= 2^31).  Keys past the last one this wave needs (causal
+    // diagonal, Lk, or steps past the end) are clamped onto its last 8-key
+    // group, lines it has just read: every step issues the same copies (the
+    // wait counts rely on it) and skipped work costs no memory traffic.
+    const int64_t kend_w = causal ? min(kv_end, qw0 + WROWS) : kv_end;  // exclusive, multiple of 8
+    const uint64_t s_base = uniform_u64(Sh);
+    uint32_t s_row[S_LD], s_p8[S_LD];
 #pragma unroll
-    for (int j = 0; j < S_INS; ++j) {
-        const int r = (wave + j * NW) * 8 + (lane >> 3);
-        s_piece[j] = (lane & 7) ^ s_swz(r);
-        s_row[j] = Sh + min(q0 + r, Lq - 1) * Lk;
+    for (int j = 0; j < S_LD; ++j) {
+        const int r = 8 * j + (lane >> 3);
+        const int64_t q = qw0 + r < Lq ? qw0 + r : Lq - 1;
+        s_row[j] = (uint32_t)(q * Lk * 2);
+        s_p8[j] = (uint32_t)(((lane & 7) ^ s_swz(r)) * 8);
     }
+    const uint32_t s_lds = smem_addr + (uint32_t)(NS * V_BYTES + wave * PF * S_SLOT);
+    const uint32_t klast = (uint32_t)(kend_w - 8);  // the wave's last 8-key group
+    auto issue_s = [&](int step) {
+        const uint32_t dst = s_lds + (uint32_t)((step % PF) * S_SLOT);
+        const uint32_t k0 = (uint32_t)step * BKV;
+#pragma unroll
+        for (int j = 0; j < S_LD; ++j) {
+            const uint32_t key = k0 + s_p8[j] < klast ? k0 + s_p8[j] : klast;  // a select, no branch
+            g2lds16_async_sb(s_base, s_row[j] + key * 2u, dst + j * kChunkBytes);
+        }
+    };
+    // fragment reads: lane (i, G) takes row 16f + i, piece 4kc + G (8 keys), the B-operand order
+    int s_rd[2];
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) s_rd[kc] = i * 128 + (((4 * kc + G) ^ s_swz(i)) << 4);
+    const char* s_ring = smem + NS * V_BYTES + wave * PF * S_SLOT;
+    auto read_s = [&](int step, u32x4(&r)[QW][2]) {
+        const char* b = s_ring + (step % PF) * S_SLOT;
+#pragma unroll
+        for (int f = 0; f < QW; ++f)
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) r[f][kc] = lds_ld16(lds_ptr((char*)b + f * 16 * 128 + s_rd[kc]));
+    };
+
+    // ---- V: shared by every wave, so it goes through an NS-deep ring with a
+    // barrier per step (copy instruction j covers key rows VRPI*(wave + j*NW) ..).
     int v_row[V_INS], v_piece[V_INS];
 #pragma unroll
     for (int j = 0; j < V_INS; ++j) {
@@ -145,20 +195,14 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
         v_row[j] = r;
         v_piece[j] = (lane % VPR) ^ v_swz<D>(r);
     }
-    const uint32_t smem_addr = lds_addr32(smem);
-    auto issue = [&](int step) {
-        const uint32_t base = smem_addr + (uint32_t)((step % NS) * STAGE);
+    auto issue_v = [&](int step) {
+        const uint32_t base = smem_addr + (uint32_t)((step % NS) * V_BYTES);
         const int64_t k0 = (int64_t)step * BKV;
-        const bool tail = k0 + BKV > Lk;  // only the last step of a ragged key range needs clamping
-#pragma unroll
-        for (int j = 0; j < S_INS; ++j) {
-            const int64_t key = tail ? min(k0 + s_piece[j] * 8, Lk - 8) : k0 + s_piece[j] * 8;
-            g2lds16_async(s_row[j] + key, base + (uint32_t)((wave + j * NW) * kChunkBytes));
-        }
+        const bool tail = k0 + BKV > Lk;  // only the last steps of a key range need clamping
 #pragma unroll
         for (int j = 0; j < V_INS; ++j) {
             const int64_t key = tail ? min(k0 + v_row[j], Lk - 1) : k0 + v_row[j];
-            g2lds16_async(Vh + key * D + v_piece[j] * 8, base + (uint32_t)(S_BYTES + (wave + j * NW) * kChunkBytes));
+            g2lds16_async(Vh + key * D + v_piece[j] * 8, base + (uint32_t)((wave + j * NW) * kChunkBytes));
         }
     };
 
@@ -171,19 +215,9 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     }
     const u32x4 ones = {0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
 
-#pragma unroll
-    for (int st = 0; st < NS - 1; ++st)
-        if (st < nsteps) issue(st);
-
-    // Lane-constant LDS offsets.  The S swizzle depends only on the row's low 4
-    // bits (lane & 15); the V swizzle only on bits of (8G + (i >> 2)), which the
-    // chunk (kc) and half (hh) offsets leave unchanged.  The per-step parts are
-    // uniform and fold into the instructions' immediate offsets.
-    const int G = lane >> 4, i = lane & 15;
-    int s_off[2];
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc)
-        s_off[kc] = (wave * QW * 16 + i) * 128 + (((kc * 4 + G) ^ s_swz(i)) << 4);
+    // Lane-constant LDS offsets of the V^T fragments.  The V swizzle depends
+    // only on bits of (8G + (i >> 2)), which the chunk (kc) and half offsets
+    // leave unchanged; the per-step parts are uniform.
     const int vsw2 = v_swz<D>(8 * G + (i >> 2)) >> 1;  // even swizzle, applied to the 32-byte d block
     int v_off[DB];
 #pragma unroll
@@ -198,63 +232,23 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
 #pragma unroll
     for (int f = 0; f < QW; ++f) mref[f] = -__builtin_inff();
 
-    for (int step = 0; step < nsteps; ++step) {
-        // this wave's copies of this step have landed (later steps may still be in flight)
-        if (NS > 2 && step + 1 < nsteps)
-            wait_vmcnt<(NS > 2 ? PER : 0)>();
-        else
-            wait_vmcnt<0>();
-        wait_lgkm0();  // this wave's reads of the previous step are complete
-        block_barrier();
-        if (step + NS - 1 < nsteps) issue(step + NS - 1);  // into the buffer the previous step vacated
-
-        const int64_t k0 = (int64_t)step * BKV;
-        // this wave has work unless every key of the step lies above all of its queries
-        if (causal && k0 > qw0 + QW * 16 - 1) continue;
-        const char* sb = smem + (step % NS) * STAGE;
-        const char* vb = sb + S_BYTES;
-
-        u32x4 sraw[QW][2];
-#pragma unroll
-        for (int f = 0; f < QW; ++f)
-#pragma unroll
-            for (int kc = 0; kc < 2; ++kc) sraw[f][kc] = lds_ld16(lds_ptr((char*)sb + s_off[kc] + f * 16 * 128));
-        // V^T fragments (A operand) of key chunk kc: two transposing reads of 4 keys per d block
-        auto read_v = [&](int kc, u32x4(&vf)[DB]) {
-#pragma unroll
-            for (int b = 0; b < DB; ++b) {
-                const uint2 lo = lds_tr16(vb + v_off[b] + (kc * 32) * VROW);
-                const uint2 hi = lds_tr16(vb + v_off[b] + (kc * 32 + 4) * VROW);
-                vf[b] = u32x4{lo.x, lo.y, hi.x, hi.y};
-            }
-        };
-        u32x4 vf0[DB], vf1[DB];
-        read_v(0, vf0);  // in flight during the softmax arithmetic below
-        __builtin_amdgcn_sched_barrier(0);
-
-        const bool edge = (causal && k0 + BKV - 1 > qw0) || k0 + BKV > kv_end;
-        u32x4 pf[QW][2];
+    // Numerators of one step: bf16 exp2(s log2e - mref) in the B-operand order,
+    // with the reference raised where the step's maximum requires it; alpha is
+    // the factor the partial sums must take to follow (1 where unchanged).
+    // Masked keys arrive as -inf scores (mask_scores) and yield zeros.
+    auto numerators = [&](const u32x4(&sc)[QW][2], u32x4(&pfo)[QW][2], float(&alpha)[QW]) {
+        bool raised = false;
 #pragma unroll
         for (int f = 0; f < QW; ++f) {
             float sv[2][8];
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
-                const uint32_t w[4] = {sraw[f][kc].x, sraw[f][kc].y, sraw[f][kc].z, sraw[f][kc].w};
+                const uint32_t w[4] = {sc[f][kc].x, sc[f][kc].y, sc[f][kc].z, sc[f][kc].w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     sv[kc][2 * e] = bf_lo(w[e]);
                     sv[kc][2 * e + 1] = bf_hi(w[e]);
                 }
-            }
-            if (edge) {  // keys beyond the row (causal) or beyond Lk are not part of it
-                const int64_t last = causal ? (qrow[f] < kv_end - 1 ? qrow[f] : kv_end - 1) : kv_end - 1;
-                const int64_t rel = last - k0;  // last kept key, relative to the step
-                const int lim = rel < 0 ? -1 : (rel > BKV ? BKV : (int)rel);
-#pragma unroll
-                for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (kc * 32 + G * 8 + e > lim) sv[kc][e] = -__builtin_inff();
             }
             // balanced max tree over the lane's 16 scores, then across the 4 lanes of the query
             const float m0 = max3f(sv[0][0], sv[0][1], sv[0][2]), m1 = max3f(sv[0][3], sv[0][4], sv[0][5]);
@@ -263,47 +257,138 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
             const float tmax = max3f(max3f(m0, m1, m2), max3f(m3, m4, sv[1][7]), m0);
             const float tmax2 = max_lane_groups(tmax) * kLog2e;
             const bool raise = tmax2 > mref[f] + 8.0f;
-            if (__any(raise)) {
-                const float mnew = raise ? tmax2 : mref[f];
-                const float alpha = __builtin_amdgcn_exp2f(mref[f] - mnew);  // 1 if unchanged, 0 from -inf
-#pragma unroll
-                for (int b = 0; b < DB; ++b) scale_inplace(acc[f][b], alpha);
-                scale_inplace(accl[f], alpha);
-                mref[f] = mnew;
-            }
-            const float nb = mref[f] == -__builtin_inff() ? 0.f : -mref[f];
+            const float mnew = raise ? tmax2 : mref[f];
+            // the select keeps -inf - -inf out of exp2 for rows that have not started
+            alpha[f] = __builtin_amdgcn_exp2f(raise ? mref[f] - mnew : 0.f);
+            mref[f] = mnew;
+            raised |= raise;
+            const float nb = mnew == -__builtin_inff() ? 0.f : -mnew;
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[kc][2 * e], kLog2e, nb));
                     const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[kc][2 * e + 1], kLog2e, nb));
-                    pf[f][kc][e] = pack_bf16(p0, p1);
+                    pfo[f][kc][e] = pack_bf16(p0, p1);
                 }
         }
-        __builtin_amdgcn_sched_barrier(0);
-        read_v(1, vf1);  // in flight during chunk 0's products
+        return raised;
+    };
+    // Keys beyond the row (causal) or beyond Lk are not part of it: their raw
+    // bf16 scores are replaced by -inf (0xff80), two per word.  A step wholly
+    // above a wave's queries, or past the last step, is masked entirely.
+    auto mask_scores = [&](int step, u32x4(&sc)[QW][2]) {
+        const int64_t k0 = (int64_t)step * BKV;
 #pragma unroll
-        for (int b = 0; b < DB; ++b)
+        for (int f = 0; f < QW; ++f) {
+            const int64_t last = causal ? (qrow[f] < kv_end - 1 ? qrow[f] : kv_end - 1) : kv_end - 1;
+            const int64_t rel = last - k0;  // last kept key, relative to the step
+            const int lim = rel < 0 ? -1 : (rel > BKV ? BKV : (int)rel);
 #pragma unroll
-            for (int f = 0; f < QW; ++f) acc[f][b] = mfma_chunk<__bf16>(vf0[b], pf[f][0], acc[f][b]);
+            for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-        for (int f = 0; f < QW; ++f) accl[f] = mfma_chunk<__bf16>(ones, pf[f][0], accl[f]);
+                for (int e = 0; e < 4; ++e) {
+                    const int k = kc * 32 + G * 8 + 2 * e;  // key of the low half
+                    const uint32_t m = (k > lim ? 0x0000ffffu : 0u) | (k + 1 > lim ? 0xffff0000u : 0u);
+                    sc[f][kc][e] = (sc[f][kc][e] & ~m) | (0xff80ff80u & m);
+                }
+        }
+    };
+    auto is_edge = [&](int step) {
+        const int64_t k0 = (int64_t)step * BKV;
+        return (causal && k0 + BKV - 1 > qw0) || k0 + BKV > kv_end;
+    };
+
+    // Prologue: the copies of iterations -AHEAD .. -1 in the steady-state
+    // order (iteration j issues, at its top, the V copies of step j+NS-1 and,
+    // after its numerators, the S copies of step j+1+PF), with the numerators
+    // of step 0 computed in iteration -1.
 #pragma unroll
-        for (int b = 0; b < DB; ++b)
-#pragma unroll
-            for (int f = 0; f < QW; ++f) acc[f][b] = mfma_chunk<__bf16>(vf1[b], pf[f][1], acc[f][b]);
-#pragma unroll
-        for (int f = 0; f < QW; ++f) accl[f] = mfma_chunk<__bf16>(ones, pf[f][1], accl[f]);
+    for (int j = -AHEAD; j < -1; ++j) {
+        if (j + NS - 1 >= 0) issue_v(j + NS - 1);
+        if (j + 1 + PF >= 0) issue_s(j + 1 + PF);
     }
-    wait_vmcnt<0>();
+    issue_v(NS - 2);
+    wait_vmcnt_asm<(PF - 1) * S_LD>();  // S(0) is complete once only the later S copies may remain
+    u32x4 pf[QW][2];
+    float alpha[QW];
+    bool raised;
+    {
+        u32x4 sc[QW][2];
+        read_s(0, sc);
+        if (is_edge(0)) mask_scores(0, sc);
+        numerators(sc, pf, alpha);
+    }
+    raised = false;  // the partial sums are still zero: nothing to rescale
+    issue_s(PF);     // into the slot step 0 vacated
+
+    // Iteration s: the products of step s (V(s) from the ring, numerators
+    // computed one iteration earlier) and, independent of them, the numerators
+    // of step s+1 -- one basic block, so the scheduler interleaves the matrix
+    // instructions with the exponentials.  When step s's numerators raised the
+    // reference, the partial sums follow it first (a rare branch ahead of the
+    // block).
+    for (int s = 0; s < nsteps; ++s) {
+        wait_vmcnt_asm<WAIT_N>();  // S(s+1) and this wave's V copies of step s are complete
+        wait_lgkm0();              // this wave's LDS reads of step s-1 are complete
+        block_barrier();
+        issue_v(s + NS - 1);  // into the slot step s-1 vacated
+        if (__any(raised)) {
+#pragma unroll
+            for (int f = 0; f < QW; ++f) {
+#pragma unroll
+                for (int b = 0; b < DB; ++b) acc[f][b] *= alpha[f];
+                accl[f] *= alpha[f];
+            }
+        }
+        u32x4 sc[QW][2];
+        read_s(s + 1, sc);
+        if (is_edge(s + 1)) mask_scores(s + 1, sc);
+        const char* vb = smem + (s % NS) * V_BYTES;
+        // V^T fragments of key chunk kc (A operand): two transposing reads of 4 keys per d block
+        auto read_v = [&](int kc, u32x4(&vf)[DB]) {
+#pragma unroll
+            for (int b = 0; b < DB; ++b) {
+                const uint2 lo = lds_tr16(vb + v_off[b] + (kc * 32) * VROW);
+                const uint2 hi = lds_tr16(vb + v_off[b] + (kc * 32 + 4) * VROW);
+                vf[b] = u32x4{lo.x, lo.y, hi.x, hi.y};
+            }
+        };
+        auto products = [&](int kc, const u32x4(&vf)[DB]) {
+#pragma unroll
+            for (int b = 0; b < DB; ++b)
+#pragma unroll
+                for (int f = 0; f < QW; ++f) acc[f][b] = mfma_chunk<__bf16>(vf[b], pf[f][kc], acc[f][b]);
+#pragma unroll
+            for (int f = 0; f < QW; ++f) accl[f] = mfma_chunk<__bf16>(ones, pf[f][kc], accl[f]);
+        };
+        u32x4 pfn[QW][2];
+        {
+            u32x4 vf[DB];
+            read_v(0, vf);
+            raised = numerators(sc, pfn, alpha);
+            issue_s(s + 1 + PF);  // the slot of S(s+1) has been read
+            products(0, vf);
+        }
+        {
+            u32x4 vf[DB];
+            read_v(1, vf);
+            products(1, vf);
+        }
+#pragma unroll
+        for (int f = 0; f < QW; ++f) {
+            pf[f][0] = pfn[f][0];
+            pf[f][1] = pfn[f][1];
+        }
+    }
+    wait_vmcnt_asm<0>();  // no copy into LDS may outlive the workgroup
 
     // ---- epilogue: the single deferred division, one rounding to bf16
 #pragma unroll
     for (int f = 0; f < QW; ++f) {
         if (qrow[f] >= Lq) continue;
         const float inv = 1.0f / accl[f][0];
-        __bf16* orow = Oh + qrow[f] * D + 4 * (lane >> 4);
+        __bf16* orow = Oh + qrow[f] * D + 4 * G;
 #pragma unroll
         for (int b = 0; b < DB; ++b) {
             uint2 v;
@@ -314,26 +399,27 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     }
 }
 
-template <int D, int NW, int NS>
+template <int D, int NW, int QW, int NS, int PF>
 static hipError_t run_softmax_pv(const void* S, const void* V, int64_t BH, int64_t Lq, int64_t Lk, int causal,
                                  void* out, hipStream_t s) {
-    constexpr int BQ = NW * 32;
+    constexpr int BQ = NW * QW * 16;
     const int nqb = (int)((Lq + BQ - 1) / BQ);
     dim3 grid((unsigned)(BH * nqb));
-    softmax_pv_kernel<D, NW, NS><<<grid, NW * 64, 0, s>>>((const __bf16*)S, (const __bf16*)V, (int)BH, Lq, Lk, causal,
-                                                          nqb, (__bf16*)out);
+    softmax_pv_kernel<D, NW, QW, NS, PF><<<grid, NW * 64, 0, s>>>((const __bf16*)S, (const __bf16*)V, (int)BH, Lq,
+                                                                  Lk, causal, nqb, (__bf16*)out);
     return hipGetLastError();
 }
 
-// 8 waves x 32 queries and a two-stage ring: 80 KiB (d = 64) or 96 KiB (d = 128)
-// of LDS, one workgroup per CU; measured faster than 4 waves or three stages
-// on the causal 32 x 8192 x 128 workload.
-constexpr int kSmWaves = 8, kSmStages = 2;
+// 8 waves x 2 fragments (256 queries per workgroup), two V slots and two S
+// slots per wave: 64 KiB (d = 64) or 96 KiB (d = 128) of LDS.  Deeper rings
+// measured no faster on the causal 32 x 8192 x 8192, d = 128 workload.
+constexpr int kSmWaves = 8, kSmFrags = 2, kSmStages = 2, kSmPrefetch = 2;
 
 hipError_t launch_softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq, int64_t Lk, int64_t d,
                                       int causal, void* out, hipStream_t s) {
-    if (d == 64) return run_softmax_pv<64, kSmWaves, kSmStages>(S, V, BH, Lq, Lk, causal, out, s);
-    return run_softmax_pv<128, kSmWaves, kSmStages>(S, V, BH, Lq, Lk, causal, out, s);
+    if (d == 64)
+        return run_softmax_pv<64, kSmWaves, kSmFrags, kSmStages, kSmPrefetch>(S, V, BH, Lq, Lk, causal, out, s);
+    return run_softmax_pv<128, kSmWaves, kSmFrags, kSmStages, kSmPrefetch>(S, V, BH, Lq, Lk, causal, out, s);
 }
 
 }  // namespace dn
