@@ -18,6 +18,7 @@
 // chunk order [N_pad/16][K_pad/kchunk][64 lanes][16 B], zero padded.  One
 // chunk is 1 KiB, contiguous, already in MFMA operand order: a wave copies it
 // with one fully coalesced instruction, and a lane's 16 bytes are its operand.
+#include <algorithm>
 #include <type_traits>
 
 #include "dn_device.hpp"
@@ -360,12 +361,12 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
 // middle of stage s (when every wave has finished reading stage s), so it has
 // a whole stage of MFMA time to land.
 // =============================================================================
-constexpr int kSgMfma = 0x008, kSgValu = 0x002, kSgDsRead = 0x100;
+constexpr int kSgMfma = 0x008, kSgDsRead = 0x100;
 
 __device__ __forceinline__ int a_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 template <Epi EPI>
-__global__ __launch_bounds__(512) void pipe_kernel(MainArgs p) {
+__global__ __launch_bounds__(512) void pipe_kernel(MainArgs p, int group) {
     constexpr int BM = 256, BN = 256, WM = 4, WN = 2, NW = 8;
     constexpr int BK = 64;                        // bf16 elements per stage (128 B per row)
     constexpr int WTM = BM / WM, WTN = BN / WN;   // 64 x 128 per wave
@@ -387,14 +388,22 @@ __global__ __launch_bounds__(512) void pipe_kernel(MainArgs p) {
     const int wm = wave / WN, wn = wave % WN;
     const int64_t M = p.M, K = p.K, N = p.N;
 
+    // A workgroup owns one 256-row block and `group` consecutive 256-column
+    // tiles of it.  The row moments depend only on the rows, so they are
+    // reduced once, alongside the first tile's main loop, and kept in LDS for
+    // the epilogues of all the group's tiles.  Workgroup order: XCD-contiguous,
+    // then blocks of GM row blocks x all column groups (operand panels shared
+    // under one L2).
+    if constexpr (!LN) group = 1;  // the plain product has no per-row work to share
     const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
+    const int ngroups = (tiles_n + group - 1) / group;
     const int t = xcd_contiguous(blockIdx.x, gridDim.x);
     constexpr int GM = 4;
-    const int group = GM * tiles_n, gid = t / group, first = gid * GM;
+    const int span = GM * ngroups, gid = t / span, first = gid * GM;
     const int gsz = min(tiles_m - first, GM);
-    const int pm = first + (t % group) % gsz;
-    const int pn = (t % group) / gsz;
-    const int64_t m0 = (int64_t)pm * BM, n0 = (int64_t)pn * BN;
+    const int pm = first + (t % span) % gsz;
+    const int gn = (t % span) / gsz;
+    const int64_t m0 = (int64_t)pm * BM;
 
     const __bf16* A = reinterpret_cast<const __bf16*>(p.A);
     const char* Bp = reinterpret_cast<const char*>(p.B);
@@ -413,26 +422,8 @@ __global__ __launch_bounds__(512) void pipe_kernel(MainArgs p) {
         const int piece = (lane & 7) ^ a_swz(r);                    // 16-byte piece it fetches
         a_off[j] = (uint32_t)(((min(m0 + r, M - 1) - m0) * K + piece * 8) * 2);
     }
-    uint32_t b_off[B_INS];
-    const int64_t nb0 = n0 / 16;
-#pragma unroll
-    for (int j = 0; j < B_INS; ++j) {
-        const int c = wave + j * NW, nb = c >> 1, kb = c & 1;
-        b_off[j] = (uint32_t)packed_chunk(min(nb0 + nb, p.nblocks - 1) - nb0, kb, p.kchunks, lane);
-    }
     const uint64_t a_base = uniform_u64(A + m0 * K);
-    const uint64_t b_base = uniform_u64(Bp + packed_chunk(nb0, 0, p.kchunks, 0));
     const uint32_t smem_addr = lds_addr32(smem);
-    auto issue = [&](int s) {
-        const uint32_t base = smem_addr + (uint32_t)((s & 1) * STAGE);
-        const uint64_t ab = a_base + (uint64_t)s * (BK * 2), bb = b_base + (uint64_t)s * (2 * kChunkBytes);
-#pragma unroll
-        for (int j = 0; j < A_INS; ++j)
-            g2lds16_async_sb(ab, a_off[j], base + (uint32_t)((wave + j * NW) * kChunkBytes));
-#pragma unroll
-        for (int j = 0; j < B_INS; ++j)
-            g2lds16_async_sb(bb, b_off[j], base + (uint32_t)(A_BYTES + (wave + j * NW) * kChunkBytes));
-    };
     // fragments of stage s, half h (k 32h .. 32h+31)
     auto read = [&](int s, int h, u32x4(&fa)[FM], u32x4(&fb)[FN]) {
         const char* base = smem + (s & 1) * STAGE;
@@ -447,141 +438,172 @@ __global__ __launch_bounds__(512) void pipe_kernel(MainArgs p) {
             fb[fn] = lds_ld16(lds_ptr((char*)base + A_BYTES + ((wn * FN + fn) * 2 + h) * kChunkBytes + lane * 16));
     };
 
-    f32x4 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     float s1[FMW], s2[FMW];
 #pragma unroll
     for (int i = 0; i < FMW; ++i) s1[i] = s2[i] = 0.f;
 
-    // MFMAs on (fa, fb), the owned rows' moments from fa, with the next half's
-    // fragment reads (already issued) interleaved by the scheduler.
-    auto compute = [&](auto own, u32x4(&fa)[FM], u32x4(&fb)[FN]) {
-        constexpr int OWN = decltype(own)::value;
-        if constexpr (LN) {
-#pragma unroll
-            for (int i = 0; i < FMW; ++i) chunk_moments<__bf16>(fa[OWN * FMW + i], s1[i], s2[i]);
-        }
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-            for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma_chunk<__bf16>(fa[fm], fb[fn], acc[fm][fn]);
-#pragma unroll
-        for (int i = 0; i < NMF; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
-            if (i < NRD) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
-        }
-    };
+    for (int tt = 0; tt < group; ++tt) {
+        const int pn = gn * group + tt;
+        if (pn >= tiles_n) break;
+        const int64_t n0 = (int64_t)pn * BN;
+        if (tt > 0) __syncthreads();  // every wave is done with the previous tile's stages
 
-    auto run = [&](auto own) {
-        issue(0);
-        if (nst > 1) {
-            issue(1);
-            wait_vmcnt<PER>();
-        } else {
-            wait_vmcnt<0>();
+        uint32_t b_off[B_INS];
+        const int64_t nb0 = n0 / 16;
+#pragma unroll
+        for (int j = 0; j < B_INS; ++j) {
+            const int c = wave + j * NW, nb = c >> 1, kb = c & 1;
+            b_off[j] = (uint32_t)packed_chunk(min(nb0 + nb, p.nblocks - 1) - nb0, kb, p.kchunks, lane);
         }
-        block_barrier();
-        u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
-        read(0, 0, fa0, fb0);
-        for (int s = 0; s < nst; ++s) {
-            read(s, 1, fa1, fb1);
-            compute(own, fa0, fb0);
-            wait_vmcnt<0>();  // this wave's copies of stage s+1 have landed
-            wait_lgkm0();     // this wave's reads of stage s are complete
+        const uint64_t b_base = uniform_u64(Bp + packed_chunk(nb0, 0, p.kchunks, 0));
+        auto issue = [&](int s) {
+            const uint32_t base = smem_addr + (uint32_t)((s & 1) * STAGE);
+            const uint64_t ab = a_base + (uint64_t)s * (BK * 2), bb = b_base + (uint64_t)s * (2 * kChunkBytes);
+#pragma unroll
+            for (int j = 0; j < A_INS; ++j)
+                g2lds16_async_sb(ab, a_off[j], base + (uint32_t)((wave + j * NW) * kChunkBytes));
+#pragma unroll
+            for (int j = 0; j < B_INS; ++j)
+                g2lds16_async_sb(bb, b_off[j], base + (uint32_t)(A_BYTES + (wave + j * NW) * kChunkBytes));
+        };
+
+        f32x4 acc[FM][FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        // MFMAs on (fa, fb) -- and, on the group's first tile, the owned rows'
+        // moments from the same fa registers -- with the next half's fragment
+        // reads (already issued) interleaved by the scheduler.  OWN < 0: no moments.
+        auto compute = [&](auto own, u32x4(&fa)[FM], u32x4(&fb)[FN]) {
+            constexpr int OWN = decltype(own)::value;
+            if constexpr (LN && OWN >= 0) {
+#pragma unroll
+                for (int i = 0; i < FMW; ++i) chunk_moments<__bf16>(fa[OWN * FMW + i], s1[i], s2[i]);
+            }
+#pragma unroll
+            for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+                for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma_chunk<__bf16>(fa[fm], fb[fn], acc[fm][fn]);
+#pragma unroll
+            for (int i = 0; i < NMF; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+                if (i < NRD) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
+            }
+        };
+        auto run = [&](auto own) {
+            issue(0);
+            if (nst > 1) {
+                issue(1);
+                wait_vmcnt<PER>();
+            } else {
+                wait_vmcnt<0>();
+            }
             block_barrier();
-            if (s + 2 < nst) issue(s + 2);  // into the buffer stage s just vacated
-            read(s + 1, 0, fa0, fb0);       // past the end this reads stale data that is never used
-            compute(own, fa1, fb1);
-        }
-    };
-    if (LN && wn == 1)
-        run(std::integral_constant<int, 1>{});
-    else
-        run(std::integral_constant<int, 0>{});
-    wait_lgkm0();
-
-    if constexpr (LN) {
-#pragma unroll
-        for (int i = 0; i < FMW; ++i) {
-            const float a = sum_lane_groups(s1[i]);
-            const float b = sum_lane_groups(s2[i]);
-            if (lane < 16) {
-                const int r = wm * WTM + (wn * FMW + i) * 16 + lane;
-                row_s1[r] = a;
-                row_s2[r] = b;
+            u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+            read(0, 0, fa0, fb0);
+            for (int s = 0; s < nst; ++s) {
+                read(s, 1, fa1, fb1);
+                compute(own, fa0, fb0);
+                wait_vmcnt<0>();  // this wave's copies of stage s+1 have landed
+                wait_lgkm0();     // this wave's reads of stage s are complete
+                block_barrier();
+                if (s + 2 < nst) issue(s + 2);  // into the buffer stage s just vacated
+                read(s + 1, 0, fa0, fb0);       // past the end this reads stale data that is never used
+                compute(own, fa1, fb1);
             }
-        }
-        __syncthreads();
-        for (int r = tid; r < BM; r += NW * kWave) {
-            const float mean = row_s1[r] / (float)K;
-            const float var = __builtin_fmaxf(row_s2[r] / (float)K - mean * mean, 0.f);
-            row_s1[r] = mean;
-            row_s2[r] = 1.0f / __builtin_sqrtf(var + p.eps);
-        }
-        __syncthreads();
-    }
-
-    // Per-lane epilogue operands, loaded once: the column terms c_n, b_n (or
-    // the bias) of the lane's 8 columns and the row terms mean_m, rstd_m of
-    // its 16 rows.
-    const int lc = wn * WTN + (lane & 15), lr = wm * WTM + 4 * (lane >> 4);  // lane's first column / row in the tile
-    float cn[FN], bn[FN];
-#pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
-        const int64_t nc = min(n0 + lc + fn * 16, N - 1);
-        cn[fn] = 0.f;
-        bn[fn] = 0.f;
-        if constexpr (LN) {
-            cn[fn] = p.c_col[nc];
-            bn[fn] = p.b_col[nc];
+        };
+        if (LN && tt == 0) {
+            if (wn == 1)
+                run(std::integral_constant<int, 1>{});
+            else
+                run(std::integral_constant<int, 0>{});
         } else {
-            if (p.bias) bn[fn] = to_f32<__bf16>(reinterpret_cast<const __bf16*>(p.bias)[nc]);
+            run(std::integral_constant<int, -1>{});
         }
-    }
-    float mu[FM][4], rs[FM][4];
+        wait_lgkm0();
+
+        if (LN && tt == 0) {
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            mu[fm][i] = LN ? row_s1[lr + fm * 16 + i] : 0.f;
-            rs[fm][i] = LN ? row_s2[lr + fm * 16 + i] : 1.f;
-        }
-    auto value = [&](int fm, int fn, int i) {
-        const float v = acc[fm][fn][i];
-        if constexpr (LN)
-            return __builtin_fmaf(rs[fm][i], __builtin_fmaf(-mu[fm][i], cn[fn], v), bn[fn]);
-        else
-            return v + bn[fn];
-    };
-    if (m0 + BM <= M && n0 + BN <= N) {
-        // whole tile in range: no per-element checks; the row offsets are
-        // uniform (scalar) and the lane's offset from the tile base is fixed
-        // (32 bits: 256 rows of N elements)
-        __bf16* Ct = C + m0 * N + n0;
-        const uint32_t lo = (uint32_t)(lr * N + lc);
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                __bf16* Cr = Ct + (int64_t)(fm * 16 + i) * N;
-#pragma unroll
-                for (int fn = 0; fn < FN; ++fn) Cr[lo + fn * 16] = (__bf16)value(fm, fn, i);
-            }
-    } else {
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int64_t r = m0 + lr + fm * 16 + i;
-#pragma unroll
-                for (int fn = 0; fn < FN; ++fn) {
-                    const int64_t n = n0 + lc + fn * 16;
-                    if (r < M && n < N) C[r * N + n] = (__bf16)value(fm, fn, i);
+            for (int i = 0; i < FMW; ++i) {
+                const float a = sum_lane_groups(s1[i]);
+                const float b = sum_lane_groups(s2[i]);
+                if (lane < 16) {
+                    const int r = wm * WTM + (wn * FMW + i) * 16 + lane;
+                    row_s1[r] = a;
+                    row_s2[r] = b;
                 }
             }
+            __syncthreads();
+            for (int r = tid; r < BM; r += NW * kWave) {
+                const float mean = row_s1[r] / (float)K;
+                const float var = __builtin_fmaxf(row_s2[r] / (float)K - mean * mean, 0.f);
+                row_s1[r] = mean;
+                row_s2[r] = 1.0f / __builtin_sqrtf(var + p.eps);
+            }
+            __syncthreads();
+        }
+
+        // Per-lane epilogue operands, loaded once per tile: the column terms c_n,
+        // b_n (or the bias) of the lane's 8 columns and the row terms mean_m,
+        // rstd_m of its 16 rows.
+        const int lc = wn * WTN + (lane & 15), lr = wm * WTM + 4 * (lane >> 4);  // lane's first column / row
+        float cn[FN], bn[FN];
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+            const int64_t nc = min(n0 + lc + fn * 16, N - 1);
+            cn[fn] = 0.f;
+            bn[fn] = 0.f;
+            if constexpr (LN) {
+                cn[fn] = p.c_col[nc];
+                bn[fn] = p.b_col[nc];
+            } else {
+                if (p.bias) bn[fn] = to_f32<__bf16>(reinterpret_cast<const __bf16*>(p.bias)[nc]);
+            }
+        }
+        float mu[FM][4], rs[FM][4];
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                mu[fm][i] = LN ? row_s1[lr + fm * 16 + i] : 0.f;
+                rs[fm][i] = LN ? row_s2[lr + fm * 16 + i] : 1.f;
+            }
+        auto value = [&](int fm, int fn, int i) {
+            const float v = acc[fm][fn][i];
+            if constexpr (LN)
+                return __builtin_fmaf(rs[fm][i], __builtin_fmaf(-mu[fm][i], cn[fn], v), bn[fn]);
+            else
+                return v + bn[fn];
+        };
+        if (m0 + BM <= M && n0 + BN <= N) {
+            // whole tile in range: no per-element checks; the row offsets are
+            // uniform (scalar) and the lane's offset from the tile base is fixed
+            // (32 bits: 256 rows of N elements)
+            __bf16* Ct = C + m0 * N + n0;
+            const uint32_t lo = (uint32_t)(lr * N + lc);
+#pragma unroll
+            for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    __bf16* Cr = Ct + (int64_t)(fm * 16 + i) * N;
+#pragma unroll
+                    for (int fn = 0; fn < FN; ++fn) Cr[lo + fn * 16] = (__bf16)value(fm, fn, i);
+                }
+        } else {
+#pragma unroll
+            for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int64_t r = m0 + lr + fm * 16 + i;
+#pragma unroll
+                    for (int fn = 0; fn < FN; ++fn) {
+                        const int64_t n = n0 + lc + fn * 16;
+                        if (r < M && n < N) C[r * N + n] = (__bf16)value(fm, fn, i);
+                    }
+                }
+        }
     }
 }
 
@@ -777,8 +799,13 @@ static hipError_t run_main(const MainArgs& a, int64_t batch, hipStream_t s) {
 
 template <Epi EPI>
 static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
-    const int64_t tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
-    pipe_kernel<EPI><<<dim3((unsigned)tiles), 512, 0, s>>>(a);
+    const int64_t tm = (a.M + 255) / 256, tn = (a.N + 255) / 256;
+    // deferred LN: as many column tiles per workgroup as keeps at least 256
+    // workgroups (one per CU), so the row moments are reduced once per group
+    int64_t group = 1;
+    if (EPI == Epi::kLnDeferred) group = std::max<int64_t>(1, std::min<int64_t>(tn, tm * tn / 256));
+    const int64_t wgs = tm * ((tn + group - 1) / group);
+    pipe_kernel<EPI><<<dim3((unsigned)wgs), 512, 0, s>>>(a, (int)group);
     return hipGetLastError();
 }
 
