@@ -117,8 +117,8 @@ DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, i
  * stored values at j > i are ignored (tiles wholly above the diagonal are
  * never read; inside diagonal tiles they are masked).  causal = 0 uses every
  * key.  A row whose kept scores are all -inf gives NaN.  dtype must be
- * DN_BF16; d must be 64 or 128; Lk a multiple of 8 and Lq * Lk <= 2^31
- * (else DN_ERR_UNSUPPORTED).
+ * DN_BF16; d must be 64 or 128; Lk a multiple of 8, Lq * Lk <= 2^31 and
+ * Lk * d * 2 < 2^32 (else DN_ERR_UNSUPPORTED).
  */
 DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq,
                               int64_t Lk, int64_t d, int causal, int dtype, void* out,

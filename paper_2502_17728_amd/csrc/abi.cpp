@@ -113,7 +113,8 @@ DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, i
         __builtin_mul_overflow(BH, Lq, &bhlq))
         return DN_ERR_INVALID_ARG;
     if (dtype != DN_BF16 || (d != 64 && d != 128) || Lk % 8) return DN_ERR_UNSUPPORTED;
-    if (Lq * Lk > (int64_t(1) << 31)) return DN_ERR_UNSUPPORTED;  // one head's scores within 4 GiB
+    if (Lq * Lk > (int64_t(1) << 31) || Lk * d * 2 >= (int64_t(1) << 32))
+        return DN_ERR_UNSUPPORTED;  // one head's scores and values within 4 GiB
     if (!aligned(S, 16) || !aligned(V, 16) || !aligned(out, 16)) return DN_ERR_MISALIGNED;
     if (overlaps(out, ob, S, sb) || overlaps(out, ob, V, vb)) return DN_ERR_INVALID_ARG;
     if (BH * ((Lq + 255) / 256) > kMaxGridX) return DN_ERR_UNSUPPORTED;

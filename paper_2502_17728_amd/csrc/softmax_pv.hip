@@ -188,21 +188,23 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
 
     // ---- V: shared by every wave, so it goes through an NS-deep ring with a
     // barrier per step (copy instruction j covers key rows VRPI*(wave + j*NW) ..).
-    int v_row[V_INS], v_piece[V_INS];
+    // Byte offsets from the head's base: 32 bits (Lk * d * 2 < 2^32).
+    uint32_t v_row[V_INS], v_p16[V_INS];
 #pragma unroll
     for (int j = 0; j < V_INS; ++j) {
         const int r = (wave + j * NW) * VRPI + lane / VPR;
-        v_row[j] = r;
-        v_piece[j] = (lane % VPR) ^ v_swz<D>(r);
+        v_row[j] = (uint32_t)r;
+        v_p16[j] = (uint32_t)(((lane % VPR) ^ v_swz<D>(r)) * 16);
     }
+    const uint64_t v_base = uniform_u64(Vh);
+    const uint32_t vlast = (uint32_t)(Lk - 1);
     auto issue_v = [&](int step) {
         const uint32_t base = smem_addr + (uint32_t)((step % NS) * V_BYTES);
-        const int64_t k0 = (int64_t)step * BKV;
-        const bool tail = k0 + BKV > Lk;  // only the last steps of a key range need clamping
+        const uint32_t k0 = (uint32_t)step * BKV;
 #pragma unroll
         for (int j = 0; j < V_INS; ++j) {
-            const int64_t key = tail ? min(k0 + v_row[j], Lk - 1) : k0 + v_row[j];
-            g2lds16_async(Vh + key * D + v_piece[j] * 8, base + (uint32_t)((wave + j * NW) * kChunkBytes));
+            const uint32_t key = k0 + v_row[j] < vlast ? k0 + v_row[j] : vlast;  // rows past Lk clamp onto the last
+            g2lds16_async_sb(v_base, key * (uint32_t)VROW + v_p16[j], base + (uint32_t)((wave + j * NW) * kChunkBytes));
         }
     };
 
@@ -294,9 +296,10 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
                 }
         }
     };
+    const int qw0i = (int)qw0, kv_endi = (int)kv_end;  // positions fit 32 bits (Lq * Lk <= 2^31)
     auto is_edge = [&](int step) {
-        const int64_t k0 = (int64_t)step * BKV;
-        return (causal && k0 + BKV - 1 > qw0) || k0 + BKV > kv_end;
+        const int k0 = step * BKV;
+        return (causal && k0 + BKV - 1 > qw0i) || k0 + BKV > kv_endi;
     };
 
     // Prologue: the copies of iterations -AHEAD .. -1 in the steady-state
@@ -328,7 +331,10 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     // instructions with the exponentials.  When step s's numerators raised the
     // reference, the partial sums follow it first (a rare branch ahead of the
     // block).
-    for (int s = 0; s < nsteps; ++s) {
+    // two numerator buffers used in turn: the loop is unrolled by two so that
+    // neither is ever copied
+    u32x4 pf2[QW][2];
+    auto iteration = [&](int s, u32x4(&pcur)[QW][2], u32x4(&pnext)[QW][2]) {
         wait_vmcnt_asm<WAIT_N>();  // S(s+1) and this wave's V copies of step s are complete
         wait_lgkm0();              // this wave's LDS reads of step s-1 are complete
         block_barrier();
@@ -358,15 +364,14 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
 #pragma unroll
             for (int b = 0; b < DB; ++b)
 #pragma unroll
-                for (int f = 0; f < QW; ++f) acc[f][b] = mfma_chunk<__bf16>(vf[b], pf[f][kc], acc[f][b]);
+                for (int f = 0; f < QW; ++f) acc[f][b] = mfma_chunk<__bf16>(vf[b], pcur[f][kc], acc[f][b]);
 #pragma unroll
-            for (int f = 0; f < QW; ++f) accl[f] = mfma_chunk<__bf16>(ones, pf[f][kc], accl[f]);
+            for (int f = 0; f < QW; ++f) accl[f] = mfma_chunk<__bf16>(ones, pcur[f][kc], accl[f]);
         };
-        u32x4 pfn[QW][2];
         {
             u32x4 vf[DB];
             read_v(0, vf);
-            raised = numerators(sc, pfn, alpha);
+            raised = numerators(sc, pnext, alpha);
             issue_s(s + 1 + PF);  // the slot of S(s+1) has been read
             products(0, vf);
         }
@@ -375,11 +380,10 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
             read_v(1, vf);
             products(1, vf);
         }
-#pragma unroll
-        for (int f = 0; f < QW; ++f) {
-            pf[f][0] = pfn[f][0];
-            pf[f][1] = pfn[f][1];
-        }
+    };
+    for (int s = 0; s < nsteps; s += 2) {
+        iteration(s, pf, pf2);
+        if (s + 1 < nsteps) iteration(s + 1, pf2, pf);
     }
     wait_vmcnt_asm<0>();  // no copy into LDS may outlive the workgroup
 

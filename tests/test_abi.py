@@ -95,6 +95,7 @@ def test_softmax_pv_deferred_validation():
     assert f(P, P2, 1, 64, 64, 96, 0, 1, P3, None) == UNSUPPORTED        # d must be 64 or 128
     assert f(P, P2, 1, 64, 60, 64, 0, 1, P3, None) == UNSUPPORTED        # Lk % 8
     assert f(P, P2, 1, 65536, 65536, 64, 1, 1, P3, None) == UNSUPPORTED  # one head's scores > 4 GiB
+    assert f(P, P2, 1, 8, 1 << 24, 128, 0, 1, P3, None) == UNSUPPORTED    # one head's values >= 4 GiB
     assert f(P, P2 + 4, 1, 64, 64, 64, 0, 1, P3, None) == MISALIGNED
     assert f(P, P2, 1, 64, 64, 64, 0, 1, P + 64, None) == INVALID        # out overlaps S
 
