@@ -415,7 +415,7 @@ static hipError_t run_softmax_pv(const void* S, const void* V, int64_t BH, int64
 }
 
 // 8 waves x 2 fragments (256 queries per workgroup), two V slots and two S
-// slots per wave: 64 KiB (d = 64) or 96 KiB (d = 128) of LDS.  Deeper rings
+// slots per wave: 80 KiB (d = 64) or 96 KiB (d = 128) of LDS.  Deeper rings
 // measured no faster on the causal 32 x 8192 x 8192, d = 128 workload.
 constexpr int kSmWaves = 8, kSmFrags = 2, kSmStages = 2, kSmPrefetch = 2;
 
