@@ -609,80 +609,100 @@ __global__ __launch_bounds__(512) void pipe_kernel(MainArgs p, int group) {
 
 // =============================================================================
 // Decode-shaped deferred LN -> Linear: M <= 16 tokens, bf16.
-// The work is streaming W' from HBM, so each workgroup owns 16 output columns
-// and its four waves split K; one 16x16x32 MFMA per 32-k chunk multiplies the
-// (zero-padded) x rows with a packed W' chunk, which a wave reads straight
-// from HBM into operand registers as one contiguous KiB.  The row moments
-// ride on the otherwise idle matrix core: with B = all-ones the product gives
-// sum_k x[m][k] in every column, and with B = x itself the Gram matrix x x^T
-// whose diagonal is sum_k x[m][k]^2.
+// The work is streaming W' from HBM.  Each workgroup owns NC blocks of 16
+// output columns and its KS waves split K; per 32-k chunk a wave reads the
+// (zero-padded) x fragment once and NC packed W' chunks straight from HBM into
+// operand registers (one contiguous KiB each), and runs one 16x16x32 MFMA per
+// column block.  The row moments ride on the otherwise idle matrix core: with
+// B = all-ones the product gives sum_k x[m][k] in every column, and with B = x
+// itself the Gram matrix x x^T whose diagonal is sum_k x[m][k]^2 -- once per
+// chunk for all NC column blocks.
 // =============================================================================
-constexpr int kDecUnroll = 8;
-
-__global__ __launch_bounds__(256) void ln_decode_bf16_kernel(const __bf16* __restrict__ x,
+template <int KS, int NC, int U>
+__global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16* __restrict__ x,
                                                              const char* __restrict__ Wp, int64_t kchunks,
-                                                             const float* __restrict__ c_col,
+                                                             int64_t nblocks, const float* __restrict__ c_col,
                                                              const float* __restrict__ b_col, int M, int64_t K,
                                                              int64_t N, float eps, __bf16* __restrict__ out) {
-    __shared__ f32x4 part[3][4][kWave];
+    __shared__ f32x4 part[2 + NC][KS][kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t nb = blockIdx.x;
-    const int64_t n0 = nb * 16;
+    const int64_t nb0 = (int64_t)blockIdx.x * NC;
     const int row = lane & 15;
     const bool row_ok = row < M;
     const __bf16* xr = x + (int64_t)(row_ok ? row : 0) * K;
-    const char* wr = Wp + packed_chunk(nb, 0, kchunks, lane);
+    const char* wr[NC];
+#pragma unroll
+    for (int q = 0; q < NC; ++q) wr[q] = Wp + packed_chunk(min(nb0 + q, nblocks - 1), 0, kchunks, lane);
 
     const int64_t nchunks = kchunks;
-    const int64_t per = (nchunks + 3) / 4;
+    const int64_t per = (nchunks + KS - 1) / KS;
     const int64_t c_begin = wave * per, c_end = min(nchunks, c_begin + per);
 
     const u32x4 ones = {0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
     const u32x4 zero = {0, 0, 0, 0};
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f}, sx = acc, sxx = acc;
+    f32x4 acc[NC], sx = {0.f, 0.f, 0.f, 0.f}, sxx = sx;
+#pragma unroll
+    for (int q = 0; q < NC; ++q) acc[q] = sx;
 
-    int64_t c = c_begin;
-    for (; c + kDecUnroll <= c_end; c += kDecUnroll) {
-        u32x4 a[kDecUnroll], b[kDecUnroll];
+    // Software pipeline over groups of U chunks: the loads of group g + 1 are in
+    // flight while group g multiplies.  Every load is unconditional (chunk
+    // indexes clamp to the wave's last chunk, x reads past the range turn into
+    // zeros) so the wait counts stay exact; the group count is rounded up to
+    // even and a group wholly past the range adds x = 0 times finite W'.
+    const int64_t ngroups = c_end > c_begin ? (c_end - c_begin + U - 1) / U : 0;
+    u32x4 a0[U], b0[U][NC], a1[U], b1[U][NC];
+    auto load = [&](u32x4(&a)[U], u32x4(&b)[U][NC], int64_t g) {
 #pragma unroll
-        for (int u = 0; u < kDecUnroll; ++u) {
-            const int64_t kk = (c + u) * 32 + (lane >> 4) * 8;
-            b[u] = ld16(wr + (c + u) * kWave * 16);  // zero-padded past K
-            a[u] = (kk < K && row_ok) ? ld16(xr + kk) : zero;
+        for (int u = 0; u < U; ++u) {
+            const int64_t cc = c_begin + g * U + u;
+            const bool ok = cc < c_end;
+            const int64_t cl = ok ? cc : c_end - 1;
+            const int64_t kk = cl * 32 + (lane >> 4) * 8;
+#pragma unroll
+            for (int q = 0; q < NC; ++q) b[u][q] = ld16(wr[q] + cl * kWave * 16);  // zero-padded past K
+            const u32x4 xv = ld16(xr + min(kk, K - 8));                              // K % 8 == 0
+            a[u] = (ok && kk < K && row_ok) ? xv : zero;
         }
+    };
+    auto compute = [&](const u32x4(&a)[U], const u32x4(&b)[U][NC]) {
 #pragma unroll
-        for (int u = 0; u < kDecUnroll; ++u) {
-            acc = mfma_chunk<__bf16>(a[u], b[u], acc);
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int q = 0; q < NC; ++q) acc[q] = mfma_chunk<__bf16>(a[u], b[u][q], acc[q]);
             sx = mfma_chunk<__bf16>(a[u], ones, sx);
             sxx = mfma_chunk<__bf16>(a[u], a[u], sxx);
         }
+    };
+    if (ngroups > 0) {
+        load(a0, b0, 0);
+        for (int64_t g = 0; g < ngroups; g += 2) {
+            load(a1, b1, g + 1);
+            compute(a0, b0);
+            load(a0, b0, g + 2);
+            compute(a1, b1);
+        }
     }
-    for (; c < c_end; ++c) {
-        const int64_t kk = c * 32 + (lane >> 4) * 8;
-        const u32x4 b = ld16(wr + c * kWave * 16);
-        const u32x4 a = (kk < K && row_ok) ? ld16(xr + kk) : zero;
-        acc = mfma_chunk<__bf16>(a, b, acc);
-        sx = mfma_chunk<__bf16>(a, ones, sx);
-        sxx = mfma_chunk<__bf16>(a, a, sxx);
-    }
-    part[0][wave][lane] = acc;
-    part[1][wave][lane] = sx;
-    part[2][wave][lane] = sxx;
+#pragma unroll
+    for (int q = 0; q < NC; ++q) part[2 + q][wave][lane] = acc[q];
+    part[0][wave][lane] = sx;
+    part[1][wave][lane] = sxx;
     __syncthreads();
-    if (wave == 0) {
+    // column block j of the workgroup: reduce over the KS slices of K, then the epilogue
+    for (int j = wave; j < NC && nb0 + j < nblocks; j += KS) {
         f32x4 tot[3];
 #pragma unroll
-        for (int q = 0; q < 3; ++q) {
-            tot[q] = part[q][0][lane];
-#pragma unroll
-            for (int w = 1; w < 4; ++w) tot[q] += part[q][w][lane];
+        for (int w = 0; w < KS; ++w) {
+            const f32x4 a0 = part[2 + j][w][lane], a1 = part[0][w][lane], a2 = part[1][w][lane];
+            tot[0] = w ? tot[0] + a0 : a0;
+            tot[1] = w ? tot[1] + a1 : a1;
+            tot[2] = w ? tot[2] + a2 : a2;
         }
         // Gram diagonal (r, r) sits in lane r + 16*(r>>2), element r&3.  This lane's
         // rows are r = 4*(l>>4) + i, so the source lane is 20*(l>>4) + i.
         float diag[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) diag[i] = __shfl(tot[2][i], 20 * (lane >> 4) + i);
-        const int64_t col = n0 + (lane & 15);
+        const int64_t col = (nb0 + j) * 16 + (lane & 15);
         const int64_t n = min(col, N - 1);
         const float cn = c_col[n], bn = b_col[n];
 #pragma unroll
@@ -839,8 +859,22 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
     MainArgs a = packed_args(x, packed, M, K, N, dtype, out);
     a.eps = eps;
     if (dtype == 1 && M <= 16) {
-        ln_decode_bf16_kernel<<<dim3((unsigned)a.nblocks), 256, 0, s>>>(
-            (const __bf16*)x, (const char*)a.B, a.kchunks, a.c_col, a.b_col, (int)M, K, N, eps, (__bf16*)out);
+        // Layouts measured on the 8192 x 28672 up-projection: up to 4 tokens the x
+        // fragments are nearly free and 4 K-slices per column block stream best;
+        // at 5-8 one wave per column block (the whole K) does; beyond that x is
+        // re-read from L2 often enough that each wave shares it across 4 blocks.
+        auto launch = [&](auto kern, int ks, int cols) {
+            const int64_t wgs = (a.nblocks + cols - 1) / cols;
+            kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks,
+                                                            a.nblocks, a.c_col, a.b_col, (int)M, K, N, eps,
+                                                            (__bf16*)out);
+        };
+        if (M <= 4)
+            launch(ln_decode_bf16_kernel<4, 1, 8>, 4, 1);
+        else if (M <= 8)
+            launch(ln_decode_bf16_kernel<1, 1, 8>, 1, 1);
+        else
+            launch(ln_decode_bf16_kernel<4, 4, 2>, 4, 4);
         return hipGetLastError();
     }
     if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);

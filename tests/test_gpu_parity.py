@@ -53,8 +53,11 @@ def test_ln_linear_bf16_ragged(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M + K))
 
 
-@pytest.mark.parametrize("M", [1, 3, 4, 16])
-@pytest.mark.parametrize("K,N", [(1024, 520), (8200, 64)])
+# token counts on both sides of each decode-layout switch (4 | 5..8 | 9..16);
+# K = 8 leaves three of four K-slices empty, N = 24 / 520 leave a partial
+# group of column blocks
+@pytest.mark.parametrize("M", [1, 3, 4, 5, 8, 9, 16])
+@pytest.mark.parametrize("K,N", [(1024, 520), (8200, 64), (8, 24)])
 def test_ln_linear_bf16_decode_shapes(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M * 7 + 1, outliers=4))
 
@@ -117,7 +120,7 @@ def test_ln_linear_qkv_workload_sampled(ops):
     _ln_check(ops, case, rows=I.sample_rows(w.M, 24, seed=3))
 
 
-@pytest.mark.parametrize("t", [1, 4, 16])
+@pytest.mark.parametrize("t", [1, 4, 8, 16])
 def test_ln_linear_ffn_decode_workload(ops, t):
     _ln_check(ops, I.make_ln(I.ln_ffn_decode(t)))
 
