@@ -47,10 +47,12 @@ def _load():
         lib.oracle_layernorm.argtypes = [d, d, d, i64, i64, ctypes.c_double, d, i32]
         lib.oracle_linear.argtypes = [d, d, d, i64, i64, i64, i64, d, i32]
         lib.oracle_ln_linear.argtypes = [d, d, d, d, d, i64, i64, i64, ctypes.c_double, d, i32]
+        lib.oracle_rmsnorm.argtypes = [d, d, d, i64, i64, ctypes.c_double, d, i32]
+        lib.oracle_rms_linear.argtypes = [d, d, d, d, d, i64, i64, i64, ctypes.c_double, d, i32]
         lib.oracle_softmax.argtypes = [d, d, i64, i64, d, i32]
         lib.oracle_softmax_pv.argtypes = [d, d, d, d, i64, i64, i64, d, i32]
-        for f in ("oracle_layernorm", "oracle_linear", "oracle_ln_linear",
-                  "oracle_softmax", "oracle_softmax_pv"):
+        for f in ("oracle_layernorm", "oracle_linear", "oracle_ln_linear", "oracle_rmsnorm",
+                  "oracle_rms_linear", "oracle_softmax", "oracle_softmax_pv"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -127,6 +129,33 @@ def ln_linear(x, gamma, beta, W, bias, eps, nthreads=None):
     out = np.empty((M, N), np.float64)
     _check(_load().oracle_ln_linear(_ptr(x), _ptr(g), _ptr(b), _ptr(W), _ptr(bb), M, K, N,
                                     float(eps), _ptr(out), _threads(nthreads)), "ln_linear")
+    return out
+
+
+def rmsnorm(x, gamma, eps, beta=None, nthreads=None):
+    """Eq. (6) per row of x[M, K] (eps inside the root; beta optional); returns y[M, K] in fp64."""
+    x = to_f64(x)
+    M, K = x.shape
+    g = to_f64(gamma).reshape(K)
+    b = None if beta is None else to_f64(beta).reshape(K)
+    y = np.empty((M, K), np.float64)
+    _check(_load().oracle_rmsnorm(_ptr(x), _ptr(g), _ptr(b), M, K, float(eps),
+                                  _ptr(y), _threads(nthreads)), "rmsnorm")
+    return y
+
+
+def rms_linear(x, gamma, W, bias, eps, beta=None, nthreads=None):
+    """RMSNorm(x[M, K]) (Eq. (6)) . W[K, N] + bias, fp64."""
+    x = to_f64(x)
+    M, K = x.shape
+    W = to_f64(W)
+    N = W.shape[1]
+    g = to_f64(gamma).reshape(K)
+    b = None if beta is None else to_f64(beta).reshape(K)
+    bb = None if bias is None else to_f64(bias).reshape(N)
+    out = np.empty((M, N), np.float64)
+    _check(_load().oracle_rms_linear(_ptr(x), _ptr(g), _ptr(b), _ptr(W), _ptr(bb), M, K, N,
+                                     float(eps), _ptr(out), _threads(nthreads)), "rms_linear")
     return out
 
 

@@ -15,6 +15,8 @@
  *   - LayerNorm statistics, Eq. (1): mean and the biased (1/n) variance.
  *   - LayerNorm output,     Eq. (2): y = (x - mean)/sqrt(var + eps) * gamma + beta.
  *   - Linear layer,         Eq. (4): out = y F (+ bias), F stored as W[K][N].
+ *   - RMSNorm,              Eq. (6): y = x / sqrt(x x^T / n + eps) * gamma (+ beta),
+ *                           and RMSNorm followed by the linear layer.
  *   - Softmax then values,  Eq. (7) with the footnote's max subtraction:
  *       m = max_j x_j, e_j = exp(x_j - m), y_j = e_j / sum_i e_i, out = y V.
  *
@@ -26,6 +28,9 @@
  *   - eps is an argument (Eq. (2) names it without a value) and sits inside
  *     the square root as printed.
  *   - The variance is the biased one of Eq. (1): divide by n, two passes.
+ *   - RMSNorm (Eq. (6)) prints no eps; it is an argument here, inside the
+ *     root like LayerNorm's, and eps = 0 is the printed form.  Eq. (6) has no
+ *     shift; an optional beta is added after gamma, as for LayerNorm.
  *   - Causal masking keeps key j for query i iff j <= i.  Keys outside the
  *     mask are ignored, not read as values.
  *   - A row whose kept scores are all -inf yields NaN (0/0), as the plain
@@ -201,6 +206,56 @@ int oracle_ln_linear(const double* x, const double* gamma, const double* beta,
     if (!x || !gamma || !W || !out || M < 1 || K < 1 || N < 1) return -1;
     lnlin_ctx c = {x, gamma, beta, W, bias, K, N, eps, out};
     run_rows(lnlin_rows, &c, M, nthreads);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* RMSNorm, Eq. (6), one row: the root mean square replaces the standard     */
+/* deviation and no mean is subtracted.                                      */
+
+static void rmsnorm_row(const double* x, int64_t K, const double* gamma,
+                        const double* beta, double eps, double* y) {
+    double ss = 0.0;
+    for (int64_t k = 0; k < K; ++k) ss += x[k] * x[k];
+    double denom = sqrt(ss / (double)K + eps);
+    for (int64_t k = 0; k < K; ++k) {
+        double v = x[k] / denom * gamma[k];
+        y[k] = beta ? v + beta[k] : v;
+    }
+}
+
+static void rms_rows(void* p, int64_t r0, int64_t r1) {
+    ln_ctx* c = (ln_ctx*)p;
+    for (int64_t m = r0; m < r1; ++m)
+        rmsnorm_row(c->x + m * c->K, c->K, c->gamma, c->beta, c->eps, c->y + m * c->K);
+}
+
+int oracle_rmsnorm(const double* x, const double* gamma, const double* beta,
+                   int64_t M, int64_t K, double eps, double* y, int nthreads) {
+    if (!x || !gamma || !y || M < 1 || K < 1) return -1;
+    ln_ctx c = {x, gamma, beta, K, eps, y};
+    run_rows(rms_rows, &c, M, nthreads);
+    return 0;
+}
+
+/* RMSNorm followed by the linear layer: the product of Eq. (4) on Eq. (6)'s y. */
+static void rmslin_rows(void* p, int64_t r0, int64_t r1) {
+    lnlin_ctx* c = (lnlin_ctx*)p;
+    double* y = (double*)malloc((size_t)c->K * sizeof(double));
+    if (!y) return;
+    for (int64_t m = r0; m < r1; ++m) {
+        rmsnorm_row(c->x + m * c->K, c->K, c->gamma, c->beta, c->eps, y);
+        linear_row(y, c->W, c->bias, c->K, c->N, c->out + m * c->N);
+    }
+    free(y);
+}
+
+int oracle_rms_linear(const double* x, const double* gamma, const double* beta,
+                      const double* W, const double* bias, int64_t M, int64_t K,
+                      int64_t N, double eps, double* out, int nthreads) {
+    if (!x || !gamma || !W || !out || M < 1 || K < 1 || N < 1) return -1;
+    lnlin_ctx c = {x, gamma, beta, W, bias, K, N, eps, out};
+    run_rows(rmslin_rows, &c, M, nthreads);
     return 0;
 }
 

@@ -28,6 +28,16 @@ int oracle_ln_linear(const double* x, const double* gamma, const double* beta,
                      const double* W, const double* bias, int64_t M, int64_t K,
                      int64_t N, double eps, double* out, int nthreads);
 
+/* Eq. (6): y[M][K] = x / sqrt(mean(x^2) + eps) * gamma + beta (beta may be NULL;
+   eps = 0 is the printed form). */
+int oracle_rmsnorm(const double* x, const double* gamma, const double* beta,
+                   int64_t M, int64_t K, double eps, double* y, int nthreads);
+
+/* out[M][N] = RMSNorm(x[M][K]) . W[K][N] + bias[N]. */
+int oracle_rms_linear(const double* x, const double* gamma, const double* beta,
+                      const double* W, const double* bias, int64_t M, int64_t K,
+                      int64_t N, double eps, double* out, int nthreads);
+
 /* Eq. (7) softmax of R rows of length Lk.  qpos[r] >= 0 keeps keys j <= qpos[r]
    (causal) and writes 0 beyond; qpos NULL or qpos[r] < 0 keeps every key. */
 int oracle_softmax(const double* S, const int64_t* qpos, int64_t R, int64_t Lk,

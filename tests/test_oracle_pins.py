@@ -1,11 +1,11 @@
 """Pins of the fp64 oracle against what the paper and mathematics fix.
 
-The oracle (``oracle/``) is the plain definition of Eq. (1), (2), (4) and (7).
+The oracle (``oracle/``) is the plain definition of Eq. (1), (2), (4), (6) and (7).
 Before it may judge the GPU path it is tied here to things other than itself:
 
 - hand-worked examples stored in ``tests/golden`` (exact values);
 - closed forms and special cases (K = 2, constant rows, one-hot scores, V = I);
-- library routines: ``torch.nn.functional.layer_norm`` and ``torch.softmax``
+- library routines: ``torch.nn.functional.layer_norm``, ``rms_norm`` and ``torch.softmax``
   in fp64, which the oracle does not call;
 - the paper's fused forms, Eq. (5) and Eq. (8), evaluated independently here
   with numpy, which reach the same result by different arithmetic;
@@ -48,6 +48,16 @@ def test_golden_ln_linear(golden_dir):
     np.testing.assert_array_equal(y, _arr(g["y"]))
     out = oracle.ln_linear(x, gamma, beta, W, bias, g["eps"])
     np.testing.assert_array_equal(out, _arr(g["out"]))
+    np.testing.assert_array_equal(oracle.linear(y, W, bias), _arr(g["out"]))
+
+
+def test_golden_rms_linear(golden_dir):
+    g = json.load(open(os.path.join(golden_dir, "rms_linear_worked.json")))
+    x, W = _arr(g["x"]), _arr(g["W"])
+    gamma, bias = (np.array(g[k], np.float64) for k in ("gamma", "bias"))
+    y = oracle.rmsnorm(x, gamma, g["eps"])
+    np.testing.assert_array_equal(y, _arr(g["y"]))
+    np.testing.assert_array_equal(oracle.rms_linear(x, gamma, W, bias, g["eps"]), _arr(g["out"]))
     np.testing.assert_array_equal(oracle.linear(y, W, bias), _arr(g["out"]))
 
 
@@ -171,6 +181,20 @@ def test_ln_linear_matches_torch_layer_norm(M, K, N, eps):
     np.testing.assert_allclose(oracle.ln_linear(x, gamma, beta, W, bias, eps), want, rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("M,K,N,eps", [(5, 7, 3, 1e-5), (13, 64, 17, 0.1), (2, 1, 4, 0.0)])
+def test_rms_linear_matches_torch_rms_norm(M, K, N, eps):
+    rng = np.random.default_rng(M * K * N + 1)
+    x = rng.normal(size=(M, K)) * 3 + 0.5
+    gamma, beta = rng.uniform(0.5, 1.5, K), rng.normal(size=K) * 0.1
+    W, bias = rng.normal(size=(K, N)), rng.normal(size=N)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (K,), torch.from_numpy(gamma), eps)
+    np.testing.assert_allclose(oracle.rmsnorm(x, gamma, eps), ref.numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(oracle.rmsnorm(x, gamma, eps, beta=beta), ref.numpy() + beta, rtol=1e-12,
+                               atol=1e-13)
+    want = (ref @ torch.from_numpy(W) + torch.from_numpy(bias)).numpy()
+    np.testing.assert_allclose(oracle.rms_linear(x, gamma, W, bias, eps), want, rtol=1e-12, atol=1e-12)
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_softmax_pv_matches_torch_softmax(causal):
     rng = np.random.default_rng(11)
@@ -214,6 +238,19 @@ def test_eq5_fused_layernorm_equals_oracle(M, K, N):
     np.testing.assert_allclose(oracle.ln_linear(x, gamma, beta, W, bias, eps), epi, rtol=1e-11, atol=1e-12)
 
 
+@pytest.mark.parametrize("M,K,N", [(6, 32, 9), (3, 5, 2)])
+def test_eq6_deferred_rmsnorm_equals_oracle(M, K, N):
+    """Eq. (6) deferred past the product: r (x Gamma F) + beta F (+ bias), r = 1/sqrt(mean(x^2) + eps)."""
+    rng = np.random.default_rng(23)
+    eps = 1e-3
+    x = rng.normal(size=(M, K)) + 0.7
+    gamma, beta, W, bias = rng.uniform(0.5, 1.5, K), rng.normal(size=K), rng.normal(size=(K, N)), rng.normal(size=N)
+    r = 1.0 / np.sqrt((x * x).mean(axis=1) + eps)        # the collective sub-operation
+    fused = r[:, None] * (x @ (np.diag(gamma) @ W)) + beta @ W + bias
+    np.testing.assert_allclose(oracle.rms_linear(x, gamma, W, bias, eps, beta=beta), fused, rtol=1e-11,
+                               atol=1e-12)
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_eq8_fused_softmax_equals_oracle(causal):
     """Eq. (8): yV = (1 / sum_i e^{x_i}) ([e^{x_1} ... e^{x_n}] V)."""
@@ -250,6 +287,38 @@ def test_layernorm_shift_and_scale_invariance_without_eps():
     np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-13)
 
 
+def test_rmsnorm_k1_and_constant_rows():
+    # K = 1: y = x / sqrt(x^2 + eps) * gamma; eps = 0 gives sign(x) * gamma
+    for xv, eps in ((3.0, 16.0), (-0.5, 0.0), (2.0, 0.0)):
+        want = xv / math.sqrt(xv * xv + eps) * 1.5
+        assert oracle.rmsnorm(np.array([[xv]]), np.array([1.5]), eps)[0, 0] == pytest.approx(want, rel=1e-15)
+    # constant row c (eps = 0): the root mean square is |c|, so y = sign(c) * gamma exactly
+    gamma = np.array([0.5, -2.0, 3.0, 1.25])
+    for c in (7.0, -0.375):
+        np.testing.assert_array_equal(oracle.rmsnorm(np.full((1, 4), c), gamma, 0.0)[0], np.sign(c) * gamma)
+    # a zero row: eps > 0 gives zeros (the linear layer then yields beta W + bias); eps = 0 gives 0/0
+    assert (oracle.rmsnorm(np.zeros((1, 3)), np.ones(3), 1e-5) == 0).all()
+    assert np.isnan(oracle.rmsnorm(np.zeros((1, 3)), np.ones(3), 0.0)).all()
+
+
+def test_rmsnorm_pre_affine_mean_square_and_scale_invariance():
+    rng = np.random.default_rng(36)
+    M, K, eps = 8, 257, 0.05
+    x = rng.normal(size=(M, K)) * rng.uniform(0.1, 3, size=(M, 1)) + rng.normal(size=(M, 1))
+    y = oracle.rmsnorm(x, np.ones(K), eps)
+    ms = (x * x).mean(1)
+    np.testing.assert_allclose((y ** 2).mean(1), ms / (ms + eps), rtol=1e-13)
+    gamma = rng.normal(size=K)
+    a = oracle.rmsnorm(x, gamma, 0.0)
+    np.testing.assert_allclose(oracle.rmsnorm(-2.5 * x, gamma, 0.0), -a, rtol=1e-13, atol=1e-14)
+    # unlike LayerNorm it is not shift invariant ...
+    assert not np.allclose(oracle.rmsnorm(x + 1.0, gamma, 0.0), a)
+    # ... and on zero-mean rows it is LayerNorm (the pinned oracle) exactly in R
+    xc = x - x.mean(1, keepdims=True)
+    np.testing.assert_allclose(oracle.rmsnorm(xc, gamma, eps), oracle.layernorm(xc, gamma, None, eps),
+                               rtol=1e-12, atol=1e-13)
+
+
 def test_softmax_rows_sum_to_one_and_shift_invariance():
     rng = np.random.default_rng(33)
     L = 50
@@ -278,6 +347,8 @@ def test_threads_do_not_change_results():
     g, b = rng.normal(size=24), rng.normal(size=24)
     np.testing.assert_array_equal(oracle.ln_linear(x, g, b, W, None, 1e-5, nthreads=1),
                                   oracle.ln_linear(x, g, b, W, None, 1e-5, nthreads=5))
+    np.testing.assert_array_equal(oracle.rms_linear(x, g, W, None, 1e-5, nthreads=1),
+                                  oracle.rms_linear(x, g, W, None, 1e-5, nthreads=6))
     S, V = rng.normal(size=(37, 37)), rng.normal(size=(37, 3))
     np.testing.assert_array_equal(oracle.softmax_pv(S, V, qpos=np.arange(37), nthreads=1),
                                   oracle.softmax_pv(S, V, qpos=np.arange(37), nthreads=7))
@@ -298,6 +369,14 @@ def test_bruteforce_mpmath_tiny():
         var = mp.fsum((v - mean) ** 2 for v in xs) / K
         y = [(xs[k] - mean) / mp.sqrt(var + mp.mpf(eps)) * mp.mpf(float(g[k])) + mp.mpf(float(b[k]))
              for k in range(K)]
+        for n in range(N):
+            ref = mp.fsum(y[k] * mp.mpf(float(W[k, n])) for k in range(K)) + mp.mpf(float(bias[n]))
+            assert abs(float(ref) - got[m, n]) <= 1e-13 * max(1.0, abs(float(ref)))
+    got = oracle.rms_linear(x, g, W, bias, eps, beta=b)
+    for m in range(M):
+        xs = [mp.mpf(float(v)) for v in x[m]]
+        rms = mp.sqrt(mp.fsum(v * v for v in xs) / K + mp.mpf(eps))
+        y = [xs[k] / rms * mp.mpf(float(g[k])) + mp.mpf(float(b[k])) for k in range(K)]
         for n in range(N):
             ref = mp.fsum(y[k] * mp.mpf(float(W[k, n])) for k in range(K)) + mp.mpf(float(bias[n]))
             assert abs(float(ref) - got[m, n]) <= 1e-13 * max(1.0, abs(float(ref)))
