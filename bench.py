@@ -8,6 +8,10 @@ Softmax -> P.V (Sec. II-B, Eq. (8)).  The default workload is a 7B-class
 Transformer layer's two fusion sites: LN -> QKV projection, x[4096, 4096] .
 W[4096, 12288], and causal Softmax -> P.V over 32 heads, 8192 keys, d = 128.
 
+Warmup: the W untimed steps, continued until at least --warm-seconds (0.3 s)
+of them have run, so that the timed steps see the chip's steady clocks rather
+than its ramp out of idle (which costs 10-25 % on the first few milliseconds).
+
 Prints ONE JSON line.  `value` is whole-step throughput (TFLOP/s, algorithmic
 FLOP of both products) with inputs already resident in HBM; per-kernel times
 come from HIP events recorded on the stream the kernels are launched on.  The
@@ -42,7 +46,8 @@ PEAK_HBM_GBS = 8000.0       # HBM3E
 # the kernel source it was taken on: each entry carries the sha256 of its kernel's source files, and
 # the bench reports null once they differ.
 KERNEL_SOURCES = {"softmax_pv_deferred": ("softmax_pv.hip", "dn_device.hpp"),
-                  "ln_linear_deferred": ("ln_gemm.hip", "dn_device.hpp")}
+                  "ln_linear_deferred": ("ln_gemm.hip", "dn_device.hpp"),
+                  "rms_linear_deferred": ("ln_gemm.hip", "dn_device.hpp")}
 TRAFFIC = {
     ("softmax_pv_deferred", "causal_softmax_pv_bf16_32x8192x8192_d128"): {
         "sha256": ("4cb5880e7992356ce9815f38539bb72117dc54ee40675acb45549ac65f640d11",
@@ -78,9 +83,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warm-seconds", type=float, default=0.3,
+                    help="keep running warmup steps until this much wall time has passed")
     ap.add_argument("--workload", default="layer",
                     choices=["layer", "small", "ln_qkv", "causal_softmax_pv", "ffn_prefill",
-                             "ffn_decode_t1", "ffn_decode_t4", "ffn_decode_t16"])
+                             "ffn_decode_t1", "ffn_decode_t4", "ffn_decode_t16", "rms_qkv",
+                             "rms_ffn_decode_t1"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None)
@@ -103,29 +111,37 @@ def sm_bytes(w) -> float:
 
 
 class LNSite:
+    """LayerNorm -> Linear (Eq. (5)), or RMSNorm -> Linear (Eq. (6)) when the workload says so."""
+
     def __init__(self, ops, I, w):
         self.w = w
+        self.rms = w.norm == "rms"
+        self.kernel = "rms_linear_deferred" if self.rms else "ln_linear_deferred"
         self.case = I.make_ln(w)
         c = self.case
+        cuda = lambda t: None if t is None else t.cuda()
         self.x = c["x"].cuda()
         self.W = c["W"].cuda()
-        self.prep = ops.ln_linear_prepare(self.W, c["gamma"].cuda(), c["beta"].cuda(),
-                                          None if c["bias"] is None else c["bias"].cuda())
+        self.prep = ops.ln_linear_prepare(self.W, c["gamma"].cuda(), cuda(c["beta"]), cuda(c["bias"]))
         self.out = torch.empty((w.M, w.N), dtype=self.x.dtype, device="cuda")
         # unfused comparator: the same static weights packed once the same way (gamma = 1 folds
         # nothing), so both paths run the same weight layout and MFMA main loop
         self.Wpk = ops.ln_linear_prepare(self.W, torch.ones(w.K, dtype=self.W.dtype, device="cuda"))
-        self.g, self.b = c["gamma"].cuda(), c["beta"].cuda()
-        self.bias = None if c["bias"] is None else c["bias"].cuda()
+        self.g, self.b = c["gamma"].cuda(), cuda(c["beta"])
+        self.bias = cuda(c["bias"])
         self.y = torch.empty_like(self.x)
         self.ops = ops
         torch.cuda.synchronize()
 
     def fused(self):
-        self.ops.ln_linear_deferred(self.x, self.prep, self.w.eps, out=self.out)
+        f = self.ops.rms_linear_deferred if self.rms else self.ops.ln_linear_deferred
+        f(self.x, self.prep, self.w.eps, out=self.out)
 
     def unfused(self):
-        self.ops.layernorm(self.x, self.g, self.b, self.w.eps, out=self.y)
+        if self.rms:
+            self.ops.rmsnorm(self.x, self.g, self.w.eps, out=self.y)
+        else:
+            self.ops.layernorm(self.x, self.g, self.b, self.w.eps, out=self.y)
         self.ops.gemm(self.y, self.Wpk, self.bias, out=self.out.view(1, self.w.M, self.w.N))
 
     def flops(self):
@@ -142,9 +158,13 @@ class LNSite:
         c = self.case
         xs = c["x"][torch.as_tensor(idx)]
         t0 = time.perf_counter()
-        oracle.ln_linear(xs, c["gamma"], c["beta"], c["W"], c["bias"], c["eps"], nthreads=threads)
+        if self.rms:
+            oracle.rms_linear(xs, c["gamma"], c["W"], c["bias"], c["eps"], nthreads=threads)
+        else:
+            oracle.ln_linear(xs, c["gamma"], c["beta"], c["W"], c["bias"], c["eps"], nthreads=threads)
         dt = time.perf_counter() - t0
-        return dt, len(idx) / self.w.M, f"{len(idx)} of {self.w.M} LayerNorm->Linear rows"
+        norm = "RMSNorm" if self.rms else "LayerNorm"
+        return dt, len(idx) / self.w.M, f"{len(idx)} of {self.w.M} {norm}->Linear rows"
 
 
 class SMSite:
@@ -205,33 +225,53 @@ def build_sites(ops, I, name):
         return [SMSite(ops, I, I.SM_CAUSAL)], I.SM_CAUSAL.name
     if name == "ffn_prefill":
         return [LNSite(ops, I, I.LN_FFN_PREFILL)], I.LN_FFN_PREFILL.name
+    if name == "rms_qkv":
+        return [LNSite(ops, I, I.RMS_QKV)], I.RMS_QKV.name
     t = int(name.rsplit("t", 1)[1])
-    w = I.ln_ffn_decode(t)
+    w = I.rms_ffn_decode(t) if name.startswith("rms_") else I.ln_ffn_decode(t)
     return [LNSite(ops, I, w)], w.name
 
 
 # ------------------------------------------------------------------------------ timing
-def time_steps(fns, steps, warmup):
-    """Run `fns` in order per step; per-fn HIP-event durations and the total, in ms."""
-    for _ in range(warmup):
+def warm(fns, steps, seconds):
+    """Untimed: `steps` steps, then more until `seconds` of wall time have passed."""
+    t0 = time.perf_counter()
+    done = 0
+    while done < steps or time.perf_counter() - t0 < seconds:
         for f in fns:
             f()
+        done += 1
+        if done % 16 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
+
+
+def time_steps(fns, steps, warmup, warm_seconds=0.0):
+    """Run `fns` in order per step; per-fn HIP-event durations and the total, in ms.
+
+    The total comes from a pass with events only around the K steps; a second
+    pass of K steps with an event after every kernel gives the per-kernel times.
+    """
+    warm(fns, warmup, warm_seconds)
     stream = torch.cuda.current_stream()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(steps)]
     t_begin = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_begin.record(stream)
+    for _ in range(steps):
+        for f in fns:
+            f()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total = t_begin.elapsed_time(t_end) / steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(steps)]
     for s in range(steps):
         ev[s][0].record(stream)
         for i, f in enumerate(fns):
             f()
             ev[s][i + 1].record(stream)
-    t_end.record(stream)
     torch.cuda.synchronize()
     per = [sum(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(steps)) / steps for i in range(len(fns))]
-    total = t_begin.elapsed_time(t_end) / steps
     return per, total
 
 
@@ -251,7 +291,7 @@ def main():
     sites, wl_name = build_sites(ops, I, args.workload)
     setup_s = time.perf_counter() - t_setup
 
-    per, total = time_steps([s.fused for s in sites], args.steps, args.warmup)
+    per, total = time_steps([s.fused for s in sites], args.steps, args.warmup, args.warm_seconds)
     if args.calib_copy_mib > 0:
         src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -265,7 +305,7 @@ def main():
     kernels = {}
     dom = max(range(len(sites)), key=lambda i: per[i])
     for i, s in enumerate(sites):
-        name = "ln_linear_deferred" if isinstance(s, LNSite) else "softmax_pv_deferred"
+        name = s.kernel if isinstance(s, LNSite) else "softmax_pv_deferred"
         tf = s.flops() / (per[i] * 1e-3) / 1e12
         gbs = s.bytes() / (per[i] * 1e-3) / 1e9
         k = {"workload": s.w.name, "ms": round(per[i], 4), "tflops": round(tf, 2),
@@ -276,14 +316,21 @@ def main():
         k["hbm_traffic_mbytes"] = None if tr is None else round(tr / 1e6, 2)
         if not args.no_unfused:
             # speedups compare like with like: each path timed alone, back to back on its own inputs
-            # (inside the step the kernel follows the other site, whose traffic evicts the caches)
-            (fi,), _ = time_steps([s.fused], max(3, args.steps // 2), 2)
-            (u,), _ = time_steps([s.unfused], max(3, args.steps // 2), 2)
+            # (inside the step the kernel follows the other site, whose traffic evicts the caches);
+            # the two alternate over 5 rounds and each reports its median
+            n = max(3, args.steps // 2)
+            fis, us, uds = [], [], []
+            for _ in range(5):
+                fis.append(time_steps([s.fused], n, 2)[0][0])
+                us.append(time_steps([s.unfused], n, 2)[0][0])
+                if isinstance(s, SMSite) and s.w.causal:
+                    uds.append(time_steps([s.unfused_dense], max(3, n // 2), 1)[0][0])
+            fi, u = float(np.median(fis)), float(np.median(us))
             k["isolated_ms"] = round(fi, 4)
             k["unfused_ms"] = round(u, 4)
             k["speedup_vs_unfused"] = round(u / fi, 3)
-            if isinstance(s, SMSite) and s.w.causal:
-                (ud,), _ = time_steps([s.unfused_dense], max(3, args.steps // 4), 1)
+            if uds:
+                ud = float(np.median(uds))
                 k["unfused_dense_ms"] = round(ud, 4)
                 k["speedup_vs_unfused_dense"] = round(ud / fi, 3)
         kernels[name] = k

@@ -103,6 +103,21 @@ DN_API dn_status ln_linear_prepare(const void* W, const void* gamma, const void*
 DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M,
                              float eps, void* out, hipStream_t stream);
 
+/*
+ * out[M][N] = RMSNorm(x[M][K]) . W + bias (Sec. II-A, RMSNorm in Llama
+ * models, Eq. (6)), the deferred way: acc = x . W' on the MFMA with the row
+ * sum of squares reduced concurrently, then  out = rstd * acc + b  with
+ * rstd = 1/sqrt(sum_k x^2 / K + eps).  Eq. (6) subtracts no mean, so c is not
+ * used.  Eq. (6) prints no eps: eps is an argument inside the root, finite
+ * and >= 0, and eps = 0 is the printed form (an all-zero row then gives NaN).
+ * w comes from ln_linear_prepare with the RMSNorm gamma; Eq. (6) has no
+ * shift, so pass beta = NULL there (a non-NULL beta adds beta W to every
+ * row, as it does for LayerNorm).  Same argument rules, layout, ownership
+ * and status codes as ln_linear_deferred.
+ */
+DN_API dn_status rms_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M,
+                              float eps, void* out, hipStream_t stream);
+
 /* ======================================================================= */
 /* Softmax -> P.V, deferred (Sec. II-B, Eq. (7), (8) and its footnote)      */
 /* ======================================================================= */
@@ -131,6 +146,11 @@ DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, i
 /* y[M][K] = (x - mean)/sqrt(var + eps) * gamma + beta, Eq. (1)-(2).  beta may be NULL. */
 DN_API dn_status layernorm(const void* x, const void* gamma, const void* beta, int64_t M,
                     int64_t K, float eps, int dtype, void* y, hipStream_t stream);
+
+/* y[M][K] = x / sqrt(sum_k x^2 / K + eps) * gamma, Eq. (6) (eps as for
+   rms_linear_deferred).  Same rules and status codes as layernorm. */
+DN_API dn_status rmsnorm(const void* x, const void* gamma, int64_t M, int64_t K, float eps,
+                  int dtype, void* y, hipStream_t stream);
 
 /*
  * P[BH][Lq][Lk] = softmax of each row of S (Eq. (7) with the max subtraction).

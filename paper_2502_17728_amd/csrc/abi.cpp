@@ -83,8 +83,8 @@ DN_API dn_status ln_linear_prepare(const void* W, const void* gamma, const void*
     return st;
 }
 
-DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M, float eps, void* out,
-                                    hipStream_t stream) {
+static dn_status deferred_linear(const void* x, const ln_linear_weights* w, int64_t M, float eps, int rms,
+                                 void* out, hipStream_t stream) {
     if (!x || !w || !out || !w->packed || M < 1) return DN_ERR_INVALID_ARG;
     if (w->layout_version != DN_LN_LAYOUT_VERSION || w->K < 1 || w->N < 1 || !valid_dtype(w->dtype))
         return DN_ERR_INVALID_ARG;
@@ -99,7 +99,17 @@ DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, i
     const size_t pb = ln_linear_packed_bytes(K, N, dt);
     if (overlaps(out, ob, x, xb) || overlaps(out, ob, w->packed, pb)) return DN_ERR_INVALID_ARG;
     if (((M + 15) / 16) * ((N + 15) / 16) > kMaxGridX) return DN_ERR_UNSUPPORTED;
-    return from_hip(dn::launch_ln_linear_deferred(x, w->packed, M, K, N, dt, eps, out, stream));
+    return from_hip(dn::launch_ln_linear_deferred(x, w->packed, M, K, N, dt, eps, rms, out, stream));
+}
+
+DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M, float eps, void* out,
+                                    hipStream_t stream) {
+    return deferred_linear(x, w, M, eps, 0, out, stream);
+}
+
+DN_API dn_status rms_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M, float eps, void* out,
+                                     hipStream_t stream) {
+    return deferred_linear(x, w, M, eps, 1, out, stream);
 }
 
 DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq, int64_t Lk, int64_t d,
@@ -121,8 +131,8 @@ DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, i
     return from_hip(dn::launch_softmax_pv_deferred(S, V, BH, Lq, Lk, d, causal, out, stream));
 }
 
-DN_API dn_status layernorm(const void* x, const void* gamma, const void* beta, int64_t M, int64_t K, float eps,
-                           int dtype, void* y, hipStream_t stream) {
+static dn_status row_norm(const void* x, const void* gamma, const void* beta, int64_t M, int64_t K, float eps,
+                          int rms, int dtype, void* y, hipStream_t stream) {
     if (!x || !gamma || !y || M < 1 || K < 1 || !valid_dtype(dtype)) return DN_ERR_INVALID_ARG;
     if (!isfinite(eps) || eps < 0.f) return DN_ERR_INVALID_ARG;
     size_t xb;
@@ -133,7 +143,17 @@ DN_API dn_status layernorm(const void* x, const void* gamma, const void* beta, i
     if (overlaps(y, xb, x, xb) || overlaps(y, xb, gamma, K * es) || overlaps(y, xb, beta, K * es))
         return DN_ERR_INVALID_ARG;
     if ((M + 3) / 4 > kMaxGridX) return DN_ERR_UNSUPPORTED;
-    return from_hip(dn::launch_layernorm(x, gamma, beta, M, K, eps, dtype, y, stream));
+    return from_hip(dn::launch_layernorm(x, gamma, beta, M, K, eps, rms, dtype, y, stream));
+}
+
+DN_API dn_status layernorm(const void* x, const void* gamma, const void* beta, int64_t M, int64_t K, float eps,
+                           int dtype, void* y, hipStream_t stream) {
+    return row_norm(x, gamma, beta, M, K, eps, 0, dtype, y, stream);
+}
+
+DN_API dn_status rmsnorm(const void* x, const void* gamma, int64_t M, int64_t K, float eps, int dtype, void* y,
+                         hipStream_t stream) {
+    return row_norm(x, gamma, nullptr, M, K, eps, 1, dtype, y, stream);
 }
 
 DN_API dn_status softmax(const void* S, int64_t BH, int64_t Lq, int64_t Lk, int causal, int dtype, void* P,

@@ -47,11 +47,12 @@ __device__ __forceinline__ u32x4 pack16<float>(const float* f) {
 }
 
 // y = (x - mean) / sqrt(var + eps) * gamma + beta; lane chunk j covers elements
-// [(j*64 + lane) * EPL, +EPL).
+// [(j*64 + lane) * EPL, +EPL).  rms = 1: RMSNorm (Eq. (6)), the mean taken as 0,
+// so var is the mean square.
 template <class T, int NCH>
 __global__ __launch_bounds__(256) void layernorm_kernel(const T* __restrict__ x, const T* __restrict__ gamma,
                                                         const T* __restrict__ beta, int64_t M, int64_t K, float eps,
-                                                        T* __restrict__ y) {
+                                                        int rms, T* __restrict__ y) {
     constexpr int EPL = elem<T>::per16;
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -71,7 +72,7 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const T* __restrict__ x,
 #pragma unroll
         for (int e = 0; e < EPL; ++e) s += v[j][e];
     }
-    const float mean = wave_sum(s) / (float)K;
+    const float mean = rms ? 0.f : wave_sum(s) / (float)K;
     float ss = 0.f;
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
@@ -158,30 +159,30 @@ __global__ __launch_bounds__(256) void softmax_kernel(const __bf16* __restrict__
 }
 
 template <class T, int NCH>
-static hipError_t run_ln(const void* x, const void* g, const void* b, int64_t M, int64_t K, float eps, void* y,
-                         hipStream_t s) {
+static hipError_t run_ln(const void* x, const void* g, const void* b, int64_t M, int64_t K, float eps, int rms,
+                         void* y, hipStream_t s) {
     layernorm_kernel<T, NCH><<<dim3((unsigned)((M + 3) / 4)), 256, 0, s>>>((const T*)x, (const T*)g, (const T*)b, M,
-                                                                          K, eps, (T*)y);
+                                                                          K, eps, rms, (T*)y);
     return hipGetLastError();
 }
 
 template <class T>
-static hipError_t dispatch_ln(const void* x, const void* g, const void* b, int64_t M, int64_t K, float eps, void* y,
-                              hipStream_t s) {
+static hipError_t dispatch_ln(const void* x, const void* g, const void* b, int64_t M, int64_t K, float eps,
+                              int rms, void* y, hipStream_t s) {
     const int64_t per_chunk = 64 * elem<T>::per16;
     const int64_t nch = (K + per_chunk - 1) / per_chunk;
-    if (nch <= 1) return run_ln<T, 1>(x, g, b, M, K, eps, y, s);
-    if (nch <= 2) return run_ln<T, 2>(x, g, b, M, K, eps, y, s);
-    if (nch <= 4) return run_ln<T, 4>(x, g, b, M, K, eps, y, s);
-    if (nch <= 8) return run_ln<T, 8>(x, g, b, M, K, eps, y, s);
-    if (nch <= 16) return run_ln<T, 16>(x, g, b, M, K, eps, y, s);
-    return run_ln<T, 32>(x, g, b, M, K, eps, y, s);
+    if (nch <= 1) return run_ln<T, 1>(x, g, b, M, K, eps, rms, y, s);
+    if (nch <= 2) return run_ln<T, 2>(x, g, b, M, K, eps, rms, y, s);
+    if (nch <= 4) return run_ln<T, 4>(x, g, b, M, K, eps, rms, y, s);
+    if (nch <= 8) return run_ln<T, 8>(x, g, b, M, K, eps, rms, y, s);
+    if (nch <= 16) return run_ln<T, 16>(x, g, b, M, K, eps, rms, y, s);
+    return run_ln<T, 32>(x, g, b, M, K, eps, rms, y, s);
 }
 
 hipError_t launch_layernorm(const void* x, const void* gamma, const void* beta, int64_t M, int64_t K, float eps,
-                            int dtype, void* y, hipStream_t s) {
-    if (dtype == 0) return dispatch_ln<float>(x, gamma, beta, M, K, eps, y, s);
-    return dispatch_ln<__bf16>(x, gamma, beta, M, K, eps, y, s);
+                            int rms, int dtype, void* y, hipStream_t s) {
+    if (dtype == 0) return dispatch_ln<float>(x, gamma, beta, M, K, eps, rms, y, s);
+    return dispatch_ln<__bf16>(x, gamma, beta, M, K, eps, rms, y, s);
 }
 
 template <int NCH>

@@ -21,8 +21,9 @@ PackedLayout packed_layout(int64_t K, int64_t N, int dtype);
 hipError_t launch_ln_prepare(const void* W, const void* gamma, const void* beta, const void* bias,
                              int64_t K, int64_t N, int dtype, void* packed, hipStream_t s);
 
+// rms = 1: RMSNorm statistics (Eq. (6)), the mean taken as zero.
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K,
-                                     int64_t N, int dtype, float eps, void* out, hipStream_t s);
+                                     int64_t N, int dtype, float eps, int rms, void* out, hipStream_t s);
 
 hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t batch, int64_t M,
                        int64_t K, int64_t N, int b_layout, int a_causal, int dtype, void* C,
@@ -32,7 +33,7 @@ hipError_t launch_softmax_pv_deferred(const void* S, const void* V, int64_t BH, 
                                       int64_t Lk, int64_t d, int causal, void* out, hipStream_t s);
 
 hipError_t launch_layernorm(const void* x, const void* gamma, const void* beta, int64_t M,
-                            int64_t K, float eps, int dtype, void* y, hipStream_t s);
+                            int64_t K, float eps, int rms, int dtype, void* y, hipStream_t s);
 
 hipError_t launch_softmax(const void* S, int64_t BH, int64_t Lq, int64_t Lk, int causal, void* P,
                           hipStream_t s);

@@ -12,6 +12,10 @@
 // "collective sub-operation" running concurrently with the matmul -- and the
 // epilogue applies the normalization once before the single rounded store.
 //
+// Deferred RMSNorm -> Linear (Eq. (6)) is the same computation with the mean
+// taken as zero: rstd_m = 1/sqrt(sum x^2 / K + eps) and no mean_m * c_n term,
+// so every kernel here serves it through one flag (MainArgs::rms).
+//
 // Packed weight layout (written by the prepare kernels, read by every LN
 // kernel and by gemm with b_layout = 2).  W'^T is cut into 16-row x 64-byte
 // fragment chunks (16 output features x 32 bf16 / 16 fp32 of K), stored in
@@ -40,6 +44,7 @@ struct MainArgs {
     const float* c_col;   // LN: c[N]
     const float* b_col;   // LN: b[N]
     float eps;            // LN
+    int rms;              // LN: RMSNorm statistics (Eq. (6)): mean taken as 0
     const void* bias;     // GEMM: bias[N] in the element type, or null
     int a_causal;         // GEMM: A lower-triangular, skip k > row
 };
@@ -304,7 +309,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 a += red[(0 * WN + w) * BM + r];
                 b += red[(1 * WN + w) * BM + r];
             }
-            const float mean = a / (float)K;
+            const float mean = p.rms ? 0.f : a / (float)K;
             const float var = __builtin_fmaxf(b / (float)K - mean * mean, 0.f);
             row_mean[r] = mean;
             row_rstd[r] = 1.0f / __builtin_sqrtf(var + p.eps);
@@ -365,9 +370,9 @@ constexpr int kSgMfma = 0x008, kSgDsRead = 0x100;
 
 __device__ __forceinline__ int a_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-template <Epi EPI>
-__global__ __launch_bounds__(512) void pipe_kernel(MainArgs p, int group) {
-    constexpr int BM = 256, BN = 256, WM = 4, WN = 2, NW = 8;
+template <Epi EPI, int WM, int WN>
+__global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int group) {
+    constexpr int BM = 256, BN = 256, NW = WM * WN;
     constexpr int BK = 64;                        // bf16 elements per stage (128 B per row)
     constexpr int WTM = BM / WM, WTN = BN / WN;   // 64 x 128 per wave
     constexpr int FM = WTM / 16, FN = WTN / 16;   // 4 x 8 output fragments
@@ -537,7 +542,7 @@ __global__ __launch_bounds__(512) void pipe_kernel(MainArgs p, int group) {
             }
             __syncthreads();
             for (int r = tid; r < BM; r += NW * kWave) {
-                const float mean = row_s1[r] / (float)K;
+                const float mean = p.rms ? 0.f : row_s1[r] / (float)K;
                 const float var = __builtin_fmaxf(row_s2[r] / (float)K - mean * mean, 0.f);
                 row_s1[r] = mean;
                 row_s2[r] = 1.0f / __builtin_sqrtf(var + p.eps);
@@ -623,7 +628,8 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
                                                              const char* __restrict__ Wp, int64_t kchunks,
                                                              int64_t nblocks, const float* __restrict__ c_col,
                                                              const float* __restrict__ b_col, int M, int64_t K,
-                                                             int64_t N, float eps, __bf16* __restrict__ out) {
+                                                             int64_t N, float eps, int rms,
+                                                             __bf16* __restrict__ out) {
     __shared__ f32x4 part[2 + NC][KS][kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t nb0 = (int64_t)blockIdx.x * NC;
@@ -708,7 +714,7 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = 4 * (lane >> 4) + i;
-            const float mean = tot[1][i] / (float)K;
+            const float mean = rms ? 0.f : tot[1][i] / (float)K;
             const float var = __builtin_fmaxf(diag[i] / (float)K - mean * mean, 0.f);
             const float rstd = 1.0f / __builtin_sqrtf(var + eps);
             float v = __builtin_fmaf(-mean, cn, tot[0][i]);
@@ -820,12 +826,29 @@ static hipError_t run_main(const MainArgs& a, int64_t batch, hipStream_t s) {
 template <Epi EPI>
 static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
     const int64_t tm = (a.M + 255) / 256, tn = (a.N + 255) / 256;
-    // deferred LN: as many column tiles per workgroup as keeps at least 256
-    // workgroups (one per CU), so the row moments are reduced once per group
+    // deferred LN: each workgroup takes `group` column tiles of one row block and
+    // reduces the row moments once, on its first tile.  With one workgroup per CU
+    // the run takes about ceil(workgroups / 256) * group tile times; take the
+    // group that minimises that, and of equal ones the largest (fewest moment
+    // reductions).  384 tiles: group 2 (192 workgroups, 2 tile times) instead of
+    // group 1 (384 workgroups, also 2 tile times, twice the moment work).
     int64_t group = 1;
-    if (EPI == Epi::kLnDeferred) group = std::max<int64_t>(1, std::min<int64_t>(tn, tm * tn / 256));
+    if (EPI == Epi::kLnDeferred) {
+        int64_t best = -1;
+        for (int64_t g = 1; g <= tn; ++g) {
+            const int64_t span = (tm * ((tn + g - 1) / g) + 255) / 256 * g;
+            if (best < 0 || span <= best) {
+                best = span;
+                group = g;
+            }
+        }
+    }
     const int64_t wgs = tm * ((tn + group - 1) / group);
-    pipe_kernel<EPI><<<dim3((unsigned)wgs), 512, 0, s>>>(a, (int)group);
+#ifndef DN_PIPE_WM
+#define DN_PIPE_WM 4
+#define DN_PIPE_WN 2
+#endif
+    pipe_kernel<EPI, DN_PIPE_WM, DN_PIPE_WN><<<dim3((unsigned)wgs), DN_PIPE_WM * DN_PIPE_WN * kWave, 0, s>>>(a, (int)group);
     return hipGetLastError();
 }
 
@@ -855,9 +878,10 @@ static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_
 }
 
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
-                                     int dtype, float eps, void* out, hipStream_t s) {
+                                     int dtype, float eps, int rms, void* out, hipStream_t s) {
     MainArgs a = packed_args(x, packed, M, K, N, dtype, out);
     a.eps = eps;
+    a.rms = rms;
     if (dtype == 1 && M <= 16) {
         // Layouts measured on the 8192 x 28672 up-projection: up to 4 tokens the x
         // fragments are nearly free and 4 K-slices per column block stream best;
@@ -866,7 +890,7 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
         auto launch = [&](auto kern, int ks, int cols) {
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks,
-                                                            a.nblocks, a.c_col, a.b_col, (int)M, K, N, eps,
+                                                            a.nblocks, a.c_col, a.b_col, (int)M, K, N, eps, rms,
                                                             (__bf16*)out);
         };
         if (M <= 4)

@@ -15,6 +15,7 @@ variance v):
 
 - LayerNorm -> Linear: x ~ N(0, 1); gamma ~ U(0.5, 1.5); beta ~ N(0, 0.02);
   W[K, N] ~ N(0, 1/K); bias = 0 where a workload states it, else absent.
+  RMSNorm -> Linear (Eq. (6), Llama shapes): the same draws without beta.
   Optional outlier channels: a fixed set of channel indices (drawn once,
   without replacement) is scaled by a factor in every token, before rounding.
 - Softmax -> P.V: either S ~ N(0, s^2) directly (no mask), or S = Q K^T /
@@ -45,6 +46,7 @@ class LNWorkload:
     outliers: int = 0  # number of fixed outlier channels
     outlier_scale: float = 20.0
     zero_bias: bool = False  # workload states "bias 0"
+    norm: str = "layernorm"  # "layernorm" (Eq. (1)-(2)) | "rms" (Eq. (6))
 
     def flops(self, rows: Optional[int] = None) -> float:
         return 2.0 * (self.M if rows is None else rows) * self.K * self.N
@@ -85,8 +87,20 @@ def ln_ffn_decode(t: int) -> LNWorkload:
     return LNWorkload(f"ln_ffn_up_bf16_decode_t{t}_8192x28672", 5, t, 8192, 28672, "bf16")
 
 
+# RMSNorm -> Linear with Llama shapes: the fused QKV projection of an 8B-class
+# model with grouped-query attention (32 query + 2 x 8 key/value heads of 128
+# over hidden 4096), and the 70B-class FFN up-projection at decode.
+RMS_QKV = LNWorkload("rms_qkv_bf16_4096x4096x6144", 6, 4096, 4096, 6144, "bf16", outliers=8, norm="rms")
+
+
+def rms_ffn_decode(t: int) -> LNWorkload:
+    """Decode-sized RMSNorm -> FFN up-projection: x[t, 8192], W[8192, 28672]."""
+    return LNWorkload(f"rms_ffn_up_bf16_decode_t{t}_8192x28672", 7, t, 8192, 28672, "bf16", norm="rms")
+
+
 WORKLOADS = {w.name: w for w in (LN_F32_SMALL, SM_BF16_SMALL, LN_QKV, SM_CAUSAL, LN_FFN_PREFILL,
-                                 ln_ffn_decode(1), ln_ffn_decode(4), ln_ffn_decode(16))}
+                                 ln_ffn_decode(1), ln_ffn_decode(4), ln_ffn_decode(16),
+                                 RMS_QKV, rms_ffn_decode(1))}
 
 # tensor ids inside a workload's seed
 _X, _GAMMA, _BETA, _W, _OUTLIER_CH, _S, _Q, _KEY, _V = range(9)
@@ -124,17 +138,19 @@ def make_ln(w: LNWorkload, seed: int = 0, M: Optional[int] = None, x_extra: int 
     beta = _normal(_rng(seed, w.wid, _BETA), (w.K,), math.sqrt(0.02))
     W = _normal(_rng(seed, w.wid, _W), (w.K, w.N), 1.0 / math.sqrt(w.K))
     out = dict(x=to_storage(x, w.dtype), gamma=to_storage(gamma, w.dtype),
-               beta=to_storage(beta, w.dtype), W=to_storage(W, w.dtype), bias=None, eps=w.eps)
+               beta=to_storage(beta, w.dtype) if w.norm == "layernorm" else None,
+               W=to_storage(W, w.dtype), bias=None, eps=w.eps, norm=w.norm)
     if w.zero_bias:
         out["bias"] = torch.zeros(w.N, dtype=DTYPES[w.dtype])
     return out
 
 
 def make_ln_case(M: int, K: int, N: int, dtype: str, seed: int = 0, outliers: int = 0,
-                 zero_bias: bool = False, mean_offset: float = 0.0, eps: float = 1e-5) -> dict:
-    """A LayerNorm -> Linear case of any size with the same recipe (for parity tests)."""
+                 zero_bias: bool = False, mean_offset: float = 0.0, eps: float = 1e-5,
+                 norm: str = "layernorm") -> dict:
+    """A LayerNorm (or RMSNorm) -> Linear case of any size with the same recipe (for parity tests)."""
     w = LNWorkload(f"case_{M}x{K}x{N}_{dtype}", 100, M, K, N, dtype, eps=eps, outliers=outliers,
-                   zero_bias=zero_bias)
+                   zero_bias=zero_bias, norm=norm)
     out = make_ln(w, seed)
     if mean_offset:
         x = out["x"].float() + mean_offset

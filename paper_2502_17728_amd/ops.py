@@ -21,7 +21,8 @@ DN_F32, DN_BF16 = 0, 1
 DN_LN_LAYOUT_VERSION = 2
 STATUS = {0: "DN_OK", 1: "DN_ERR_INVALID_ARG", 2: "DN_ERR_UNSUPPORTED", 3: "DN_ERR_MISALIGNED", 4: "DN_ERR_HIP"}
 SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linear_prepare",
-           "ln_linear_deferred", "softmax_pv_deferred", "layernorm", "softmax", "gemm")
+           "ln_linear_deferred", "rms_linear_deferred", "softmax_pv_deferred", "layernorm", "rmsnorm",
+           "softmax", "gemm")
 
 
 class DNError(RuntimeError):
@@ -48,11 +49,14 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.ln_linear_prepare.argtypes = [vp, vp, vp, vp, i64, i64, i32, vp, ctypes.c_size_t,
                                       ctypes.POINTER(LnLinearWeights), vp]
     lib.ln_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
+    lib.rms_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
     lib.softmax_pv_deferred.argtypes = [vp, vp, i64, i64, i64, i64, i32, i32, vp, vp]
     lib.layernorm.argtypes = [vp, vp, vp, i64, i64, f32, i32, vp, vp]
+    lib.rmsnorm.argtypes = [vp, vp, i64, i64, f32, i32, vp, vp]
     lib.softmax.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp]
     lib.gemm.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, i32, i32, vp, vp]
-    for f in ("ln_linear_prepare", "ln_linear_deferred", "softmax_pv_deferred", "layernorm", "softmax", "gemm"):
+    for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "softmax_pv_deferred",
+              "layernorm", "rmsnorm", "softmax", "gemm"):
         getattr(lib, f).restype = i32
     return lib
 
@@ -139,6 +143,18 @@ def ln_linear_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
     return out
 
 
+def rms_linear_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
+                        out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    M = x.shape[0]
+    if out is None:
+        out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
+    if _dt(x) != w.desc.dtype:
+        raise TypeError("x dtype differs from the prepared weights")
+    _check("rms_linear_deferred", _lib.rms_linear_deferred(
+        _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(out, "out"), _stream(stream)))
+    return out
+
+
 def softmax_pv_deferred(S: torch.Tensor, V: torch.Tensor, causal: bool = False,
                         out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     BH, Lq, Lk = S.shape
@@ -157,6 +173,16 @@ def layernorm(x: torch.Tensor, gamma: torch.Tensor, beta: Optional[torch.Tensor]
         out = torch.empty_like(x)
     _check("layernorm", _lib.layernorm(_dev(x, "x"), _dev(gamma, "gamma"), _dev(beta, "beta"), M, K, eps,
                                        _dt(x), _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def rmsnorm(x: torch.Tensor, gamma: torch.Tensor, eps: float = 1e-5, out: Optional[torch.Tensor] = None,
+            stream=None) -> torch.Tensor:
+    M, K = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    _check("rmsnorm", _lib.rmsnorm(_dev(x, "x"), _dev(gamma, "gamma"), M, K, eps, _dt(x), _dev(out, "out"),
+                                   _stream(stream)))
     return out
 
 

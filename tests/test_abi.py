@@ -52,8 +52,9 @@ def _w(K=64, N=64, dtype=1, version=2, packed=P3):
     return ops.LnLinearWeights(K, N, dtype, version, packed)
 
 
-def test_ln_linear_deferred_validation():
-    f = ops._lib.ln_linear_deferred
+@pytest.mark.parametrize("entry", ["ln_linear_deferred", "rms_linear_deferred"])
+def test_ln_linear_deferred_validation(entry):
+    f = getattr(ops._lib, entry)
     w = _w()
     assert f(None, ctypes.byref(w), 4, 1e-5, P2, None) == INVALID
     assert f(P, None, 4, 1e-5, P2, None) == INVALID
@@ -108,6 +109,13 @@ def test_unfused_validation():
     assert ln(P, P2, None, 4, 1 << 20, 1e-5, 1, P3, None) == UNSUPPORTED  # row kept in registers
     assert ln(P, P2, P + 8, 4, 64, 1e-5, 1, P3, None) == MISALIGNED
     assert ln(P, P2, None, 4, 64, 1e-5, 1, P, None) == INVALID           # in place not allowed
+    rms = ops._lib.rmsnorm
+    assert rms(None, P2, 4, 64, 1e-5, 1, P3, None) == INVALID
+    assert rms(P, P2, 4, 64, float("nan"), 1, P3, None) == INVALID
+    assert rms(P, P2, 0, 64, 1e-5, 1, P3, None) == INVALID
+    assert rms(P, P2, 4, 20, 1e-5, 1, P3, None) == UNSUPPORTED
+    assert rms(P, P2 + 8, 4, 64, 1e-5, 1, P3, None) == MISALIGNED
+    assert rms(P, P2, 4, 64, 1e-5, 1, P + 64, None) == INVALID         # y overlaps x
     assert sm(P, 1, 64, 64, 3, 1, P2, None) == INVALID
     assert sm(P, 1, 64, 32, 1, 1, P2, None) == INVALID
     assert sm(P, 1, 64, 64, 0, 0, P2, None) == UNSUPPORTED

@@ -24,15 +24,21 @@ def ops():
 
 
 def _ln_check(ops, case, rows=None, tol=None):
+    """LayerNorm -> Linear, or RMSNorm -> Linear when case["norm"] == "rms"."""
+    rms = case.get("norm") == "rms"
     x, W = cuda(case["x"]), cuda(case["W"])
     w = ops.ln_linear_prepare(W, cuda(case["gamma"]), cuda(case["beta"]), cuda(case["bias"]))
-    out = ops.ln_linear_deferred(x, w, case["eps"])
+    out = (ops.rms_linear_deferred if rms else ops.ln_linear_deferred)(x, w, case["eps"])
     torch.cuda.synchronize()
     xs = case["x"] if rows is None else case["x"][torch.as_tensor(rows)]
-    ref = oracle.ln_linear(xs, case["gamma"], case["beta"], case["W"], case["bias"], case["eps"])
+    if rms:
+        ref = oracle.rms_linear(xs, case["gamma"], case["W"], case["bias"], case["eps"], beta=case["beta"])
+    else:
+        ref = oracle.ln_linear(xs, case["gamma"], case["beta"], case["W"], case["bias"], case["eps"])
     got = out.cpu() if rows is None else out.cpu()[torch.as_tensor(rows)]
     err = rowwise_rel_err(got, ref)
-    print(f"ln_linear_deferred {tuple(case['x'].shape)}x{tuple(case['W'].shape)} {case['x'].dtype}: err={err:.3e}")
+    name = "rms_linear_deferred" if rms else "ln_linear_deferred"
+    print(f"{name} {tuple(case['x'].shape)}x{tuple(case['W'].shape)} {case['x'].dtype}: err={err:.3e}")
     assert err <= (tol or TOL[case["x"].dtype]), err
     return out, w
 
@@ -144,6 +150,56 @@ def test_ln_linear_guard_band(ops):
     assert (buf[:512] == 7.0).all() and (buf[-512:] == 7.0).all()
 
 
+# ---------------------------------------------------------------------------- RMSNorm -> Linear
+@pytest.mark.parametrize("M,K,N", [(37, 104, 72), (1, 8, 8), (300, 512, 200)])
+def test_rms_linear_f32_ragged(ops, M, K, N):
+    _ln_check(ops, I.make_ln_case(M, K, N, "f32", seed=M + 1, norm="rms"))
+
+
+@pytest.mark.parametrize("M,K,N", [(17, 64, 136), (257, 1024, 264), (128, 768, 3072), (1, 8, 8)])
+def test_rms_linear_bf16_ragged(ops, M, K, N):
+    _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M + K + 1, norm="rms"))
+
+
+@pytest.mark.parametrize("M", [1, 5, 16])
+@pytest.mark.parametrize("K,N", [(1024, 520), (8, 24)])
+def test_rms_linear_bf16_decode_shapes(ops, M, K, N):
+    _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M * 5 + 2, outliers=4, norm="rms"))
+
+
+@pytest.mark.parametrize("M,K,N", [(4000, 544, 4104), (4000, 520, 4104)])
+def test_rms_linear_bf16_large_tiles_sampled(ops, M, K, N):
+    case = I.make_ln_case(M, K, N, "bf16", seed=M % 89, outliers=3, norm="rms")
+    _ln_check(ops, case, rows=I.sample_rows(M, 40, seed=4))
+
+
+def test_rms_linear_qkv_workload_sampled(ops):
+    w = I.RMS_QKV
+    _ln_check(ops, I.make_ln(w), rows=I.sample_rows(w.M, 24, seed=5))
+
+
+def test_rms_linear_ffn_decode_workload(ops):
+    _ln_check(ops, I.make_ln(I.rms_ffn_decode(1)))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rms_linear_with_beta_and_bias(ops, dtype):
+    # a shift folded at prepare adds beta W for every row, as the oracle's optional beta does
+    case = I.make_ln_case(70, 256, 136, dtype, seed=8, norm="rms")
+    case["beta"] = I.make_ln_case(1, 256, 8, dtype, seed=9)["beta"]
+    case["bias"] = I.make_ln_case(1, 136, 8, dtype, seed=10)["beta"]
+    _ln_check(ops, case)
+
+
+def test_rms_linear_zero_rows_give_b(ops):
+    # an all-zero row: sum x^2 = 0, rstd = 1/sqrt(eps) times acc = 0 -> out = b (= bias here)
+    case = I.make_ln_case(40, 512, 264, "bf16", seed=14, norm="rms")
+    case["x"][3:9] = 0
+    case["bias"] = I.make_ln_case(1, 264, 8, "bf16", seed=15)["beta"]
+    out, _ = _ln_check(ops, case)
+    assert torch.equal(out.cpu()[3:9], case["bias"].expand(6, -1))
+
+
 # ---------------------------------------------------------------------------- Softmax -> P.V
 def _sm_check(ops, case, rows=None):
     S, V = case["S"], case["V"]
@@ -225,6 +281,15 @@ def test_layernorm_unfused(ops, dtype):
     assert err <= TOL[case["x"].dtype] / (4 if dtype == "bf16" else 1), err
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rmsnorm_unfused(ops, dtype):
+    case = I.make_ln_case(77, 1032, 8, dtype, seed=5, outliers=2, norm="rms")
+    y = ops.rmsnorm(cuda(case["x"]), cuda(case["gamma"]), case["eps"])
+    ref = oracle.rmsnorm(case["x"], case["gamma"], case["eps"])
+    err = rowwise_rel_err(y.cpu(), ref)
+    assert err <= TOL[case["x"].dtype] / (4 if dtype == "bf16" else 1), err
+
+
 @pytest.mark.parametrize("causal", [0, 1])
 def test_softmax_unfused(ops, causal):
     case = I.make_sm_case(2, 136, 64, bool(causal), seed=4)
@@ -276,6 +341,13 @@ def test_unfused_chains_match_deferred(ops):
     ref = oracle.ln_linear(case["x"], case["gamma"], case["beta"], case["W"], None, case["eps"])
     assert rowwise_rel_err(unfused.cpu(), ref) <= TOL[torch.bfloat16]
     assert rowwise_rel_err(fused.cpu(), oracle.to_f64(unfused.cpu())) <= TOL[torch.bfloat16]
+    rfused = ops.rms_linear_deferred(x, ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"])))
+    y = ops.rmsnorm(x, cuda(case["gamma"]))
+    runfused = ops.gemm(y, ops.ln_linear_prepare(cuda(case["W"]), torch.ones(512, dtype=torch.bfloat16,
+                                                                            device="cuda")))
+    rref = oracle.rms_linear(case["x"], case["gamma"], case["W"], None, case["eps"])
+    assert rowwise_rel_err(runfused.cpu(), rref) <= TOL[torch.bfloat16]
+    assert rowwise_rel_err(rfused.cpu(), rref) <= TOL[torch.bfloat16]
     sm = I.make_sm_case(2, 256, 128, True, seed=13)
     S, V = cuda(sm["S"]), cuda(sm["V"])
     P = ops.softmax(S, causal=2)
