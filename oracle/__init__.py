@@ -49,10 +49,11 @@ def _load():
         lib.oracle_ln_linear.argtypes = [d, d, d, d, d, i64, i64, i64, ctypes.c_double, d, i32]
         lib.oracle_rmsnorm.argtypes = [d, d, d, i64, i64, ctypes.c_double, d, i32]
         lib.oracle_rms_linear.argtypes = [d, d, d, d, d, i64, i64, i64, ctypes.c_double, d, i32]
+        lib.oracle_rms_swiglu.argtypes = [d, d, d, d, i64, i64, i64, ctypes.c_double, d, i32]
         lib.oracle_softmax.argtypes = [d, d, i64, i64, d, i32]
         lib.oracle_softmax_pv.argtypes = [d, d, d, d, i64, i64, i64, d, i32]
         for f in ("oracle_layernorm", "oracle_linear", "oracle_ln_linear", "oracle_rmsnorm",
-                  "oracle_rms_linear", "oracle_softmax", "oracle_softmax_pv"):
+                  "oracle_rms_linear", "oracle_rms_swiglu", "oracle_softmax", "oracle_softmax_pv"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -157,6 +158,20 @@ def rms_linear(x, gamma, W, bias, eps, beta=None, nthreads=None):
     _check(_load().oracle_rms_linear(_ptr(x), _ptr(g), _ptr(b), _ptr(W), _ptr(bb), M, K, N,
                                      float(eps), _ptr(out), _threads(nthreads)), "rms_linear")
     return out
+
+
+def rms_swiglu(x, gamma, Wg, Wu, eps, nthreads=None):
+    """SiLU(RMSNorm(x) . Wg) * (RMSNorm(x) . Wu) for x[M, K], Wg/Wu[K, N]; returns h[M, N] fp64."""
+    x = to_f64(x)
+    M, K = x.shape
+    Wg, Wu = to_f64(Wg), to_f64(Wu)
+    N = Wg.shape[1]
+    assert Wg.shape == (K, N) and Wu.shape == (K, N), (x.shape, Wg.shape, Wu.shape)
+    g = to_f64(gamma).reshape(K)
+    h = np.empty((M, N), np.float64)
+    _check(_load().oracle_rms_swiglu(_ptr(x), _ptr(g), _ptr(Wg), _ptr(Wu), M, K, N, float(eps), _ptr(h),
+                                     _threads(nthreads)), "rms_swiglu")
+    return h
 
 
 def _rows_meta(R, head, qpos):

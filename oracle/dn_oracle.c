@@ -17,6 +17,9 @@
  *   - Linear layer,         Eq. (4): out = y F (+ bias), F stored as W[K][N].
  *   - RMSNorm,              Eq. (6): y = x / sqrt(x x^T / n + eps) * gamma (+ beta),
  *                           and RMSNorm followed by the linear layer.
+ *   - The Llama MLP input stage that the same subsubsection fuses: RMSNorm,
+ *     the gate and up projections, and h = SiLU(y Wg) * (y Wu) with
+ *     SiLU(z) = z / (1 + exp(-z)).
  *   - Softmax then values,  Eq. (7) with the footnote's max subtraction:
  *       m = max_j x_j, e_j = exp(x_j - m), y_j = e_j / sum_i e_i, out = y V.
  *
@@ -256,6 +259,47 @@ int oracle_rms_linear(const double* x, const double* gamma, const double* beta,
     if (!x || !gamma || !W || !out || M < 1 || K < 1 || N < 1) return -1;
     lnlin_ctx c = {x, gamma, beta, W, bias, K, N, eps, out};
     run_rows(rmslin_rows, &c, M, nthreads);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* RMSNorm, then the gated MLP input stage of a Llama block: the gate and up */
+/* projections of y, combined as SiLU(gate) * up (element-wise).             */
+
+static double silu(double z) { return z / (1.0 + exp(-z)); }
+
+typedef struct {
+    const double *x, *gamma, *Wg, *Wu;
+    int64_t K, N;
+    double eps;
+    double* h;
+} swiglu_ctx;
+
+static void swiglu_rows(void* p, int64_t r0, int64_t r1) {
+    swiglu_ctx* c = (swiglu_ctx*)p;
+    double* y = (double*)malloc((size_t)c->K * sizeof(double));
+    double* g = (double*)malloc((size_t)c->N * sizeof(double));
+    double* u = (double*)malloc((size_t)c->N * sizeof(double));
+    if (y && g && u) {
+        for (int64_t m = r0; m < r1; ++m) {
+            rmsnorm_row(c->x + m * c->K, c->K, c->gamma, NULL, c->eps, y);
+            linear_row(y, c->Wg, NULL, c->K, c->N, g);
+            linear_row(y, c->Wu, NULL, c->K, c->N, u);
+            double* h = c->h + m * c->N;
+            for (int64_t n = 0; n < c->N; ++n) h[n] = silu(g[n]) * u[n];
+        }
+    }
+    free(u);
+    free(g);
+    free(y);
+}
+
+int oracle_rms_swiglu(const double* x, const double* gamma, const double* Wg,
+                      const double* Wu, int64_t M, int64_t K, int64_t N, double eps,
+                      double* h, int nthreads) {
+    if (!x || !gamma || !Wg || !Wu || !h || M < 1 || K < 1 || N < 1) return -1;
+    swiglu_ctx c = {x, gamma, Wg, Wu, K, N, eps, h};
+    run_rows(swiglu_rows, &c, M, nthreads);
     return 0;
 }
 

@@ -38,6 +38,13 @@ int oracle_rms_linear(const double* x, const double* gamma, const double* beta,
                       const double* W, const double* bias, int64_t M, int64_t K,
                       int64_t N, double eps, double* out, int nthreads);
 
+/* Llama MLP input stage (the subsubsection on RMSNorm in Llama models):
+   y = RMSNorm(x[M][K]) (Eq. (6)), h[M][N] = SiLU(y . Wg) * (y . Wu) element-wise,
+   SiLU(z) = z / (1 + exp(-z)); Wg, Wu are [K][N]. */
+int oracle_rms_swiglu(const double* x, const double* gamma, const double* Wg,
+                      const double* Wu, int64_t M, int64_t K, int64_t N, double eps,
+                      double* h, int nthreads);
+
 /* Eq. (7) softmax of R rows of length Lk.  qpos[r] >= 0 keeps keys j <= qpos[r]
    (causal) and writes 0 beyond; qpos NULL or qpos[r] < 0 keeps every key. */
 int oracle_softmax(const double* S, const int64_t* qpos, int64_t R, int64_t Lk,

@@ -5,7 +5,7 @@ Before it may judge the GPU path it is tied here to things other than itself:
 
 - hand-worked examples stored in ``tests/golden`` (exact values);
 - closed forms and special cases (K = 2, constant rows, one-hot scores, V = I);
-- library routines: ``torch.nn.functional.layer_norm``, ``rms_norm`` and ``torch.softmax``
+- library routines: ``torch.nn.functional.layer_norm``, ``rms_norm``, ``silu`` and ``torch.softmax``
   in fp64, which the oracle does not call;
 - the paper's fused forms, Eq. (5) and Eq. (8), evaluated independently here
   with numpy, which reach the same result by different arithmetic;
@@ -195,6 +195,17 @@ def test_rms_linear_matches_torch_rms_norm(M, K, N, eps):
     np.testing.assert_allclose(oracle.rms_linear(x, gamma, W, bias, eps), want, rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("M,K,N,eps", [(5, 7, 3, 1e-5), (9, 64, 17, 0.1)])
+def test_rms_swiglu_matches_torch(M, K, N, eps):
+    rng = np.random.default_rng(M * K + N)
+    x = rng.normal(size=(M, K)) * 2 + 0.3
+    gamma = rng.uniform(0.5, 1.5, K)
+    Wg, Wu = rng.normal(size=(K, N)) * 2, rng.normal(size=(K, N))
+    y = torch.nn.functional.rms_norm(torch.from_numpy(x), (K,), torch.from_numpy(gamma), eps)
+    want = torch.nn.functional.silu(y @ torch.from_numpy(Wg)) * (y @ torch.from_numpy(Wu))
+    np.testing.assert_allclose(oracle.rms_swiglu(x, gamma, Wg, Wu, eps), want.numpy(), rtol=1e-12, atol=1e-12)
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_softmax_pv_matches_torch_softmax(causal):
     rng = np.random.default_rng(11)
@@ -319,6 +330,38 @@ def test_rmsnorm_pre_affine_mean_square_and_scale_invariance():
                                rtol=1e-12, atol=1e-13)
 
 
+def test_silu_closed_forms():
+    # K = 1, x = 1, eps = 0: y = gamma exactly, so g = gamma * Wg and u = gamma * Wu.
+    # SiLU(ln a) = ln a * a / (1 + a): ln 3 -> 0.75 ln 3, -ln 3 -> -0.25 ln 3
+    l3 = math.log(3.0)
+    h = oracle.rms_swiglu(np.ones((1, 1)), np.array([l3]), np.array([[1.0, -1.0]]), np.array([[2.0, 2.0]]), 0.0)
+    np.testing.assert_allclose(h[0], [0.75 * l3 * 2 * l3, -0.25 * l3 * 2 * l3], rtol=4e-16)
+    # a zero gate gives exactly zero; a large gate passes through (SiLU(z) -> z)
+    rng = np.random.default_rng(37)
+    x, g = rng.normal(size=(4, 16)), rng.uniform(0.5, 1.5, 16)
+    Wu = rng.normal(size=(16, 5))
+    assert (oracle.rms_swiglu(x, g, np.zeros((16, 5)), Wu, 1e-5) == 0).all()
+    big = oracle.rms_swiglu(np.ones((1, 1)), np.array([1.0]), np.array([[60.0]]), np.array([[1.0]]), 0.0)
+    assert big[0, 0] == 60.0
+
+
+def test_swiglu_odd_part_identity():
+    # SiLU(z) - SiLU(-z) = z, so h(Wg) - h(-Wg) = (y Wg) * (y Wu), with y Wg and y Wu from the
+    # pinned RMSNorm -> Linear; a sign slip inside exp(-z) or a swapped gate/up fails this
+    rng = np.random.default_rng(38)
+    M, K, N, eps = 6, 24, 7, 1e-3
+    x, gamma = rng.normal(size=(M, K)) + 0.2, rng.uniform(0.5, 1.5, K)
+    Wg, Wu = rng.normal(size=(K, N)), rng.normal(size=(K, N))
+    d = oracle.rms_swiglu(x, gamma, Wg, Wu, eps) - oracle.rms_swiglu(x, gamma, -Wg, Wu, eps)
+    want = oracle.rms_linear(x, gamma, Wg, None, eps) * oracle.rms_linear(x, gamma, Wu, None, eps)
+    np.testing.assert_allclose(d, want, rtol=1e-12, atol=1e-13)
+    # and the deferred form: SiLU(r (x Gamma Wg)) * (r (x Gamma Wu)), r applied before the SiLU
+    r = 1.0 / np.sqrt((x * x).mean(1) + eps)
+    gg, uu = r[:, None] * (x @ (np.diag(gamma) @ Wg)), r[:, None] * (x @ (np.diag(gamma) @ Wu))
+    np.testing.assert_allclose(oracle.rms_swiglu(x, gamma, Wg, Wu, eps), gg / (1 + np.exp(-gg)) * uu,
+                               rtol=1e-12, atol=1e-13)
+
+
 def test_softmax_rows_sum_to_one_and_shift_invariance():
     rng = np.random.default_rng(33)
     L = 50
@@ -379,6 +422,17 @@ def test_bruteforce_mpmath_tiny():
         y = [xs[k] / rms * mp.mpf(float(g[k])) + mp.mpf(float(b[k])) for k in range(K)]
         for n in range(N):
             ref = mp.fsum(y[k] * mp.mpf(float(W[k, n])) for k in range(K)) + mp.mpf(float(bias[n]))
+            assert abs(float(ref) - got[m, n]) <= 1e-13 * max(1.0, abs(float(ref)))
+    Wu = rng.normal(size=(K, N))
+    got = oracle.rms_swiglu(x, g, W, Wu, eps)
+    for m in range(M):
+        xs = [mp.mpf(float(v)) for v in x[m]]
+        rms = mp.sqrt(mp.fsum(v * v for v in xs) / K + mp.mpf(eps))
+        y = [xs[k] / rms * mp.mpf(float(g[k])) for k in range(K)]
+        for n in range(N):
+            gate = mp.fsum(y[k] * mp.mpf(float(W[k, n])) for k in range(K))
+            up = mp.fsum(y[k] * mp.mpf(float(Wu[k, n])) for k in range(K))
+            ref = gate / (1 + mp.exp(-gate)) * up
             assert abs(float(ref) - got[m, n]) <= 1e-13 * max(1.0, abs(float(ref)))
     L, d = 5, 3
     S, V = rng.normal(size=(L, L)) * 2, rng.normal(size=(L, d))
