@@ -47,7 +47,8 @@ PEAK_HBM_GBS = 8000.0       # HBM3E
 # the bench reports null once they differ.
 KERNEL_SOURCES = {"softmax_pv_deferred": ("softmax_pv.hip", "dn_device.hpp"),
                   "ln_linear_deferred": ("ln_gemm.hip", "dn_device.hpp"),
-                  "rms_linear_deferred": ("ln_gemm.hip", "dn_device.hpp")}
+                  "rms_linear_deferred": ("ln_gemm.hip", "dn_device.hpp"),
+                  "rms_swiglu_deferred": ("ln_gemm.hip", "dn_device.hpp")}
 TRAFFIC = {
     ("softmax_pv_deferred", "causal_softmax_pv_bf16_32x8192x8192_d128"): {
         "sha256": ("4cb5880e7992356ce9815f38539bb72117dc54ee40675acb45549ac65f640d11",
@@ -88,7 +89,7 @@ def parse():
     ap.add_argument("--workload", default="layer",
                     choices=["layer", "small", "ln_qkv", "causal_softmax_pv", "ffn_prefill",
                              "ffn_decode_t1", "ffn_decode_t4", "ffn_decode_t16", "rms_qkv",
-                             "rms_ffn_decode_t1"])
+                             "rms_ffn_decode_t1", "swiglu_prefill", "swiglu_decode_t1"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None)
@@ -167,6 +168,55 @@ class LNSite:
         return dt, len(idx) / self.w.M, f"{len(idx)} of {self.w.M} {norm}->Linear rows"
 
 
+class SwiGLUSite:
+    """RMSNorm -> gate and up projections -> SiLU(gate) * up, the Llama MLP input stage."""
+    kernel = "rms_swiglu_deferred"
+
+    def __init__(self, ops, I, w):
+        self.w = w
+        self.case = I.make_swiglu(w)
+        c = self.case
+        self.x = c["x"].cuda()
+        Wg, Wu, self.g = c["Wg"].cuda(), c["Wu"].cuda(), c["gamma"].cuda()
+        self.prep = ops.swiglu_prepare(Wg, Wu, self.g)
+        one = torch.ones(w.K, dtype=Wg.dtype, device="cuda")
+        self.Wg_pk, self.Wu_pk = ops.ln_linear_prepare(Wg, one), ops.ln_linear_prepare(Wu, one)
+        del Wg, Wu
+        self.out = torch.empty((w.M, w.N), dtype=self.x.dtype, device="cuda")
+        self.y = torch.empty_like(self.x)
+        self.gate = torch.empty((1, w.M, w.N), dtype=self.x.dtype, device="cuda")
+        self.up = torch.empty_like(self.gate)
+        self.ops = ops
+        torch.cuda.synchronize()
+
+    def fused(self):
+        self.ops.rms_swiglu_deferred(self.x, self.prep, self.w.eps, out=self.out)
+
+    def unfused(self):
+        self.ops.rmsnorm(self.x, self.g, self.w.eps, out=self.y)
+        self.ops.gemm(self.y, self.Wg_pk, out=self.gate)
+        self.ops.gemm(self.y, self.Wu_pk, out=self.up)
+        self.ops.silu_mul(self.gate, self.up, out=self.out.view(1, self.w.M, self.w.N))
+
+    def flops(self):
+        return 2.0 * self.w.flops()
+
+    def bytes(self):
+        w = self.w
+        return 2.0 * (w.M * w.K + 2 * w.K * w.N + w.M * w.N) + 16.0 * w.N
+
+    def peak_tflops(self):
+        return PEAK_BF16_TFLOPS
+
+    def oracle_sample(self, oracle, I, threads, rows):
+        idx = I.sample_rows(self.w.M, rows, seed=9)
+        c = self.case
+        t0 = time.perf_counter()
+        oracle.rms_swiglu(c["x"][torch.as_tensor(idx)], c["gamma"], c["Wg"], c["Wu"], c["eps"], nthreads=threads)
+        dt = time.perf_counter() - t0
+        return dt, len(idx) / self.w.M, f"{len(idx)} of {self.w.M} RMSNorm->SwiGLU rows"
+
+
 class SMSite:
     def __init__(self, ops, I, w):
         self.w = w
@@ -227,6 +277,11 @@ def build_sites(ops, I, name):
         return [LNSite(ops, I, I.LN_FFN_PREFILL)], I.LN_FFN_PREFILL.name
     if name == "rms_qkv":
         return [LNSite(ops, I, I.RMS_QKV)], I.RMS_QKV.name
+    if name == "swiglu_prefill":
+        return [SwiGLUSite(ops, I, I.SWIGLU_PREFILL)], I.SWIGLU_PREFILL.name
+    if name == "swiglu_decode_t1":
+        w = I.swiglu_decode(1)
+        return [SwiGLUSite(ops, I, w)], w.name
     t = int(name.rsplit("t", 1)[1])
     w = I.rms_ffn_decode(t) if name.startswith("rms_") else I.ln_ffn_decode(t)
     return [LNSite(ops, I, w)], w.name
@@ -305,7 +360,7 @@ def main():
     kernels = {}
     dom = max(range(len(sites)), key=lambda i: per[i])
     for i, s in enumerate(sites):
-        name = s.kernel if isinstance(s, LNSite) else "softmax_pv_deferred"
+        name = s.kernel if isinstance(s, (LNSite, SwiGLUSite)) else "softmax_pv_deferred"
         tf = s.flops() / (per[i] * 1e-3) / 1e12
         gbs = s.bytes() / (per[i] * 1e-3) / 1e9
         k = {"workload": s.w.name, "ms": round(per[i], 4), "tflops": round(tf, 2),
@@ -337,7 +392,7 @@ def main():
 
     d = sites[dom]
     dname = list(kernels)[dom]
-    hbm_bound = isinstance(d, SMSite) or (isinstance(d, LNSite) and d.w.M <= 16)
+    hbm_bound = isinstance(d, SMSite) or (isinstance(d, (LNSite, SwiGLUSite)) and d.w.M <= 16)
     if hbm_bound:
         ach = d.bytes() / (per[dom] * 1e-3) / 1e9
         roof = {"kernel": dname, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
@@ -357,8 +412,8 @@ def main():
         t_cpu, frac_cpu, descs = 0.0, 0.0, []
         extrap = 0.0
         for s in sites:
-            rows = 16 if isinstance(s, LNSite) and s.w.K * s.w.N > 1e8 else 64
-            if isinstance(s, LNSite) and s.w.M <= 16:
+            rows = 16 if isinstance(s, (LNSite, SwiGLUSite)) and s.w.K * s.w.N > 1e8 else 64
+            if isinstance(s, (LNSite, SwiGLUSite)) and s.w.M <= 16:
                 rows = s.w.M
             if isinstance(s, SMSite):
                 rows = 1024 if s.w.L >= 4096 else 2048

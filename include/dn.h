@@ -119,6 +119,41 @@ DN_API dn_status rms_linear_deferred(const void* x, const ln_linear_weights* w, 
                               float eps, void* out, hipStream_t stream);
 
 /* ======================================================================= */
+/* RMSNorm -> gated MLP input (SwiGLU), deferred                            */
+/* ======================================================================= */
+
+/*
+ * The Llama MLP input stage (Sec. II-A, subsubsection on RMSNorm in Llama
+ * models, which fuses the up-projection and gating): y = RMSNorm(x) (Eq. (6)),
+ * h = SiLU(y Wg) * (y Wu) element-wise, SiLU(z) = z / (1 + e^-z).
+ * Deferred: both products run on the MFMA over the un-normalized x, each x
+ * fragment feeding the gate and the up columns, with sum x^2 reduced
+ * concurrently; the epilogue applies rstd to both products (before the SiLU,
+ * which is not homogeneous, so the deferral ends there) and writes h once.
+ *
+ * swiglu_prepare folds gamma into both [K][N] weights and packs them into one
+ * buffer of swiglu_packed_bytes(K, N, dtype) bytes (256-byte aligned device
+ * memory): Wg' and Wu' in the fragment-chunk layout of ln_linear_prepare,
+ * interleaved by 16-feature blocks (block 2j = gate features 16j.., block
+ * 2j+1 = up features 16j..), with c and b (zero: no shift, no bias) in the
+ * same interleaved order.  *w_out gets N (the output features) and
+ * layout_version DN_SWIGLU_LAYOUT_VERSION; only rms_swiglu_deferred takes it.
+ * rms_swiglu_deferred writes h[M][N] in w->dtype; eps as for
+ * rms_linear_deferred.  Status codes and alignment rules as for the
+ * LayerNorm -> Linear calls.
+ */
+#define DN_SWIGLU_LAYOUT_VERSION 0x102
+
+DN_API size_t swiglu_packed_bytes(int64_t K, int64_t N, int dtype);
+
+DN_API dn_status swiglu_prepare(const void* W_gate, const void* W_up, const void* gamma,
+                         int64_t K, int64_t N, int dtype, void* packed, size_t packed_bytes,
+                         ln_linear_weights* w_out, hipStream_t stream);
+
+DN_API dn_status rms_swiglu_deferred(const void* x, const ln_linear_weights* w, int64_t M,
+                              float eps, void* h, hipStream_t stream);
+
+/* ======================================================================= */
 /* Softmax -> P.V, deferred (Sec. II-B, Eq. (7), (8) and its footnote)      */
 /* ======================================================================= */
 
@@ -151,6 +186,11 @@ DN_API dn_status layernorm(const void* x, const void* gamma, const void* beta, i
    rms_linear_deferred).  Same rules and status codes as layernorm. */
 DN_API dn_status rmsnorm(const void* x, const void* gamma, int64_t M, int64_t K, float eps,
                   int dtype, void* y, hipStream_t stream);
+
+/* h[i] = SiLU(g[i]) * u[i] for count elements (count a multiple of 8); the
+   conventional last step of the gated MLP input.  h must not overlap g or u. */
+DN_API dn_status silu_mul(const void* g, const void* u, int64_t count, int dtype, void* h,
+                   hipStream_t stream);
 
 /*
  * P[BH][Lq][Lk] = softmax of each row of S (Eq. (7) with the max subtraction).

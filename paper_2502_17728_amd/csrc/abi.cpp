@@ -112,6 +112,57 @@ DN_API dn_status rms_linear_deferred(const void* x, const ln_linear_weights* w, 
     return deferred_linear(x, w, M, eps, 1, out, stream);
 }
 
+DN_API size_t swiglu_packed_bytes(int64_t K, int64_t N, int dtype) {
+    size_t wt;
+    if (K < 1 || N < 1 || !valid_dtype(dtype) || !bytes_of(K, 2 * N + 32, (int64_t)esize(dtype), &wt)) return 0;
+    return dn::swiglu_layout(K, N, dtype).total;
+}
+
+DN_API dn_status swiglu_prepare(const void* W_gate, const void* W_up, const void* gamma, int64_t K, int64_t N,
+                                int dtype, void* packed, size_t packed_bytes, ln_linear_weights* w_out,
+                                hipStream_t stream) {
+    if (!W_gate || !W_up || !gamma || !packed || !w_out || K < 1 || N < 1 || !valid_dtype(dtype))
+        return DN_ERR_INVALID_ARG;
+    const size_t need = swiglu_packed_bytes(K, N, dtype);
+    if (need == 0 || packed_bytes < need) return DN_ERR_INVALID_ARG;
+    if (K % 8 || N % 8) return DN_ERR_UNSUPPORTED;
+    if (!aligned(W_gate, 16) || !aligned(W_up, 16) || !aligned(gamma, 16) || !aligned(packed, 256))
+        return DN_ERR_MISALIGNED;
+    const size_t es = esize(dtype);
+    if (overlaps(packed, need, W_gate, (size_t)K * N * es) || overlaps(packed, need, W_up, (size_t)K * N * es) ||
+        overlaps(packed, need, gamma, K * es))
+        return DN_ERR_INVALID_ARG;
+    if ((2 * N + 255) / 256 > kMaxGridX || (K + 63) / 64 > kMaxBatch) return DN_ERR_UNSUPPORTED;
+    const dn_status st = from_hip(dn::launch_swiglu_prepare(W_gate, W_up, gamma, K, N, dtype, packed, stream));
+    if (st == DN_OK) {
+        w_out->K = K;
+        w_out->N = N;
+        w_out->dtype = dtype;
+        w_out->layout_version = DN_SWIGLU_LAYOUT_VERSION;
+        w_out->packed = packed;
+    }
+    return st;
+}
+
+DN_API dn_status rms_swiglu_deferred(const void* x, const ln_linear_weights* w, int64_t M, float eps, void* h,
+                                     hipStream_t stream) {
+    if (!x || !w || !h || !w->packed || M < 1) return DN_ERR_INVALID_ARG;
+    if (w->layout_version != DN_SWIGLU_LAYOUT_VERSION || w->K < 1 || w->N < 1 || !valid_dtype(w->dtype))
+        return DN_ERR_INVALID_ARG;
+    if (!isfinite(eps) || eps < 0.f) return DN_ERR_INVALID_ARG;
+    const int64_t K = w->K, N = w->N;
+    const int dt = w->dtype;
+    size_t xb, ob;
+    if (!bytes_of(M, K, (int64_t)esize(dt), &xb) || !bytes_of(M, N, (int64_t)esize(dt), &ob))
+        return DN_ERR_INVALID_ARG;
+    if (K % 8 || N % 8) return DN_ERR_UNSUPPORTED;
+    if (!aligned(x, 16) || !aligned(h, 16) || !aligned(w->packed, 256)) return DN_ERR_MISALIGNED;
+    const size_t pb = swiglu_packed_bytes(K, N, dt);
+    if (overlaps(h, ob, x, xb) || overlaps(h, ob, w->packed, pb)) return DN_ERR_INVALID_ARG;
+    if (((M + 15) / 16) * ((2 * N + 31) / 16) > kMaxGridX) return DN_ERR_UNSUPPORTED;
+    return from_hip(dn::launch_swiglu_deferred(x, w->packed, M, K, N, dt, eps, 1, h, stream));
+}
+
 DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq, int64_t Lk, int64_t d,
                                      int causal, int dtype, void* out, hipStream_t stream) {
     if (!S || !V || !out || BH < 1 || Lq < 1 || Lk < 1 || d < 1 || !valid_dtype(dtype)) return DN_ERR_INVALID_ARG;
@@ -154,6 +205,17 @@ DN_API dn_status layernorm(const void* x, const void* gamma, const void* beta, i
 DN_API dn_status rmsnorm(const void* x, const void* gamma, int64_t M, int64_t K, float eps, int dtype, void* y,
                          hipStream_t stream) {
     return row_norm(x, gamma, nullptr, M, K, eps, 1, dtype, y, stream);
+}
+
+DN_API dn_status silu_mul(const void* g, const void* u, int64_t count, int dtype, void* h, hipStream_t stream) {
+    if (!g || !u || !h || count < 1 || !valid_dtype(dtype)) return DN_ERR_INVALID_ARG;
+    size_t b;
+    if (!bytes_of(count, 1, (int64_t)esize(dtype), &b)) return DN_ERR_INVALID_ARG;
+    if (count % 8) return DN_ERR_UNSUPPORTED;
+    if (!aligned(g, 16) || !aligned(u, 16) || !aligned(h, 16)) return DN_ERR_MISALIGNED;
+    if (overlaps(h, b, g, b) || overlaps(h, b, u, b)) return DN_ERR_INVALID_ARG;
+    if ((count / 4 + 255) / 256 > kMaxGridX) return DN_ERR_UNSUPPORTED;
+    return from_hip(dn::launch_silu_mul(g, u, count, dtype, h, stream));
 }
 
 DN_API dn_status softmax(const void* S, int64_t BH, int64_t Lq, int64_t Lk, int causal, int dtype, void* P,

@@ -203,4 +203,29 @@ hipError_t launch_softmax(const void* S, int64_t BH, int64_t Lq, int64_t Lk, int
     return run_sm<32>(S, rows, Lq, Lk, causal, P, s);
 }
 
+// h = SiLU(g) * u element-wise, SiLU(z) = z / (1 + e^-z); one 16-byte piece per lane.
+template <class T>
+__global__ __launch_bounds__(256) void silu_mul_kernel(const T* __restrict__ g, const T* __restrict__ u,
+                                                       int64_t count, T* __restrict__ h) {
+    constexpr int EPL = elem<T>::per16;
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * EPL;
+    if (i >= count) return;
+    float a[EPL], b[EPL], o[EPL];
+    unpack16<T>(ld16(g + i), a);
+    unpack16<T>(ld16(u + i), b);
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) o[e] = a[e] / (1.0f + __builtin_amdgcn_exp2f(-a[e] * kLog2eB)) * b[e];
+    *reinterpret_cast<u32x4*>(h + i) = pack16<T>(o);
+}
+
+hipError_t launch_silu_mul(const void* g, const void* u, int64_t count, int dtype, void* h, hipStream_t s) {
+    const int64_t epl = dtype == 0 ? 4 : 8;
+    const dim3 grid((unsigned)((count / epl + 255) / 256));
+    if (dtype == 0)
+        silu_mul_kernel<float><<<grid, 256, 0, s>>>((const float*)g, (const float*)u, count, (float*)h);
+    else
+        silu_mul_kernel<__bf16><<<grid, 256, 0, s>>>((const __bf16*)g, (const __bf16*)u, count, (__bf16*)h);
+    return hipGetLastError();
+}
+
 }  // namespace dn

@@ -18,6 +18,20 @@ struct PackedLayout {
 };
 PackedLayout packed_layout(int64_t K, int64_t N, int dtype);
 
+// Layout of SwiGLU weights: the gate and up W' interleaved in 16-column blocks
+// (block 2j = gate columns 16j.., block 2j+1 = up columns 16j..), c and b likewise.
+PackedLayout swiglu_layout(int64_t K, int64_t N, int dtype);
+
+hipError_t launch_swiglu_prepare(const void* Wg, const void* Wu, const void* gamma, int64_t K, int64_t N,
+                                 int dtype, void* packed, hipStream_t s);
+
+// out[M][N] = SiLU(gate) * up with gate, up the deferred-normalized products.
+hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
+                                  int dtype, float eps, int rms, void* out, hipStream_t s);
+
+// h[M][N] = SiLU(g) * u element-wise (unfused comparator).
+hipError_t launch_silu_mul(const void* g, const void* u, int64_t count, int dtype, void* h, hipStream_t s);
+
 hipError_t launch_ln_prepare(const void* W, const void* gamma, const void* beta, const void* bias,
                              int64_t K, int64_t N, int dtype, void* packed, hipStream_t s);
 

@@ -30,7 +30,10 @@
 
 namespace dn {
 
-enum class Epi { kLnDeferred, kGemm };
+// kLnDeferred: out = rstd (acc - mean c) + b.  kSwiGlu: the same for the gate
+// and up columns, which the packed weights interleave in 16-column blocks (gate
+// block j, then up block j), combined as h = SiLU(gate) * up.  kGemm: acc + bias.
+enum class Epi { kLnDeferred, kGemm, kSwiGlu };
 enum class BMode { kKN, kNK, kPacked };
 
 struct MainArgs {
@@ -45,9 +48,15 @@ struct MainArgs {
     const float* b_col;   // LN: b[N]
     float eps;            // LN
     int rms;              // LN: RMSNorm statistics (Eq. (6)): mean taken as 0
+    int64_t n_out;        // kSwiGlu: output features (row stride of C); N counts packed columns
     const void* bias;     // GEMM: bias[N] in the element type, or null
     int a_causal;         // GEMM: A lower-triangular, skip k > row
 };
+
+// SiLU(z) = z / (1 + e^-z) with e^-z = 2^(-z log2 e) on the hardware exponential;
+// below z ~ -88 that overflows to +inf and the quotient is -0, the limit.
+constexpr float kLog2eF = 1.4426950408889634f;
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + __builtin_amdgcn_exp2f(-z * kLog2eF)); }
 
 // ---------------------------------------------------------------------------- waits
 template <int N>
@@ -85,12 +94,14 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
     constexpr int FM = WTM / 16, FN = WTN / 16;
     constexpr int A_CH = (BM / 16) * KB, B_CH = (BN / 16) * KB;
     constexpr int STAGE = (A_CH + B_CH) * kChunkBytes;
-    constexpr bool LN = EPI == Epi::kLnDeferred;
+    constexpr bool LN = EPI != Epi::kGemm;
+    constexpr bool SW = EPI == Epi::kSwiGlu;
     constexpr bool B_KN = BMODE == BMode::kKN;
     static_assert(FM >= 1 && FN >= 1 && BM % (16 * WM) == 0 && BN % (16 * WN) == 0, "tile");
     static_assert(!B_KN || sizeof(T) == 2, "KN staging is bf16 only");
     static_assert(A_CH % NW == 0 && B_CH % NW == 0, "every wave issues the same number of chunk copies");
-    static_assert(EPI != Epi::kLnDeferred || WN <= KB, "moments split: one k-chunk column per wave column");
+    static_assert(!LN || WN <= KB, "moments split: one k-chunk column per wave column");
+    static_assert(!SW || FN % 2 == 0, "gate/up fragment pairs");
 
     __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
     __shared__ float red[LN ? 2 * WN * BM : 1];
@@ -317,6 +328,29 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
         __syncthreads();
     }
 
+    if constexpr (SW) {
+        // fragment 2j holds gate columns, 2j+1 the up columns of the same outputs
+        const int64_t nw = n0 + wn * WTN;  // packed column of the wave's first fragment (multiple of 32)
+#pragma unroll
+        for (int j = 0; j < FN / 2; ++j) {
+            const int64_t ng = min(nw + 2 * j * 16 + (lane & 15), N - 1), nu = min(ng + 16, N - 1);
+            const int64_t o = nw / 2 + j * 16 + (lane & 15);
+            const float cg = p.c_col[ng], bg = p.b_col[ng], cu = p.c_col[nu], bu = p.b_col[nu];
+#pragma unroll
+            for (int fm = 0; fm < FM; ++fm) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int rl = wm * WTM + fm * 16 + 4 * (lane >> 4) + i;
+                    const int64_t r = m0 + rl;
+                    const float mu = row_mean[rl], rs = row_rstd[rl];
+                    const float g = __builtin_fmaf(rs, __builtin_fmaf(-mu, cg, acc[fm][2 * j][i]), bg);
+                    const float u = __builtin_fmaf(rs, __builtin_fmaf(-mu, cu, acc[fm][2 * j + 1][i]), bu);
+                    if (r < M && o < p.n_out) C[r * p.n_out + o] = from_f32<T>(silu(g) * u);
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
         const int64_t n = n0 + wn * WTN + fn * 16 + (lane & 15);
@@ -381,7 +415,9 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
     constexpr int A_INS = BM / 8 / NW;            // A copies per wave per stage (4)
     constexpr int B_INS = BN / 16 * 2 / NW;       // B copies per wave per stage (4)
     constexpr int PER = A_INS + B_INS;
-    constexpr bool LN = EPI == Epi::kLnDeferred;
+    constexpr bool LN = EPI != Epi::kGemm;
+    constexpr bool SW = EPI == Epi::kSwiGlu;
+    static_assert(!SW || FN % 2 == 0, "gate/up fragment pairs");
     constexpr int FMW = FM / WN;                  // row blocks whose moments each wave column owns
     constexpr int NMF = FM * FN, NRD = FM + FN;
 
@@ -582,6 +618,23 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
             else
                 return v + bn[fn];
         };
+        if constexpr (SW) {
+            // fragment 2j holds gate columns, 2j+1 the up columns of the same outputs
+            const int64_t o0 = (n0 + wn * WTN) / 2 + (lane & 15);
+#pragma unroll
+            for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int64_t r = m0 + lr + fm * 16 + i;
+#pragma unroll
+                    for (int j = 0; j < FN / 2; ++j) {
+                        const int64_t o = o0 + j * 16;
+                        const float h = silu(value(fm, 2 * j, i)) * value(fm, 2 * j + 1, i);
+                        if (r < M && o < p.n_out) C[r * p.n_out + o] = (__bf16)h;
+                    }
+                }
+            continue;
+        }
         if (m0 + BM <= M && n0 + BN <= N) {
             // whole tile in range: no per-element checks; the row offsets are
             // uniform (scalar) and the lane's offset from the tile base is fixed
@@ -623,13 +676,16 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
 // itself the Gram matrix x x^T whose diagonal is sum_k x[m][k]^2 -- once per
 // chunk for all NC column blocks.
 // =============================================================================
-template <int KS, int NC, int U>
+// SW: the packed columns interleave gate and up blocks (NC even, blocks 2j and
+// 2j+1 of the group form output block j), out[M][n_out] = SiLU(gate) * up.
+template <int KS, int NC, int U, bool SW = false>
 __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16* __restrict__ x,
                                                              const char* __restrict__ Wp, int64_t kchunks,
                                                              int64_t nblocks, const float* __restrict__ c_col,
                                                              const float* __restrict__ b_col, int M, int64_t K,
-                                                             int64_t N, float eps, int rms,
+                                                             int64_t N, float eps, int rms, int64_t n_out,
                                                              __bf16* __restrict__ out) {
+    static_assert(!SW || NC % 2 == 0, "gate/up block pairs");
     __shared__ f32x4 part[2 + NC][KS][kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t nb0 = (int64_t)blockIdx.x * NC;
@@ -693,33 +749,39 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
     part[0][wave][lane] = sx;
     part[1][wave][lane] = sxx;
     __syncthreads();
-    // column block j of the workgroup: reduce over the KS slices of K, then the epilogue
-    for (int j = wave; j < NC && nb0 + j < nblocks; j += KS) {
-        f32x4 tot[3];
+    // Column block j of the workgroup (SW: block pair j, gate then up): reduce over
+    // the KS slices of K, then the epilogue.
+    constexpr int NOUT = SW ? NC / 2 : NC;
+    for (int j = wave; j < NOUT && nb0 + (SW ? 2 * j : j) < nblocks; j += KS) {
+        const int q0 = SW ? 2 * j : j;
+        f32x4 tot[4];  // block q0, the moments, block q0 + 1 (SW)
 #pragma unroll
         for (int w = 0; w < KS; ++w) {
-            const f32x4 a0 = part[2 + j][w][lane], a1 = part[0][w][lane], a2 = part[1][w][lane];
+            const f32x4 a0 = part[2 + q0][w][lane], a1 = part[0][w][lane], a2 = part[1][w][lane];
             tot[0] = w ? tot[0] + a0 : a0;
             tot[1] = w ? tot[1] + a1 : a1;
             tot[2] = w ? tot[2] + a2 : a2;
+            if constexpr (SW) tot[3] = w ? tot[3] + part[3 + q0][w][lane] : part[3 + q0][w][lane];
         }
         // Gram diagonal (r, r) sits in lane r + 16*(r>>2), element r&3.  This lane's
         // rows are r = 4*(l>>4) + i, so the source lane is 20*(l>>4) + i.
         float diag[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) diag[i] = __shfl(tot[2][i], 20 * (lane >> 4) + i);
-        const int64_t col = (nb0 + j) * 16 + (lane & 15);
-        const int64_t n = min(col, N - 1);
+        const int64_t col = (nb0 + q0) * 16 + (lane & 15);
+        const int64_t n = min(col, N - 1), nu = min(col + 16, N - 1);
         const float cn = c_col[n], bn = b_col[n];
+        const float cu = SW ? c_col[nu] : 0.f, bu = SW ? b_col[nu] : 0.f;
+        const int64_t o = SW ? (nb0 / 2 + j) * 16 + (lane & 15) : col;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = 4 * (lane >> 4) + i;
             const float mean = rms ? 0.f : tot[1][i] / (float)K;
             const float var = __builtin_fmaxf(diag[i] / (float)K - mean * mean, 0.f);
             const float rstd = 1.0f / __builtin_sqrtf(var + eps);
-            float v = __builtin_fmaf(-mean, cn, tot[0][i]);
-            v = __builtin_fmaf(rstd, v, bn);
-            if (r < M && col < N) out[(int64_t)r * N + col] = (__bf16)v;
+            float v = __builtin_fmaf(rstd, __builtin_fmaf(-mean, cn, tot[0][i]), bn);
+            if constexpr (SW) v = silu(v) * __builtin_fmaf(rstd, __builtin_fmaf(-mean, cu, tot[3][i]), bu);
+            if (r < M && o < n_out) out[(int64_t)r * n_out + o] = (__bf16)v;
         }
     }
 }
@@ -728,31 +790,37 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
 // Static-weight preparation (off the per-token path).
 // =============================================================================
 // c[n] = sum_k round(gamma_k W[k][n]),  b[n] = sum_k beta_k W[k][n] + bias[n]; fp64 sums.
+// Column n of W lands at packed column ((n / 16) * mul + add) * 16 + n % 16 (mul = 2
+// interleaves two weight matrices block by block); columns N .. n_pad - 1 get zeros.
 template <class T>
 __global__ __launch_bounds__(256) void prep_colsum_kernel(const T* __restrict__ W, const T* __restrict__ gamma,
                                                           const T* __restrict__ beta, const T* __restrict__ bias,
-                                                          int64_t K, int64_t N, float* __restrict__ c_col,
-                                                          float* __restrict__ b_col) {
+                                                          int64_t K, int64_t N, int64_t n_pad, int mul, int add,
+                                                          float* __restrict__ c_col, float* __restrict__ b_col) {
     const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (n >= N) return;
+    if (n >= n_pad) return;
     double cs = 0.0, bs = 0.0;
-    for (int64_t k = 0; k < K; ++k) {
-        const float w = to_f32<T>(W[k * N + n]);
-        const float wp = to_f32<T>(from_f32<T>(to_f32<T>(gamma[k]) * w));
-        cs += (double)wp;
-        if (beta) bs += (double)to_f32<T>(beta[k]) * (double)w;
+    if (n < N) {
+        for (int64_t k = 0; k < K; ++k) {
+            const float w = to_f32<T>(W[k * N + n]);
+            const float wp = to_f32<T>(from_f32<T>(to_f32<T>(gamma[k]) * w));
+            cs += (double)wp;
+            if (beta) bs += (double)to_f32<T>(beta[k]) * (double)w;
+        }
+        if (bias) bs += (double)to_f32<T>(bias[n]);
     }
-    if (bias) bs += (double)to_f32<T>(bias[n]);
-    c_col[n] = (float)cs;
-    b_col[n] = (float)bs;
+    const int64_t pc = ((n / 16) * mul + add) * 16 + n % 16;
+    c_col[pc] = (float)cs;
+    b_col[pc] = (float)bs;
 }
 
 // One thread per 16-byte lane piece of the packed layout: chunk (nb, kc), lane l
-// holds W'[k][n] for n = 16 nb + (l & 15), k = kc*kchunk + (l >> 4)*EPL + e.
+// holds W'[k][n] for n = 16 nb + (l & 15), k = kc*kchunk + (l >> 4)*EPL + e; the
+// chunk is stored as block nb * mul + add.
 template <class T>
 __global__ __launch_bounds__(256) void prep_pack_kernel(const T* __restrict__ W, const T* __restrict__ gamma,
                                                         int64_t K, int64_t N, int64_t kchunks, int64_t pieces,
-                                                        char* __restrict__ packed) {
+                                                        int mul, int add, char* __restrict__ packed) {
     constexpr int EPL = elem<T>::per16, KC = elem<T>::kchunk;
     const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (id >= pieces) return;
@@ -773,7 +841,8 @@ __global__ __launch_bounds__(256) void prep_pack_kernel(const T* __restrict__ W,
     } else {
         out = u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])};
     }
-    *reinterpret_cast<u32x4*>(packed + id * 16) = out;
+    const int64_t dst = ((nb * mul + add) * kchunks + kc) * kWave + l;
+    *reinterpret_cast<u32x4*>(packed + dst * 16) = out;
 }
 
 // =============================================================================
@@ -795,24 +864,45 @@ PackedLayout packed_layout(int64_t K, int64_t N, int dtype) {
     return L;
 }
 
+// SwiGLU weights: gate and up interleaved block by block, so 2 * ceil(N / 16) blocks.
+PackedLayout swiglu_layout(int64_t K, int64_t N, int dtype) { return packed_layout(K, 2 * ((N + 15) / 16) * 16, dtype); }
+
+// Fold gamma into W and pack it as blocks nb * mul + add of a layout with L.kchunks.
 template <class T>
-static hipError_t prepare_t(const void* W, const void* gamma, const void* beta, const void* bias, int64_t K,
-                            int64_t N, void* packed, hipStream_t s) {
-    const PackedLayout L = packed_layout(K, N, sizeof(T) == 4 ? 0 : 1);
-    char* base = reinterpret_cast<char*>(packed);
-    dim3 g1((unsigned)((N + 255) / 256));
-    prep_colsum_kernel<T><<<g1, 256, 0, s>>>((const T*)W, (const T*)gamma, (const T*)beta, (const T*)bias, K, N,
-                                             (float*)(base + L.c_off), (float*)(base + L.b_off));
-    const int64_t pieces = L.nblocks * L.kchunks * kWave;
-    prep_pack_kernel<T><<<dim3((unsigned)((pieces + 255) / 256)), 256, 0, s>>>((const T*)W, (const T*)gamma, K, N,
-                                                                                L.kchunks, pieces, base + L.wt_off);
-    return hipGetLastError();
+static void pack_one(const void* W, const void* gamma, const void* beta, const void* bias, int64_t K, int64_t N,
+                     const PackedLayout& L, int mul, int add, char* base, hipStream_t s) {
+    const int64_t n_pad = (N + 15) / 16 * 16;
+    prep_colsum_kernel<T><<<dim3((unsigned)((n_pad + 255) / 256)), 256, 0, s>>>(
+        (const T*)W, (const T*)gamma, (const T*)beta, (const T*)bias, K, N, n_pad, mul, add,
+        (float*)(base + L.c_off), (float*)(base + L.b_off));
+    const int64_t pieces = (N + 15) / 16 * L.kchunks * kWave;
+    prep_pack_kernel<T><<<dim3((unsigned)((pieces + 255) / 256)), 256, 0, s>>>(
+        (const T*)W, (const T*)gamma, K, N, L.kchunks, pieces, mul, add, base + L.wt_off);
 }
 
 hipError_t launch_ln_prepare(const void* W, const void* gamma, const void* beta, const void* bias, int64_t K,
                              int64_t N, int dtype, void* packed, hipStream_t s) {
-    if (dtype == 0) return prepare_t<float>(W, gamma, beta, bias, K, N, packed, s);
-    return prepare_t<__bf16>(W, gamma, beta, bias, K, N, packed, s);
+    const PackedLayout L = packed_layout(K, N, dtype);
+    char* base = reinterpret_cast<char*>(packed);
+    if (dtype == 0)
+        pack_one<float>(W, gamma, beta, bias, K, N, L, 1, 0, base, s);
+    else
+        pack_one<__bf16>(W, gamma, beta, bias, K, N, L, 1, 0, base, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_swiglu_prepare(const void* Wg, const void* Wu, const void* gamma, int64_t K, int64_t N, int dtype,
+                                 void* packed, hipStream_t s) {
+    const PackedLayout L = swiglu_layout(K, N, dtype);
+    char* base = reinterpret_cast<char*>(packed);
+    for (int which = 0; which < 2; ++which) {
+        const void* W = which ? Wu : Wg;
+        if (dtype == 0)
+            pack_one<float>(W, gamma, nullptr, nullptr, K, N, L, 2, which, base, s);
+        else
+            pack_one<__bf16>(W, gamma, nullptr, nullptr, K, N, L, 2, which, base, s);
+    }
+    return hipGetLastError();
 }
 
 template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI>
@@ -833,7 +923,7 @@ static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
     // reductions).  384 tiles: group 2 (192 workgroups, 2 tile times) instead of
     // group 1 (384 workgroups, also 2 tile times, twice the moment work).
     int64_t group = 1;
-    if (EPI == Epi::kLnDeferred) {
+    if (EPI != Epi::kGemm) {
         int64_t best = -1;
         for (int64_t g = 1; g <= tn; ++g) {
             const int64_t span = (tm * ((tn + g - 1) / g) + 255) / 256 * g;
@@ -891,7 +981,7 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks,
                                                             a.nblocks, a.c_col, a.b_col, (int)M, K, N, eps, rms,
-                                                            (__bf16*)out);
+                                                            N, (__bf16*)out);
         };
         if (M <= 4)
             launch(ln_decode_bf16_kernel<4, 1, 8>, 4, 1);
@@ -904,6 +994,31 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
     if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
     if (use_big_tiles(M, N, K)) return run_pipe<Epi::kLnDeferred>(a, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
+}
+
+hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N, int dtype,
+                                  float eps, int rms, void* out, hipStream_t s) {
+    const int64_t np = 2 * ((N + 15) / 16) * 16;  // packed (gate + up) columns
+    MainArgs a = packed_args(x, packed, M, K, np, dtype, out);
+    a.eps = eps;
+    a.rms = rms;
+    a.n_out = N;
+    if (dtype == 1 && M <= 16) {
+        auto launch = [&](auto kern, int cols) {
+            const int64_t wgs = (a.nblocks + cols - 1) / cols;
+            kern<<<dim3((unsigned)wgs), 4 * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks, a.nblocks,
+                                                           a.c_col, a.b_col, (int)M, K, np, eps, rms, N,
+                                                           (__bf16*)out);
+        };
+        if (M <= 8)
+            launch(ln_decode_bf16_kernel<4, 2, 8, true>, 2);
+        else
+            launch(ln_decode_bf16_kernel<4, 4, 2, true>, 4);
+        return hipGetLastError();
+    }
+    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kSwiGlu>(a, 1, s);
+    if (use_big_tiles(M, np, K)) return run_pipe<Epi::kSwiGlu>(a, s);
+    return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kSwiGlu>(a, 1, s);
 }
 
 hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t batch, int64_t M, int64_t K,

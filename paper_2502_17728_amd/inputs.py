@@ -16,6 +16,8 @@ variance v):
 - LayerNorm -> Linear: x ~ N(0, 1); gamma ~ U(0.5, 1.5); beta ~ N(0, 0.02);
   W[K, N] ~ N(0, 1/K); bias = 0 where a workload states it, else absent.
   RMSNorm -> Linear (Eq. (6), Llama shapes): the same draws without beta.
+  RMSNorm -> SwiGLU: the same x and gamma, and two weights W_gate, W_up [K, N]
+  ~ N(0, 1/K) from their own streams.
   Optional outlier channels: a fixed set of channel indices (drawn once,
   without replacement) is scaled by a factor in every token, before rounding.
 - Softmax -> P.V: either S ~ N(0, s^2) directly (no mask), or S = Q K^T /
@@ -98,12 +100,24 @@ def rms_ffn_decode(t: int) -> LNWorkload:
     return LNWorkload(f"rms_ffn_up_bf16_decode_t{t}_8192x28672", 7, t, 8192, 28672, "bf16", norm="rms")
 
 
+# RMSNorm -> SwiGLU (gate and up projections of the Llama MLP): an 8B-class
+# prefill (hidden 4096, intermediate 14336) and a 70B-class decode token
+# (hidden 8192, intermediate 28672).  N is the intermediate size; FLOP count
+# both products.
+SWIGLU_PREFILL = LNWorkload("rms_swiglu_bf16_4096x4096x14336", 8, 4096, 4096, 14336, "bf16", outliers=8,
+                            norm="rms")
+
+
+def swiglu_decode(t: int) -> LNWorkload:
+    return LNWorkload(f"rms_swiglu_bf16_decode_t{t}_8192x28672", 9, t, 8192, 28672, "bf16", norm="rms")
+
+
 WORKLOADS = {w.name: w for w in (LN_F32_SMALL, SM_BF16_SMALL, LN_QKV, SM_CAUSAL, LN_FFN_PREFILL,
                                  ln_ffn_decode(1), ln_ffn_decode(4), ln_ffn_decode(16),
-                                 RMS_QKV, rms_ffn_decode(1))}
+                                 RMS_QKV, rms_ffn_decode(1), SWIGLU_PREFILL, swiglu_decode(1))}
 
 # tensor ids inside a workload's seed
-_X, _GAMMA, _BETA, _W, _OUTLIER_CH, _S, _Q, _KEY, _V = range(9)
+_X, _GAMMA, _BETA, _W, _OUTLIER_CH, _S, _Q, _KEY, _V, _W_UP = range(10)
 
 
 def _rng(seed: int, wid: int, tid: int, extra: int = 0) -> np.random.Generator:
@@ -143,6 +157,21 @@ def make_ln(w: LNWorkload, seed: int = 0, M: Optional[int] = None, x_extra: int 
     if w.zero_bias:
         out["bias"] = torch.zeros(w.N, dtype=DTYPES[w.dtype])
     return out
+
+
+def make_swiglu(w: LNWorkload, seed: int = 0, M: Optional[int] = None) -> dict:
+    """Inputs of an RMSNorm -> SwiGLU workload: x, gamma, W_gate (the LN recipe's W) and W_up."""
+    out = make_ln(w, seed, M)
+    Wu = _normal(_rng(seed, w.wid, _W_UP), (w.K, w.N), 1.0 / math.sqrt(w.K))
+    out.update(Wg=out.pop("W"), Wu=to_storage(Wu, w.dtype), beta=None)
+    return out
+
+
+def make_swiglu_case(M: int, K: int, N: int, dtype: str, seed: int = 0, outliers: int = 0,
+                     eps: float = 1e-5) -> dict:
+    """An RMSNorm -> SwiGLU case of any size with the same recipe (for parity tests)."""
+    return make_swiglu(LNWorkload(f"swiglu_{M}x{K}x{N}_{dtype}", 101, M, K, N, dtype, eps=eps, outliers=outliers,
+                                  norm="rms"), seed)
 
 
 def make_ln_case(M: int, K: int, N: int, dtype: str, seed: int = 0, outliers: int = 0,

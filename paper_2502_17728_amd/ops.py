@@ -19,10 +19,11 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdn.so")
 
 DN_F32, DN_BF16 = 0, 1
 DN_LN_LAYOUT_VERSION = 2
+DN_SWIGLU_LAYOUT_VERSION = 0x102
 STATUS = {0: "DN_OK", 1: "DN_ERR_INVALID_ARG", 2: "DN_ERR_UNSUPPORTED", 3: "DN_ERR_MISALIGNED", 4: "DN_ERR_HIP"}
 SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linear_prepare",
-           "ln_linear_deferred", "rms_linear_deferred", "softmax_pv_deferred", "layernorm", "rmsnorm",
-           "softmax", "gemm")
+           "ln_linear_deferred", "rms_linear_deferred", "swiglu_packed_bytes", "swiglu_prepare",
+           "rms_swiglu_deferred", "softmax_pv_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm")
 
 
 class DNError(RuntimeError):
@@ -50,13 +51,18 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
                                       ctypes.POINTER(LnLinearWeights), vp]
     lib.ln_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
     lib.rms_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
+    lib.swiglu_packed_bytes.argtypes, lib.swiglu_packed_bytes.restype = [i64, i64, i32], ctypes.c_size_t
+    lib.swiglu_prepare.argtypes = [vp, vp, vp, i64, i64, i32, vp, ctypes.c_size_t, ctypes.POINTER(LnLinearWeights),
+                                   vp]
+    lib.rms_swiglu_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
+    lib.silu_mul.argtypes = [vp, vp, i64, i32, vp, vp]
     lib.softmax_pv_deferred.argtypes = [vp, vp, i64, i64, i64, i64, i32, i32, vp, vp]
     lib.layernorm.argtypes = [vp, vp, vp, i64, i64, f32, i32, vp, vp]
     lib.rmsnorm.argtypes = [vp, vp, i64, i64, f32, i32, vp, vp]
     lib.softmax.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp]
     lib.gemm.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, i32, i32, vp, vp]
-    for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "softmax_pv_deferred",
-              "layernorm", "rmsnorm", "softmax", "gemm"):
+    for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "swiglu_prepare",
+              "rms_swiglu_deferred", "softmax_pv_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm"):
         getattr(lib, f).restype = i32
     return lib
 
@@ -155,6 +161,38 @@ def rms_linear_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
     return out
 
 
+def swiglu_packed_bytes(K: int, N: int, dtype: int) -> int:
+    return int(_lib.swiglu_packed_bytes(K, N, dtype))
+
+
+def swiglu_prepare(W_gate: torch.Tensor, W_up: torch.Tensor, gamma: torch.Tensor, stream=None) -> PreparedLinear:
+    K, N = W_gate.shape
+    if tuple(W_up.shape) != (K, N):
+        raise ValueError("W_gate and W_up must have the same [K, N] shape")
+    dt = _dt(W_gate)
+    nbytes = swiglu_packed_bytes(K, N, dt)
+    if nbytes == 0:
+        raise DNError("swiglu_packed_bytes", 1)
+    packed = torch.empty(nbytes, dtype=torch.uint8, device=W_gate.device)
+    desc = LnLinearWeights()
+    _check("swiglu_prepare", _lib.swiglu_prepare(
+        _dev(W_gate, "W_gate"), _dev(W_up, "W_up"), _dev(gamma, "gamma"), K, N, dt, _dev(packed, "packed"),
+        nbytes, ctypes.byref(desc), _stream(stream)))
+    return PreparedLinear(packed, desc)
+
+
+def rms_swiglu_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
+                        out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    M = x.shape[0]
+    if out is None:
+        out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
+    if _dt(x) != w.desc.dtype:
+        raise TypeError("x dtype differs from the prepared weights")
+    _check("rms_swiglu_deferred", _lib.rms_swiglu_deferred(
+        _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(out, "out"), _stream(stream)))
+    return out
+
+
 def softmax_pv_deferred(S: torch.Tensor, V: torch.Tensor, causal: bool = False,
                         out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     BH, Lq, Lk = S.shape
@@ -183,6 +221,16 @@ def rmsnorm(x: torch.Tensor, gamma: torch.Tensor, eps: float = 1e-5, out: Option
         out = torch.empty_like(x)
     _check("rmsnorm", _lib.rmsnorm(_dev(x, "x"), _dev(gamma, "gamma"), M, K, eps, _dt(x), _dev(out, "out"),
                                    _stream(stream)))
+    return out
+
+
+def silu_mul(g: torch.Tensor, u: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    if g.shape != u.shape or g.dtype != u.dtype:
+        raise ValueError("g and u must match in shape and dtype")
+    if out is None:
+        out = torch.empty_like(g)
+    _check("silu_mul", _lib.silu_mul(_dev(g, "g"), _dev(u, "u"), g.numel(), _dt(g), _dev(out, "out"),
+                                     _stream(stream)))
     return out
 
 

@@ -73,6 +73,32 @@ def test_ln_linear_deferred_validation(entry):
     assert f(P, ctypes.byref(w), 4, 1e-5, P3 + 256, None) == INVALID         # out overlaps packed
 
 
+def test_swiglu_validation():
+    prep, f = ops._lib.swiglu_prepare, ops._lib.rms_swiglu_deferred
+    nb = ops.swiglu_packed_bytes(64, 64, 1)
+    assert nb > ops.ln_linear_packed_bytes(64, 64, 1)
+    assert ops.swiglu_packed_bytes(0, 64, 1) == 0
+    w = ops.LnLinearWeights()
+    assert prep(None, P, P2, 64, 64, 1, P3, nb, ctypes.byref(w), None) == INVALID
+    assert prep(P, P, P2, 64, 64, 1, P3, nb - 1, ctypes.byref(w), None) == INVALID
+    assert prep(P, P, P2, 64, 60, 1, P3, 1 << 20, ctypes.byref(w), None) == UNSUPPORTED
+    assert prep(P, P, P2, 64, 64, 1, P3 + 16, nb, ctypes.byref(w), None) == MISALIGNED
+    assert prep(P, P2, P2 + 4096, 64, 64, 1, P2, nb, ctypes.byref(w), None) == INVALID  # packed overlaps W_up
+    assert w.layout_version == 0
+    sw = _w()
+    sw.layout_version = ops.DN_SWIGLU_LAYOUT_VERSION
+    assert f(P, ctypes.byref(_w()), 4, 1e-5, P2, None) == INVALID          # LayerNorm weights
+    assert ops._lib.ln_linear_deferred(P, ctypes.byref(sw), 4, 1e-5, P2, None) == INVALID  # and back
+    assert f(P, ctypes.byref(sw), 4, -1.0, P2, None) == INVALID
+    assert f(P + 8, ctypes.byref(sw), 4, 1e-5, P2, None) == MISALIGNED
+    assert f(P, ctypes.byref(sw), 4, 1e-5, P + 64, None) == INVALID         # h overlaps x
+    sm = ops._lib.silu_mul
+    assert sm(None, P2, 64, 1, P3, None) == INVALID
+    assert sm(P, P2, 60, 1, P3, None) == UNSUPPORTED
+    assert sm(P, P2 + 8, 64, 1, P3, None) == MISALIGNED
+    assert sm(P, P2, 64, 1, P2, None) == INVALID
+
+
 def test_ln_linear_prepare_validation():
     f = ops._lib.ln_linear_prepare
     w = ops.LnLinearWeights()

@@ -200,6 +200,77 @@ def test_rms_linear_zero_rows_give_b(ops):
     assert torch.equal(out.cpu()[3:9], case["bias"].expand(6, -1))
 
 
+# ---------------------------------------------------------------------------- RMSNorm -> SwiGLU
+def _swiglu_check(ops, case, rows=None):
+    w = ops.swiglu_prepare(cuda(case["Wg"]), cuda(case["Wu"]), cuda(case["gamma"]))
+    h = ops.rms_swiglu_deferred(cuda(case["x"]), w, case["eps"])
+    torch.cuda.synchronize()
+    xs = case["x"] if rows is None else case["x"][torch.as_tensor(rows)]
+    ref = oracle.rms_swiglu(xs, case["gamma"], case["Wg"], case["Wu"], case["eps"])
+    got = h.cpu() if rows is None else h.cpu()[torch.as_tensor(rows)]
+    err = rowwise_rel_err(got, ref)
+    print(f"rms_swiglu_deferred {tuple(case['x'].shape)}x{tuple(case['Wg'].shape)} {case['x'].dtype}: err={err:.3e}")
+    assert err <= TOL[case["x"].dtype], err
+    return h
+
+
+@pytest.mark.parametrize("M,K,N", [(37, 104, 72), (1, 8, 8), (130, 256, 200)])
+def test_rms_swiglu_f32_ragged(ops, M, K, N):
+    _swiglu_check(ops, I.make_swiglu_case(M, K, N, "f32", seed=M))
+
+
+@pytest.mark.parametrize("M,K,N", [(17, 64, 136), (257, 1024, 264), (128, 768, 1032), (1, 8, 8)])
+def test_rms_swiglu_bf16_ragged(ops, M, K, N):
+    _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M + K, outliers=2))
+
+
+@pytest.mark.parametrize("M", [1, 8, 9, 16])
+@pytest.mark.parametrize("K,N", [(1024, 520), (8, 24)])
+def test_rms_swiglu_bf16_decode_shapes(ops, M, K, N):
+    # 5-8 tokens: gate/up pairs per workgroup; 9-16: two pairs; N = 520 / 24 leave a partial pair group
+    _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M * 3 + 1, outliers=4))
+
+
+@pytest.mark.parametrize("M,K,N", [(4000, 544, 2056), (4000, 520, 2056)])
+def test_rms_swiglu_bf16_large_tiles_sampled(ops, M, K, N):
+    # 2 x 2056 packed columns: 16 x 17 tiles of 256 x 256 (pipelined loop, ragged M and N); K = 520
+    # takes the 128 x 128 loop
+    _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M % 83, outliers=3),
+                  rows=I.sample_rows(M, 32, seed=6))
+
+
+def test_rms_swiglu_prefill_workload_sampled(ops):
+    w = I.SWIGLU_PREFILL
+    _swiglu_check(ops, I.make_swiglu(w), rows=I.sample_rows(w.M, 12, seed=7))
+
+
+def test_rms_swiglu_decode_workload(ops):
+    _swiglu_check(ops, I.make_swiglu(I.swiglu_decode(1)))
+
+
+def test_rms_swiglu_matches_unfused_chain(ops):
+    case = I.make_swiglu_case(150, 512, 264, "bf16", seed=16)
+    x, one = cuda(case["x"]), torch.ones(512, dtype=torch.bfloat16, device="cuda")
+    fused = _swiglu_check(ops, case)
+    y = ops.rmsnorm(x, cuda(case["gamma"]), case["eps"])
+    g = ops.gemm(y, ops.ln_linear_prepare(cuda(case["Wg"]), one))
+    u = ops.gemm(y, ops.ln_linear_prepare(cuda(case["Wu"]), one))
+    h = ops.silu_mul(g, u)
+    ref = oracle.rms_swiglu(case["x"], case["gamma"], case["Wg"], case["Wu"], case["eps"])
+    assert rowwise_rel_err(h.cpu(), ref) <= TOL[torch.bfloat16]
+    assert rowwise_rel_err(fused.cpu(), oracle.to_f64(h.cpu())) <= TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_silu_mul_unfused(ops, dtype):
+    g = torch.Generator().manual_seed(17)
+    a = (torch.randn(33, 40, generator=g) * 6).to(I.DTYPES[dtype])
+    b = torch.randn(33, 40, generator=g).to(I.DTYPES[dtype])
+    h = ops.silu_mul(cuda(a), cuda(b))
+    ref = torch.nn.functional.silu(a.double()) * b.double()
+    assert rowwise_rel_err(h.cpu(), ref.numpy()) <= TOL[a.dtype] / 4
+
+
 # ---------------------------------------------------------------------------- Softmax -> P.V
 def _sm_check(ops, case, rows=None):
     S, V = case["S"], case["V"]
