@@ -131,8 +131,13 @@ class LNSite:
         self.g, self.b = c["gamma"].cuda(), cuda(c["beta"])
         self.bias = cuda(c["bias"])
         self.y = torch.empty_like(self.x)
+        self.stats = torch.empty(2 * w.M, dtype=torch.float32, device="cuda")
         self.ops = ops
         torch.cuda.synchronize()
+
+    def serial(self):
+        # ablation: the row statistics in a pre-pass kernel, then the same deferred epilogue
+        self.ops.ln_linear_serial(self.x, self.prep, self.w.eps, stats=self.stats, out=self.out)
 
     def fused(self):
         f = self.ops.rms_linear_deferred if self.rms else self.ops.ln_linear_deferred
@@ -374,12 +379,15 @@ def main():
             # (inside the step the kernel follows the other site, whose traffic evicts the caches);
             # the two alternate over 5 rounds and each reports its median
             n = max(3, args.steps // 2)
-            fis, us, uds = [], [], []
+            fis, us, uds, sers = [], [], [], []
+            serial = isinstance(s, LNSite) and not s.rms and s.w.K <= 16384
             for _ in range(5):
                 fis.append(time_steps([s.fused], n, 2)[0][0])
                 us.append(time_steps([s.unfused], n, 2)[0][0])
                 if isinstance(s, SMSite) and s.w.causal:
                     uds.append(time_steps([s.unfused_dense], max(3, n // 2), 1)[0][0])
+                if serial:
+                    sers.append(time_steps([s.serial], n, 2)[0][0])
             fi, u = float(np.median(fis)), float(np.median(us))
             k["isolated_ms"] = round(fi, 4)
             k["unfused_ms"] = round(u, 4)
@@ -388,6 +396,10 @@ def main():
                 ud = float(np.median(uds))
                 k["unfused_dense_ms"] = round(ud, 4)
                 k["speedup_vs_unfused_dense"] = round(ud / fi, 3)
+            if sers:  # ablation: statistics from a pre-pass instead of concurrently
+                se = float(np.median(sers))
+                k["serial_stats_ms"] = round(se, 4)
+                k["speedup_vs_serial_stats"] = round(se / fi, 3)
         kernels[name] = k
 
     d = sites[dom]

@@ -118,6 +118,39 @@ DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, i
 DN_API dn_status rms_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M,
                               float eps, void* out, hipStream_t stream);
 
+/* ----------------------------------------------------------------------- */
+/* Ablations of the LayerNorm -> Linear fusion                              */
+/* ----------------------------------------------------------------------- */
+
+/*
+ * Eq. (5) taken literally: the centering (I - E/n) of Eq. (3) folded into
+ * the static weight, W'' = (I - E/n) Diag(gamma) W, i.e. gamma_k W[k][n]
+ * minus its column mean (fp64, unrounded), rounded once to dtype; c is set
+ * to 0 so ln_linear_deferred computes out = rstd * (x . W'') + b, the
+ * epilogue of Eq. (5) with no mean term.  Same arguments, layout and status
+ * codes as ln_linear_prepare; the result is used with ln_linear_deferred.
+ * Equal to the mean * c epilogue in exact arithmetic; in floating point the
+ * rounded W'' columns no longer sum to exactly 0, so rows with a large
+ * |mean| / std lose about |mean| / std * 2^-9 of relative accuracy (bf16).
+ */
+DN_API dn_status ln_linear_prepare_centered(const void* W, const void* gamma, const void* beta,
+                                     const void* bias, int64_t K, int64_t N, int dtype,
+                                     void* packed, size_t packed_bytes,
+                                     ln_linear_weights* w_out, hipStream_t stream);
+
+/*
+ * Serial (not concurrent) statistics: a pre-pass kernel computes each row's
+ * mean and 1/sqrt(var + eps) (two passes over the row, Eq. (1)-(2)) into
+ * stats[2 M] (fp32 pairs; caller-owned device memory, 16-byte aligned, not
+ * overlapping x, out or the weights), then the product runs with the same
+ * deferred epilogue, reading them instead of reducing the moments
+ * concurrently.  It isolates what concurrency buys over a stats pre-pass.
+ * K must also fit the row kernel (<= 16384 bf16 / 8192 fp32) else
+ * DN_ERR_UNSUPPORTED.  Otherwise as ln_linear_deferred.
+ */
+DN_API dn_status ln_linear_serial(const void* x, const ln_linear_weights* w, int64_t M, float eps,
+                           float* stats, void* out, hipStream_t stream);
+
 /* ======================================================================= */
 /* RMSNorm -> gated MLP input (SwiGLU), deferred                            */
 /* ======================================================================= */

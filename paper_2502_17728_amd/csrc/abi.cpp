@@ -58,9 +58,9 @@ DN_API size_t ln_linear_packed_bytes(int64_t K, int64_t N, int dtype) {
     return dn::packed_layout(K, N, dtype).total;
 }
 
-DN_API dn_status ln_linear_prepare(const void* W, const void* gamma, const void* beta, const void* bias,
-                                   int64_t K, int64_t N, int dtype, void* packed, size_t packed_bytes,
-                                   ln_linear_weights* w_out, hipStream_t stream) {
+static dn_status prepare_ln(const void* W, const void* gamma, const void* beta, const void* bias, int64_t K,
+                            int64_t N, int dtype, int center, void* packed, size_t packed_bytes,
+                            ln_linear_weights* w_out, hipStream_t stream) {
     if (!W || !gamma || !packed || !w_out || K < 1 || N < 1 || !valid_dtype(dtype)) return DN_ERR_INVALID_ARG;
     const size_t need = ln_linear_packed_bytes(K, N, dtype);
     if (need == 0 || packed_bytes < need) return DN_ERR_INVALID_ARG;
@@ -72,7 +72,7 @@ DN_API dn_status ln_linear_prepare(const void* W, const void* gamma, const void*
         overlaps(packed, need, beta, K * es) || overlaps(packed, need, bias, N * es))
         return DN_ERR_INVALID_ARG;
     if ((N + 63) / 64 > kMaxGridX || (K + 63) / 64 > kMaxBatch) return DN_ERR_UNSUPPORTED;
-    const dn_status st = from_hip(dn::launch_ln_prepare(W, gamma, beta, bias, K, N, dtype, packed, stream));
+    const dn_status st = from_hip(dn::launch_ln_prepare(W, gamma, beta, bias, K, N, dtype, center, packed, stream));
     if (st == DN_OK) {
         w_out->K = K;
         w_out->N = N;
@@ -83,8 +83,20 @@ DN_API dn_status ln_linear_prepare(const void* W, const void* gamma, const void*
     return st;
 }
 
+DN_API dn_status ln_linear_prepare(const void* W, const void* gamma, const void* beta, const void* bias,
+                                   int64_t K, int64_t N, int dtype, void* packed, size_t packed_bytes,
+                                   ln_linear_weights* w_out, hipStream_t stream) {
+    return prepare_ln(W, gamma, beta, bias, K, N, dtype, 0, packed, packed_bytes, w_out, stream);
+}
+
+DN_API dn_status ln_linear_prepare_centered(const void* W, const void* gamma, const void* beta, const void* bias,
+                                            int64_t K, int64_t N, int dtype, void* packed, size_t packed_bytes,
+                                            ln_linear_weights* w_out, hipStream_t stream) {
+    return prepare_ln(W, gamma, beta, bias, K, N, dtype, 1, packed, packed_bytes, w_out, stream);
+}
+
 static dn_status deferred_linear(const void* x, const ln_linear_weights* w, int64_t M, float eps, int rms,
-                                 void* out, hipStream_t stream) {
+                                 float* stats, void* out, hipStream_t stream) {
     if (!x || !w || !out || !w->packed || M < 1) return DN_ERR_INVALID_ARG;
     if (w->layout_version != DN_LN_LAYOUT_VERSION || w->K < 1 || w->N < 1 || !valid_dtype(w->dtype))
         return DN_ERR_INVALID_ARG;
@@ -99,17 +111,33 @@ static dn_status deferred_linear(const void* x, const ln_linear_weights* w, int6
     const size_t pb = ln_linear_packed_bytes(K, N, dt);
     if (overlaps(out, ob, x, xb) || overlaps(out, ob, w->packed, pb)) return DN_ERR_INVALID_ARG;
     if (((M + 15) / 16) * ((N + 15) / 16) > kMaxGridX) return DN_ERR_UNSUPPORTED;
-    return from_hip(dn::launch_ln_linear_deferred(x, w->packed, M, K, N, dt, eps, rms, out, stream));
+    if (stats) {
+        if (!aligned(stats, 16)) return DN_ERR_MISALIGNED;
+        const size_t sb = (size_t)M * 8;
+        if (overlaps(stats, sb, x, xb) || overlaps(stats, sb, out, ob) || overlaps(stats, sb, w->packed, pb))
+            return DN_ERR_INVALID_ARG;
+        if (K > (dt == DN_F32 ? dn::kMaxRowElemsF32 : dn::kMaxRowElemsBf16) || (M + 3) / 4 > kMaxGridX)
+            return DN_ERR_UNSUPPORTED;
+        const dn_status st = from_hip(dn::launch_row_stats(x, M, K, eps, dt, stats, stream));
+        if (st != DN_OK) return st;
+    }
+    return from_hip(dn::launch_ln_linear_deferred(x, w->packed, M, K, N, dt, eps, rms, stats, out, stream));
 }
 
 DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M, float eps, void* out,
                                     hipStream_t stream) {
-    return deferred_linear(x, w, M, eps, 0, out, stream);
+    return deferred_linear(x, w, M, eps, 0, nullptr, out, stream);
+}
+
+DN_API dn_status ln_linear_serial(const void* x, const ln_linear_weights* w, int64_t M, float eps, float* stats,
+                                  void* out, hipStream_t stream) {
+    if (!stats) return DN_ERR_INVALID_ARG;
+    return deferred_linear(x, w, M, eps, 0, stats, out, stream);
 }
 
 DN_API dn_status rms_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M, float eps, void* out,
                                      hipStream_t stream) {
-    return deferred_linear(x, w, M, eps, 1, out, stream);
+    return deferred_linear(x, w, M, eps, 1, nullptr, out, stream);
 }
 
 DN_API size_t swiglu_packed_bytes(int64_t K, int64_t N, int dtype) {

@@ -106,6 +106,69 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const T* __restrict__ x,
     }
 }
 
+// Row statistics only (the serial ablation's pre-pass): stats[2 row] = mean,
+// stats[2 row + 1] = 1/sqrt(var + eps), two passes over the row kept in registers.
+template <class T, int NCH>
+__global__ __launch_bounds__(256) void row_stats_kernel(const T* __restrict__ x, int64_t M, int64_t K, float eps,
+                                                        float* __restrict__ stats) {
+    constexpr int EPL = elem<T>::per16;
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= M) return;
+    const T* xr = x + row * K;
+    float v[NCH][EPL];
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+        const int64_t k = (int64_t)(j * 64 + lane) * EPL;
+        if (k < K) {
+            unpack16<T>(ld16(xr + k), v[j]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) v[j][e] = 0.f;
+        }
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) s += v[j][e];
+    }
+    const float mean = wave_sum(s) / (float)K;
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+        const int64_t k = (int64_t)(j * 64 + lane) * EPL;
+        if (k < K) {
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) {
+                const float dlt = v[j][e] - mean;
+                ss = __builtin_fmaf(dlt, dlt, ss);
+            }
+        }
+    }
+    const float var = wave_sum(ss) / (float)K;
+    if (lane == 0) {
+        stats[2 * row] = mean;
+        stats[2 * row + 1] = 1.0f / __builtin_sqrtf(var + eps);
+    }
+}
+
+template <class T>
+static hipError_t dispatch_stats(const void* x, int64_t M, int64_t K, float eps, float* st, hipStream_t s) {
+    const int64_t nch = (K + 64 * elem<T>::per16 - 1) / (64 * elem<T>::per16);
+    const dim3 grid((unsigned)((M + 3) / 4));
+    const T* xt = (const T*)x;
+    if (nch <= 2) row_stats_kernel<T, 2><<<grid, 256, 0, s>>>(xt, M, K, eps, st);
+    else if (nch <= 4) row_stats_kernel<T, 4><<<grid, 256, 0, s>>>(xt, M, K, eps, st);
+    else if (nch <= 8) row_stats_kernel<T, 8><<<grid, 256, 0, s>>>(xt, M, K, eps, st);
+    else if (nch <= 16) row_stats_kernel<T, 16><<<grid, 256, 0, s>>>(xt, M, K, eps, st);
+    else row_stats_kernel<T, 32><<<grid, 256, 0, s>>>(xt, M, K, eps, st);
+    return hipGetLastError();
+}
+
+hipError_t launch_row_stats(const void* x, int64_t M, int64_t K, float eps, int dtype, float* stats,
+                            hipStream_t s) {
+    if (dtype == 0) return dispatch_stats<float>(x, M, K, eps, stats, s);
+    return dispatch_stats<__bf16>(x, M, K, eps, stats, s);
+}
+
 // P = softmax(S) row-wise (bf16).  causal: keys j <= i; mode 1 writes zeros for
 // j > i, mode 2 writes only the 8-element groups that reach the diagonal.
 template <int NCH>

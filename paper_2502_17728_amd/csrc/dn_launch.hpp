@@ -32,12 +32,19 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
 // h[M][N] = SiLU(g) * u element-wise (unfused comparator).
 hipError_t launch_silu_mul(const void* g, const void* u, int64_t count, int dtype, void* h, hipStream_t s);
 
+// center = 1: pack the literal Eq. (5) weight (I - E/n) Diag(gamma) W and set c = 0.
 hipError_t launch_ln_prepare(const void* W, const void* gamma, const void* beta, const void* bias,
-                             int64_t K, int64_t N, int dtype, void* packed, hipStream_t s);
+                             int64_t K, int64_t N, int dtype, int center, void* packed, hipStream_t s);
 
-// rms = 1: RMSNorm statistics (Eq. (6)), the mean taken as zero.
+// rms = 1: RMSNorm statistics (Eq. (6)), the mean taken as zero.  row_stats (nullable):
+// (mean, rstd) per row from a pre-pass, used instead of the concurrent moments.
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K,
-                                     int64_t N, int dtype, float eps, int rms, void* out, hipStream_t s);
+                                     int64_t N, int dtype, float eps, int rms, const float* row_stats,
+                                     void* out, hipStream_t s);
+
+// stats[2 r], stats[2 r + 1] = mean, 1/sqrt(var + eps) of row r of x (two-pass, Eq. (1)-(2)).
+hipError_t launch_row_stats(const void* x, int64_t M, int64_t K, float eps, int dtype, float* stats,
+                            hipStream_t s);
 
 hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t batch, int64_t M,
                        int64_t K, int64_t N, int b_layout, int a_causal, int dtype, void* C,

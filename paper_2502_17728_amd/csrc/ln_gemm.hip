@@ -49,6 +49,7 @@ struct MainArgs {
     float eps;            // LN
     int rms;              // LN: RMSNorm statistics (Eq. (6)): mean taken as 0
     int64_t n_out;        // kSwiGlu: output features (row stride of C); N counts packed columns
+    const float* row_stats;  // LN, serial ablation: (mean, rstd) per row from a pre-pass, or null
     const void* bias;     // GEMM: bias[N] in the element type, or null
     int a_causal;         // GEMM: A lower-triangular, skip k > row
 };
@@ -314,6 +315,12 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
         }
         __syncthreads();
         for (int r = tid; r < BM; r += NW * kWave) {
+            if (p.row_stats) {  // serial ablation: the pre-pass statistics replace the moments
+                const int64_t rr = min(m0 + r, M - 1);
+                row_mean[r] = p.row_stats[2 * rr];
+                row_rstd[r] = p.row_stats[2 * rr + 1];
+                continue;
+            }
             float a = 0.f, b = 0.f;
 #pragma unroll
             for (int w = 0; w < WN; ++w) {
@@ -555,7 +562,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
                 compute(own, fa1, fb1);
             }
         };
-        if (LN && tt == 0) {
+        const bool moments = LN && tt == 0 && !p.row_stats;
+        if (moments) {
             if (wn == 1)
                 run(std::integral_constant<int, 1>{});
             else
@@ -565,7 +573,15 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
         }
         wait_lgkm0();
 
-        if (LN && tt == 0) {
+        if (LN && tt == 0 && p.row_stats) {  // serial ablation: the pre-pass statistics
+            for (int r = tid; r < BM; r += NW * kWave) {
+                const int64_t rr = min(m0 + r, M - 1);
+                row_s1[r] = p.row_stats[2 * rr];
+                row_s2[r] = p.row_stats[2 * rr + 1];
+            }
+            __syncthreads();
+        }
+        if (moments) {
 #pragma unroll
             for (int i = 0; i < FMW; ++i) {
                 const float a = sum_lane_groups(s1[i]);
@@ -684,6 +700,7 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
                                                              int64_t nblocks, const float* __restrict__ c_col,
                                                              const float* __restrict__ b_col, int M, int64_t K,
                                                              int64_t N, float eps, int rms, int64_t n_out,
+                                                             const float* __restrict__ row_stats,
                                                              __bf16* __restrict__ out) {
     static_assert(!SW || NC % 2 == 0, "gate/up block pairs");
     __shared__ f32x4 part[2 + NC][KS][kWave];
@@ -776,9 +793,13 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = 4 * (lane >> 4) + i;
-            const float mean = rms ? 0.f : tot[1][i] / (float)K;
+            float mean = rms ? 0.f : tot[1][i] / (float)K;
             const float var = __builtin_fmaxf(diag[i] / (float)K - mean * mean, 0.f);
-            const float rstd = 1.0f / __builtin_sqrtf(var + eps);
+            float rstd = 1.0f / __builtin_sqrtf(var + eps);
+            if (row_stats) {  // serial ablation (the moment products above are then unused)
+                mean = row_stats[2 * min(r, M - 1)];
+                rstd = row_stats[2 * min(r, M - 1) + 1];
+            }
             float v = __builtin_fmaf(rstd, __builtin_fmaf(-mean, cn, tot[0][i]), bn);
             if constexpr (SW) v = silu(v) * __builtin_fmaf(rstd, __builtin_fmaf(-mean, cu, tot[3][i]), bu);
             if (r < M && o < n_out) out[(int64_t)r * n_out + o] = (__bf16)v;
@@ -790,24 +811,29 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
 // Static-weight preparation (off the per-token path).
 // =============================================================================
 // c[n] = sum_k round(gamma_k W[k][n]),  b[n] = sum_k beta_k W[k][n] + bias[n]; fp64 sums.
-// Column n of W lands at packed column ((n / 16) * mul + add) * 16 + n % 16 (mul = 2
-// interleaves two weight matrices block by block); columns N .. n_pad - 1 get zeros.
+// center = 1: c[n] = (1/K) sum_k gamma_k W[k][n] unrounded instead -- the column mean
+// that the literal Eq. (5) weight (I - E/n) Gamma W subtracts (pack reads it, then it
+// is cleared).  Column n of W lands at packed column ((n / 16) * mul + add) * 16 +
+// n % 16 (mul = 2 interleaves two weight matrices block by block); columns N ..
+// n_pad - 1 get zeros.
 template <class T>
 __global__ __launch_bounds__(256) void prep_colsum_kernel(const T* __restrict__ W, const T* __restrict__ gamma,
                                                           const T* __restrict__ beta, const T* __restrict__ bias,
                                                           int64_t K, int64_t N, int64_t n_pad, int mul, int add,
-                                                          float* __restrict__ c_col, float* __restrict__ b_col) {
+                                                          int center, float* __restrict__ c_col,
+                                                          float* __restrict__ b_col) {
     const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (n >= n_pad) return;
     double cs = 0.0, bs = 0.0;
     if (n < N) {
         for (int64_t k = 0; k < K; ++k) {
             const float w = to_f32<T>(W[k * N + n]);
-            const float wp = to_f32<T>(from_f32<T>(to_f32<T>(gamma[k]) * w));
-            cs += (double)wp;
+            const float gw = to_f32<T>(gamma[k]) * w;  // exact: a product of two bf16 values fits fp32
+            cs += center ? (double)gw : (double)to_f32<T>(from_f32<T>(gw));
             if (beta) bs += (double)to_f32<T>(beta[k]) * (double)w;
         }
         if (bias) bs += (double)to_f32<T>(bias[n]);
+        if (center) cs /= (double)K;
     }
     const int64_t pc = ((n / 16) * mul + add) * 16 + n % 16;
     c_col[pc] = (float)cs;
@@ -816,11 +842,13 @@ __global__ __launch_bounds__(256) void prep_colsum_kernel(const T* __restrict__ 
 
 // One thread per 16-byte lane piece of the packed layout: chunk (nb, kc), lane l
 // holds W'[k][n] for n = 16 nb + (l & 15), k = kc*kchunk + (l >> 4)*EPL + e; the
-// chunk is stored as block nb * mul + add.
+// chunk is stored as block nb * mul + add.  center (nullable): the column means to
+// subtract before rounding (W'' = (I - E/n) Gamma W of Eq. (5)).
 template <class T>
 __global__ __launch_bounds__(256) void prep_pack_kernel(const T* __restrict__ W, const T* __restrict__ gamma,
                                                         int64_t K, int64_t N, int64_t kchunks, int64_t pieces,
-                                                        int mul, int add, char* __restrict__ packed) {
+                                                        int mul, int add, const float* __restrict__ center,
+                                                        char* __restrict__ packed) {
     constexpr int EPL = elem<T>::per16, KC = elem<T>::kchunk;
     const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (id >= pieces) return;
@@ -833,7 +861,7 @@ __global__ __launch_bounds__(256) void prep_pack_kernel(const T* __restrict__ W,
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
         const int64_t k = k0 + e;
-        v[e] = (n < N && k < K) ? to_f32<T>(gamma[k]) * to_f32<T>(W[k * N + n]) : 0.f;
+        v[e] = (n < N && k < K) ? to_f32<T>(gamma[k]) * to_f32<T>(W[k * N + n]) - (center ? center[n] : 0.f) : 0.f;
     }
     u32x4 out;
     if constexpr (sizeof(T) == 2) {
@@ -868,26 +896,34 @@ PackedLayout packed_layout(int64_t K, int64_t N, int dtype) {
 PackedLayout swiglu_layout(int64_t K, int64_t N, int dtype) { return packed_layout(K, 2 * ((N + 15) / 16) * 16, dtype); }
 
 // Fold gamma into W and pack it as blocks nb * mul + add of a layout with L.kchunks.
+__global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0.f;
+}
+
 template <class T>
 static void pack_one(const void* W, const void* gamma, const void* beta, const void* bias, int64_t K, int64_t N,
-                     const PackedLayout& L, int mul, int add, char* base, hipStream_t s) {
+                     const PackedLayout& L, int mul, int add, int center, char* base, hipStream_t s) {
     const int64_t n_pad = (N + 15) / 16 * 16;
+    float* c_col = (float*)(base + L.c_off);
     prep_colsum_kernel<T><<<dim3((unsigned)((n_pad + 255) / 256)), 256, 0, s>>>(
-        (const T*)W, (const T*)gamma, (const T*)beta, (const T*)bias, K, N, n_pad, mul, add,
-        (float*)(base + L.c_off), (float*)(base + L.b_off));
+        (const T*)W, (const T*)gamma, (const T*)beta, (const T*)bias, K, N, n_pad, mul, add, center, c_col,
+        (float*)(base + L.b_off));
     const int64_t pieces = (N + 15) / 16 * L.kchunks * kWave;
     prep_pack_kernel<T><<<dim3((unsigned)((pieces + 255) / 256)), 256, 0, s>>>(
-        (const T*)W, (const T*)gamma, K, N, L.kchunks, pieces, mul, add, base + L.wt_off);
+        (const T*)W, (const T*)gamma, K, N, L.kchunks, pieces, mul, add, center ? c_col : nullptr, base + L.wt_off);
+    // the centred weight's columns sum to ~0: the epilogue's mean * c term is dropped, as Eq. (5) has none
+    if (center) fill_zero_kernel<<<dim3((unsigned)((n_pad + 255) / 256)), 256, 0, s>>>(c_col, n_pad);
 }
 
 hipError_t launch_ln_prepare(const void* W, const void* gamma, const void* beta, const void* bias, int64_t K,
-                             int64_t N, int dtype, void* packed, hipStream_t s) {
+                             int64_t N, int dtype, int center, void* packed, hipStream_t s) {
     const PackedLayout L = packed_layout(K, N, dtype);
     char* base = reinterpret_cast<char*>(packed);
     if (dtype == 0)
-        pack_one<float>(W, gamma, beta, bias, K, N, L, 1, 0, base, s);
+        pack_one<float>(W, gamma, beta, bias, K, N, L, 1, 0, center, base, s);
     else
-        pack_one<__bf16>(W, gamma, beta, bias, K, N, L, 1, 0, base, s);
+        pack_one<__bf16>(W, gamma, beta, bias, K, N, L, 1, 0, center, base, s);
     return hipGetLastError();
 }
 
@@ -898,9 +934,9 @@ hipError_t launch_swiglu_prepare(const void* Wg, const void* Wu, const void* gam
     for (int which = 0; which < 2; ++which) {
         const void* W = which ? Wu : Wg;
         if (dtype == 0)
-            pack_one<float>(W, gamma, nullptr, nullptr, K, N, L, 2, which, base, s);
+            pack_one<float>(W, gamma, nullptr, nullptr, K, N, L, 2, which, 0, base, s);
         else
-            pack_one<__bf16>(W, gamma, nullptr, nullptr, K, N, L, 2, which, base, s);
+            pack_one<__bf16>(W, gamma, nullptr, nullptr, K, N, L, 2, which, 0, base, s);
     }
     return hipGetLastError();
 }
@@ -968,10 +1004,12 @@ static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_
 }
 
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
-                                     int dtype, float eps, int rms, void* out, hipStream_t s) {
+                                     int dtype, float eps, int rms, const float* row_stats, void* out,
+                                     hipStream_t s) {
     MainArgs a = packed_args(x, packed, M, K, N, dtype, out);
     a.eps = eps;
     a.rms = rms;
+    a.row_stats = row_stats;
     if (dtype == 1 && M <= 16) {
         // Layouts measured on the 8192 x 28672 up-projection: up to 4 tokens the x
         // fragments are nearly free and 4 K-slices per column block stream best;
@@ -981,7 +1019,7 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks,
                                                             a.nblocks, a.c_col, a.b_col, (int)M, K, N, eps, rms,
-                                                            N, (__bf16*)out);
+                                                            N, a.row_stats, (__bf16*)out);
         };
         if (M <= 4)
             launch(ln_decode_bf16_kernel<4, 1, 8>, 4, 1);
@@ -1008,7 +1046,7 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), 4 * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks, a.nblocks,
                                                            a.c_col, a.b_col, (int)M, K, np, eps, rms, N,
-                                                           (__bf16*)out);
+                                                           nullptr, (__bf16*)out);
         };
         if (M <= 8)
             launch(ln_decode_bf16_kernel<4, 2, 8, true>, 2);

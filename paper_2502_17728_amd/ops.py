@@ -22,7 +22,8 @@ DN_LN_LAYOUT_VERSION = 2
 DN_SWIGLU_LAYOUT_VERSION = 0x102
 STATUS = {0: "DN_OK", 1: "DN_ERR_INVALID_ARG", 2: "DN_ERR_UNSUPPORTED", 3: "DN_ERR_MISALIGNED", 4: "DN_ERR_HIP"}
 SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linear_prepare",
-           "ln_linear_deferred", "rms_linear_deferred", "swiglu_packed_bytes", "swiglu_prepare",
+           "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered", "ln_linear_serial",
+           "swiglu_packed_bytes", "swiglu_prepare",
            "rms_swiglu_deferred", "softmax_pv_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm")
 
 
@@ -50,6 +51,8 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.ln_linear_prepare.argtypes = [vp, vp, vp, vp, i64, i64, i32, vp, ctypes.c_size_t,
                                       ctypes.POINTER(LnLinearWeights), vp]
     lib.ln_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
+    lib.ln_linear_prepare_centered.argtypes = lib.ln_linear_prepare.argtypes
+    lib.ln_linear_serial.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp, vp]
     lib.rms_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
     lib.swiglu_packed_bytes.argtypes, lib.swiglu_packed_bytes.restype = [i64, i64, i32], ctypes.c_size_t
     lib.swiglu_prepare.argtypes = [vp, vp, vp, i64, i64, i32, vp, ctypes.c_size_t, ctypes.POINTER(LnLinearWeights),
@@ -61,7 +64,8 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.rmsnorm.argtypes = [vp, vp, i64, i64, f32, i32, vp, vp]
     lib.softmax.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp]
     lib.gemm.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, i32, i32, vp, vp]
-    for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "swiglu_prepare",
+    for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered",
+              "ln_linear_serial", "swiglu_prepare",
               "rms_swiglu_deferred", "softmax_pv_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm"):
         getattr(lib, f).restype = i32
     return lib
@@ -123,7 +127,8 @@ def ln_linear_packed_bytes(K: int, N: int, dtype: int) -> int:
 
 
 def ln_linear_prepare(W: torch.Tensor, gamma: torch.Tensor, beta: Optional[torch.Tensor] = None,
-                      bias: Optional[torch.Tensor] = None, stream=None) -> PreparedLinear:
+                      bias: Optional[torch.Tensor] = None, stream=None, centered: bool = False) -> PreparedLinear:
+    """centered=True calls ln_linear_prepare_centered (the literal Eq. (5) weight)."""
     K, N = W.shape
     dt = _dt(W)
     nbytes = ln_linear_packed_bytes(K, N, dt)
@@ -131,7 +136,8 @@ def ln_linear_prepare(W: torch.Tensor, gamma: torch.Tensor, beta: Optional[torch
         raise DNError("ln_linear_packed_bytes", 1)
     packed = torch.empty(nbytes, dtype=torch.uint8, device=W.device)
     desc = LnLinearWeights()
-    _check("ln_linear_prepare", _lib.ln_linear_prepare(
+    fn = "ln_linear_prepare_centered" if centered else "ln_linear_prepare"
+    _check(fn, getattr(_lib, fn)(
         _dev(W, "W"), _dev(gamma, "gamma"), _dev(beta, "beta"), _dev(bias, "bias"), K, N, dt,
         _dev(packed, "packed"), nbytes, ctypes.byref(desc), _stream(stream)))
     return PreparedLinear(packed, desc)
@@ -146,6 +152,20 @@ def ln_linear_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
         raise TypeError("x dtype differs from the prepared weights")
     _check("ln_linear_deferred", _lib.ln_linear_deferred(
         _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def ln_linear_serial(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5, stats: Optional[torch.Tensor] = None,
+                     out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    M = x.shape[0]
+    if out is None:
+        out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
+    if stats is None:
+        stats = torch.empty(2 * M, dtype=torch.float32, device=x.device)
+    if _dt(x) != w.desc.dtype:
+        raise TypeError("x dtype differs from the prepared weights")
+    _check("ln_linear_serial", _lib.ln_linear_serial(
+        _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(stats, "stats"), _dev(out, "out"), _stream(stream)))
     return out
 
 

@@ -99,8 +99,19 @@ def test_swiglu_validation():
     assert sm(P, P2, 64, 1, P2, None) == INVALID
 
 
-def test_ln_linear_prepare_validation():
-    f = ops._lib.ln_linear_prepare
+def test_ln_linear_serial_validation():
+    f = ops._lib.ln_linear_serial
+    w = _w()
+    assert f(P, ctypes.byref(w), 4, 1e-5, None, P2, None) == INVALID                 # stats required
+    assert f(P, ctypes.byref(w), 4, 1e-5, P3 + (1 << 30) + 4, P2, None) == MISALIGNED
+    assert f(P, ctypes.byref(w), 4, 1e-5, P + 16, P2, None) == INVALID               # stats overlap x
+    assert f(P, ctypes.byref(_w(K=1 << 15)), 4, 1e-5, P3 + (1 << 30), P2, None) == UNSUPPORTED  # K > row kernel
+    assert f(P, ctypes.byref(_w(version=0)), 4, 1e-5, P3 + (1 << 30), P2, None) == INVALID
+
+
+@pytest.mark.parametrize("entry", ["ln_linear_prepare", "ln_linear_prepare_centered"])
+def test_ln_linear_prepare_validation(entry):
+    f = getattr(ops._lib, entry)
     w = ops.LnLinearWeights()
     nb = ops.ln_linear_packed_bytes(64, 64, 1)
     assert f(None, P2, None, None, 64, 64, 1, P3, nb, ctypes.byref(w), None) == INVALID

@@ -150,6 +150,53 @@ def test_ln_linear_guard_band(ops):
     assert (buf[:512] == 7.0).all() and (buf[-512:] == 7.0).all()
 
 
+# ---------------------------------------------------------------------------- ablations
+@pytest.mark.parametrize("M,K,N,dtype", [(37, 104, 72, "f32"), (257, 1024, 264, "bf16"), (5, 1024, 520, "bf16"),
+                                         (4000, 544, 4104, "bf16")])
+def test_ln_linear_centered_weight(ops, M, K, N, dtype):
+    # Eq. (5) literally: (I - E/n) Gamma W folded into the static weight, no mean term in the epilogue
+    case = I.make_ln_case(M, K, N, dtype, seed=M + 3, outliers=2)
+    w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]), centered=True)
+    out = ops.ln_linear_deferred(cuda(case["x"]), w, case["eps"])
+    rows = None if M < 1000 else I.sample_rows(M, 24, seed=8)
+    xs = case["x"] if rows is None else case["x"][torch.as_tensor(rows)]
+    ref = oracle.ln_linear(xs, case["gamma"], case["beta"], case["W"], None, case["eps"])
+    got = out.cpu() if rows is None else out.cpu()[torch.as_tensor(rows)]
+    assert rowwise_rel_err(got, ref) <= TOL[case["x"].dtype]
+
+
+def test_centered_weight_loses_accuracy_on_offset_rows(ops):
+    # rows with mean 4 and unit spread: the rounded W'' columns no longer sum to 0, an error of
+    # about |mean|/std * 2^-9 that the mean * c epilogue (c summed from the rounded W') cancels
+    case = I.make_ln_case(64, 1024, 256, "bf16", seed=9, mean_offset=4.0)
+    x, W, g, b = cuda(case["x"]), cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"])
+    ref = oracle.ln_linear(case["x"], case["gamma"], case["beta"], case["W"], None, case["eps"])
+    e_epi = rowwise_rel_err(ops.ln_linear_deferred(x, ops.ln_linear_prepare(W, g, b)).cpu(), ref)
+    e_lit = rowwise_rel_err(ops.ln_linear_deferred(x, ops.ln_linear_prepare(W, g, b, centered=True)).cpu(), ref)
+    print(f"mean-offset rows: epilogue form {e_epi:.3e}, literal Eq. (5) weight {e_lit:.3e}")
+    assert e_epi <= TOL[torch.bfloat16] and e_lit <= TOL[torch.bfloat16]
+    assert e_epi < e_lit
+
+
+@pytest.mark.parametrize("M,K,N,dtype", [(37, 104, 72, "f32"), (257, 1024, 264, "bf16"), (3, 1024, 520, "bf16"),
+                                         (12, 8200, 64, "bf16"), (4000, 544, 4104, "bf16")])
+def test_ln_linear_serial_stats(ops, M, K, N, dtype):
+    # statistics from a pre-pass kernel, then the same product and deferred epilogue
+    case = I.make_ln_case(M, K, N, dtype, seed=M + 4, outliers=2)
+    w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
+    stats = torch.empty(2 * M, dtype=torch.float32, device="cuda")
+    out = ops.ln_linear_serial(cuda(case["x"]), w, case["eps"], stats=stats)
+    rows = None if M < 1000 else I.sample_rows(M, 24, seed=9)
+    xs = case["x"] if rows is None else case["x"][torch.as_tensor(rows)]
+    ref = oracle.ln_linear(xs, case["gamma"], case["beta"], case["W"], None, case["eps"])
+    got = out.cpu() if rows is None else out.cpu()[torch.as_tensor(rows)]
+    assert rowwise_rel_err(got, ref) <= TOL[case["x"].dtype]
+    st = stats.cpu().double().numpy().reshape(M, 2)
+    xd = oracle.to_f64(case["x"])
+    np.testing.assert_allclose(st[:, 0], xd.mean(1), rtol=1e-4, atol=1e-5)
+    np.testing.assert_allclose(st[:, 1], 1 / np.sqrt(xd.var(1) + case["eps"]), rtol=1e-4)
+
+
 # ---------------------------------------------------------------------------- RMSNorm -> Linear
 @pytest.mark.parametrize("M,K,N", [(37, 104, 72), (1, 8, 8), (300, 512, 200)])
 def test_rms_linear_f32_ragged(ops, M, K, N):
