@@ -442,7 +442,9 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
     // the epilogues of all the group's tiles.  Workgroup order: XCD-contiguous,
     // then blocks of GM row blocks x all column groups (operand panels shared
     // under one L2).
+#ifndef DN_GROUP_FORCE
     if constexpr (!LN) group = 1;  // the plain product has no per-row work to share
+#endif
     const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
     const int ngroups = (tiles_n + group - 1) / group;
     const int t = xcd_contiguous(blockIdx.x, gridDim.x);
@@ -605,11 +607,14 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
         // Per-lane epilogue operands, loaded once per tile: the column terms c_n,
         // b_n (or the bias) of the lane's 8 columns and the row terms mean_m,
         // rstd_m of its 16 rows.
-        const int lc = wn * WTN + (lane & 15), lr = wm * WTM + 4 * (lane >> 4);  // lane's first column / row
+        // (Opaque copies: the lane's row and column terms are formed here, after the
+        // main loop, rather than hoisted out of the tile loop and held across it.)
+        int lc = wn * WTN + (lane & 15), lr = wm * WTM + 4 * (lane >> 4);  // lane's first column / row
+        asm volatile("" : "+v"(lc), "+v"(lr));
         float cn[FN], bn[FN];
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn) {
-            const int64_t nc = min(n0 + lc + fn * 16, N - 1);
+            const int64_t nc = min(n0 + (lc + fn * 16), N - 1);
             cn[fn] = 0.f;
             bn[fn] = 0.f;
             if constexpr (LN) {
@@ -634,50 +639,61 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
             else
                 return v + bn[fn];
         };
+        // Stores of a tile wholly in range go through a buffer resource on the
+        // tile's first element: the row offset of each (fm, i) is a scalar
+        // (soffset), the lane's offset in the tile a fixed 32-bit VGPR and the
+        // fragment column an immediate, so no 64-bit row addresses stay live.
+        // (The host keeps 256 rows of the output below 2^31 bytes.)
+        auto store_tile = [&](__bf16* base, int64_t ldc, int vo, auto col_value, auto ncol) {
+            const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
+            constexpr int NCOL = decltype(ncol)::value;
+#pragma unroll
+            for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int so = __builtin_amdgcn_readfirstlane((fm * 16 + i) * (int)ldc * 2);
+#pragma unroll
+                    for (int f = 0; f < NCOL; ++f)
+                        __builtin_amdgcn_raw_buffer_store_b16(
+                            __builtin_bit_cast(unsigned short, (__bf16)col_value(fm, f, i)), rc, vo + f * 32, so, 0);
+                }
+        };
+        // A ragged tile checks each store against the rows and columns left.
+        auto store_edge = [&](__bf16* base, int64_t ldc, int64_t rows_left, int64_t cols_left, int col0,
+                              auto col_value, auto ncol) {
+            const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
+            constexpr int NCOL = decltype(ncol)::value;
+#pragma unroll
+            for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int rl = lr + fm * 16 + i;
+#pragma unroll
+                    for (int f = 0; f < NCOL; ++f) {
+                        const int col = col0 + f * 16;
+                        if (rl < rows_left && col < cols_left)
+                            __builtin_amdgcn_raw_buffer_store_b16(
+                                __builtin_bit_cast(unsigned short, (__bf16)col_value(fm, f, i)), rc,
+                                (rl * (int)ldc + col) * 2, 0, 0);
+                    }
+                }
+        };
         if constexpr (SW) {
             // fragment 2j holds gate columns, 2j+1 the up columns of the same outputs
-            const int64_t o0 = (n0 + wn * WTN) / 2 + (lane & 15);
-#pragma unroll
-            for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int64_t r = m0 + lr + fm * 16 + i;
-#pragma unroll
-                    for (int j = 0; j < FN / 2; ++j) {
-                        const int64_t o = o0 + j * 16;
-                        const float h = silu(value(fm, 2 * j, i)) * value(fm, 2 * j + 1, i);
-                        if (r < M && o < p.n_out) C[r * p.n_out + o] = (__bf16)h;
-                    }
-                }
+            const int64_t ob = (n0 + wn * WTN) / 2;  // the wave's first output column
+            auto h = [&](int fm, int j, int i) { return silu(value(fm, 2 * j, i)) * value(fm, 2 * j + 1, i); };
+            if (m0 + BM <= M && ob + WTN / 2 <= p.n_out)
+                store_tile(C + m0 * p.n_out + ob, p.n_out, (int)(lr * p.n_out + (lane & 15)) * 2, h,
+                           std::integral_constant<int, FN / 2>{});
+            else
+                store_edge(C + m0 * p.n_out + ob, p.n_out, M - m0, p.n_out - ob, lane & 15, h,
+                           std::integral_constant<int, FN / 2>{});
             continue;
         }
-        if (m0 + BM <= M && n0 + BN <= N) {
-            // whole tile in range: no per-element checks; the row offsets are
-            // uniform (scalar) and the lane's offset from the tile base is fixed
-            // (32 bits: 256 rows of N elements)
-            __bf16* Ct = C + m0 * N + n0;
-            const uint32_t lo = (uint32_t)(lr * N + lc);
-#pragma unroll
-            for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    __bf16* Cr = Ct + (int64_t)(fm * 16 + i) * N;
-#pragma unroll
-                    for (int fn = 0; fn < FN; ++fn) Cr[lo + fn * 16] = (__bf16)value(fm, fn, i);
-                }
-        } else {
-#pragma unroll
-            for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int64_t r = m0 + lr + fm * 16 + i;
-#pragma unroll
-                    for (int fn = 0; fn < FN; ++fn) {
-                        const int64_t n = n0 + lc + fn * 16;
-                        if (r < M && n < N) C[r * N + n] = (__bf16)value(fm, fn, i);
-                    }
-                }
-        }
+        if (m0 + BM <= M && n0 + BN <= N)
+            store_tile(C + m0 * N + n0, N, (int)(lr * N + lc) * 2, value, std::integral_constant<int, FN>{});
+        else
+            store_edge(C + m0 * N + n0, N, M - m0, N - n0, lc, value, std::integral_constant<int, FN>{});
     }
 }
 
@@ -969,6 +985,9 @@ static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
             }
         }
     }
+#ifdef DN_GROUP_FORCE
+    group = DN_GROUP_FORCE;
+#endif
     const int64_t wgs = tm * ((tn + group - 1) / group);
 #ifndef DN_PIPE_WM
 #define DN_PIPE_WM 4
@@ -980,6 +999,7 @@ static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
 
 // The 256x256 kernel once its tiles fill the chip (and K is a multiple of its stage).
 static bool use_big_tiles(int64_t M, int64_t N, int64_t K) {
+    if (N >= (int64_t(1) << 22)) return false;  // 256 output rows < 2^31 bytes (32-bit store offsets)
     // K < 2^22 keeps the 32-bit copy offsets of a 256-row panel (256 K bf16) and of a
     // 16-chunk-column W' panel (16 x K/32 KiB) below 4 GiB.
     return K % 64 == 0 && K < (int64_t(1) << 22) && ((M + 255) / 256) * ((N + 255) / 256) >= 256;
