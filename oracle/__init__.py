@@ -51,9 +51,11 @@ def _load():
         lib.oracle_rms_linear.argtypes = [d, d, d, d, d, i64, i64, i64, ctypes.c_double, d, i32]
         lib.oracle_rms_swiglu.argtypes = [d, d, d, d, i64, i64, i64, ctypes.c_double, d, i32]
         lib.oracle_softmax.argtypes = [d, d, i64, i64, d, i32]
+        lib.oracle_attention.argtypes = [d, d, d, d, d, i64, i64, i64, ctypes.c_double, d, i32]
         lib.oracle_softmax_pv.argtypes = [d, d, d, d, i64, i64, i64, d, i32]
         for f in ("oracle_layernorm", "oracle_linear", "oracle_ln_linear", "oracle_rmsnorm",
-                  "oracle_rms_linear", "oracle_rms_swiglu", "oracle_softmax", "oracle_softmax_pv"):
+                  "oracle_rms_linear", "oracle_rms_swiglu", "oracle_softmax", "oracle_softmax_pv",
+                  "oracle_attention"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -206,4 +208,22 @@ def softmax_pv(S_rows, V, head=None, qpos=None, nthreads=None):
     out = np.empty((R, d), np.float64)
     _check(_load().oracle_softmax_pv(_ptr(S), _ptr(V), _ptr(h), _ptr(q), R, Lk, d, _ptr(out),
                                      _threads(nthreads)), "softmax_pv")
+    return out
+
+
+def attention(Q_rows, K, V, scale, head=None, qpos=None, nthreads=None):
+    """softmax(scale * Q_rows[R, d] . K[head[r]]^T) . V[head[r]], K/V[H, Lk, d]; returns [R, d] fp64."""
+    Q = to_f64(Q_rows)
+    R, d = Q.shape
+    K, V = to_f64(K), to_f64(V)
+    if K.ndim == 2:
+        K, V = K[None], V[None]
+    assert K.shape == V.shape and K.shape[2] == d, (Q.shape, K.shape, V.shape)
+    Lk = K.shape[1]
+    h, q = _rows_meta(R, head, qpos)
+    if h is not None:
+        assert h.min() >= 0 and h.max() < K.shape[0]
+    out = np.empty((R, d), np.float64)
+    _check(_load().oracle_attention(_ptr(Q), _ptr(K), _ptr(V), _ptr(h), _ptr(q), R, Lk, d, float(scale),
+                                    _ptr(out), _threads(nthreads)), "attention")
     return out

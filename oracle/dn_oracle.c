@@ -20,6 +20,8 @@
  *   - The Llama MLP input stage that the same subsubsection fuses: RMSNorm,
  *     the gate and up projections, and h = SiLU(y Wg) * (y Wu) with
  *     SiLU(z) = z / (1 + exp(-z)).
+ *   - Attention from Q, K: the scores s_ij = scale * q_i . k_j formed here,
+ *     then Eq. (7) on them (the same softmax and value product).
  *   - Softmax then values,  Eq. (7) with the footnote's max subtraction:
  *       m = max_j x_j, e_j = exp(x_j - m), y_j = e_j / sum_i e_i, out = y V.
  *
@@ -386,5 +388,55 @@ int oracle_softmax_pv(const double* S, const double* V, const int64_t* head,
     if (!S || !V || !out || R < 1 || Lk < 1 || d < 1) return -1;
     smpv_ctx c = {S, V, head, qpos, Lk, d, out};
     run_rows(smpv_rows, &c, R, nthreads);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Attention: the scores of row r against head h's keys, scale * q . k_j,    */
+/* then the softmax and value product of Eq. (7).                            */
+
+typedef struct {
+    const double *Q, *K, *V;
+    const int64_t *head, *qpos;
+    int64_t Lk, d;
+    double scale;
+    double* out;
+} attn_ctx;
+
+static void attn_rows(void* p, int64_t r0, int64_t r1) {
+    attn_ctx* c = (attn_ctx*)p;
+    double* s = (double*)malloc((size_t)c->Lk * sizeof(double));
+    double* prob = (double*)malloc((size_t)c->Lk * sizeof(double));
+    if (s && prob) {
+        for (int64_t r = r0; r < r1; ++r) {
+            const int64_t h = c->head ? c->head[r] : 0;
+            const int64_t q = c->qpos ? c->qpos[r] : -1;
+            const double* qr = c->Q + r * c->d;
+            const double* K = c->K + h * c->Lk * c->d;
+            const double* V = c->V + h * c->Lk * c->d;
+            const int64_t J = kept_keys(c->Lk, q);
+            for (int64_t j = 0; j < c->Lk; ++j) {
+                double dot = 0.0;
+                if (j < J)
+                    for (int64_t t = 0; t < c->d; ++t) dot += qr[t] * K[j * c->d + t];
+                s[j] = c->scale * dot;
+            }
+            softmax_row(s, c->Lk, q, prob);
+            double* o = c->out + r * c->d;
+            for (int64_t t = 0; t < c->d; ++t) o[t] = 0.0;
+            for (int64_t j = 0; j < J; ++j)
+                for (int64_t t = 0; t < c->d; ++t) o[t] += prob[j] * V[j * c->d + t];
+        }
+    }
+    free(prob);
+    free(s);
+}
+
+int oracle_attention(const double* Q, const double* K, const double* V, const int64_t* head,
+                     const int64_t* qpos, int64_t R, int64_t Lk, int64_t d, double scale,
+                     double* out, int nthreads) {
+    if (!Q || !K || !V || !out || R < 1 || Lk < 1 || d < 1) return -1;
+    attn_ctx c = {Q, K, V, head, qpos, Lk, d, scale, out};
+    run_rows(attn_rows, &c, R, nthreads);
     return 0;
 }

@@ -56,6 +56,13 @@ int oracle_softmax_pv(const double* S, const double* V, const int64_t* head,
                       const int64_t* qpos, int64_t R, int64_t Lk, int64_t d,
                       double* out, int nthreads);
 
+/* Attention: out[R][d] = softmax(scale * Q[r] . K[head[r]]^T) . V[head[r]] with
+   Q[R][d] (one query row per r), K, V[H][Lk][d]; head and qpos as for
+   oracle_softmax_pv (qpos[r] >= 0: keys j <= qpos[r] only). */
+int oracle_attention(const double* Q, const double* K, const double* V, const int64_t* head,
+                     const int64_t* qpos, int64_t R, int64_t Lk, int64_t d, double scale,
+                     double* out, int nthreads);
+
 #ifdef __cplusplus
 }
 #endif

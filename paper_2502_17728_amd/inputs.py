@@ -89,6 +89,10 @@ def ln_ffn_decode(t: int) -> LNWorkload:
     return LNWorkload(f"ln_ffn_up_bf16_decode_t{t}_8192x28672", 5, t, 8192, 28672, "bf16")
 
 
+# Attention from Q, K, V directly (the scores formed in the kernel): the causal
+# workload's own tensors, 32 heads x 8192 tokens, d = 128.
+ATTN_CAUSAL = SMWorkload("causal_attention_bf16_32x8192x8192_d128", 4, 32, 8192, 128, causal=True, from_qk=True)
+
 # RMSNorm -> Linear with Llama shapes: the fused QKV projection of an 8B-class
 # model with grouped-query attention (32 query + 2 x 8 key/value heads of 128
 # over hidden 4096), and the 70B-class FFN up-projection at decode.
@@ -114,7 +118,7 @@ def swiglu_decode(t: int) -> LNWorkload:
 
 WORKLOADS = {w.name: w for w in (LN_F32_SMALL, SM_BF16_SMALL, LN_QKV, SM_CAUSAL, LN_FFN_PREFILL,
                                  ln_ffn_decode(1), ln_ffn_decode(4), ln_ffn_decode(16),
-                                 RMS_QKV, rms_ffn_decode(1), SWIGLU_PREFILL, swiglu_decode(1))}
+                                 RMS_QKV, rms_ffn_decode(1), SWIGLU_PREFILL, swiglu_decode(1), ATTN_CAUSAL)}
 
 # tensor ids inside a workload's seed
 _X, _GAMMA, _BETA, _W, _OUTLIER_CH, _S, _Q, _KEY, _V, _W_UP = range(10)
@@ -215,6 +219,29 @@ def make_sm(w: SMWorkload, seed: int = 0, heads: Optional[Sequence[int]] = None,
         S[i] = s.to(torch.bfloat16)
         V[i] = to_storage(_normal(_rng(seed, w.wid, _V, h), (L, w.d), 1.0), "bf16")
     return dict(S=S, V=V, causal=w.causal)
+
+
+def make_qkv(w: SMWorkload, seed: int = 0, heads: Optional[Sequence[int]] = None,
+             L: Optional[int] = None) -> dict:
+    """Q, K, V[BH, L, d] (bf16 CPU tensors) of a workload whose scores come from Q K^T.
+
+    The same streams as make_sm's, so S = Q K^T / sqrt(d) (fp32, then bf16) of
+    make_sm is exactly the score matrix these tensors define.
+    """
+    assert w.from_qk, w
+    L = w.L if L is None else L
+    heads = list(range(w.BH)) if heads is None else list(heads)
+    Q, K, V = (torch.empty((len(heads), L, w.d), dtype=torch.bfloat16) for _ in range(3))
+    for i, h in enumerate(heads):
+        Q[i] = to_storage(_normal(_rng(seed, w.wid, _Q, h), (L, w.d), 1.0), "bf16")
+        K[i] = to_storage(_normal(_rng(seed, w.wid, _KEY, h), (L, w.d), 1.0), "bf16")
+        V[i] = to_storage(_normal(_rng(seed, w.wid, _V, h), (L, w.d), 1.0), "bf16")
+    return dict(Q=Q, K=K, V=V, causal=w.causal, scale=1.0 / math.sqrt(w.d))
+
+
+def make_qkv_case(BH: int, L: int, d: int, causal: bool, seed: int = 0) -> dict:
+    """Q, K, V of any size with the same recipe (for parity tests)."""
+    return make_qkv(SMWorkload(f"attn_{BH}x{L}_d{d}", 201, BH, L, d, causal, from_qk=True), seed)
 
 
 def make_sm_case(BH: int, L: int, d: int, causal: bool, seed: int = 0, s_std: float = 2.0,

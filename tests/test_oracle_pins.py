@@ -1,11 +1,13 @@
 """Pins of the fp64 oracle against what the paper and mathematics fix.
 
-The oracle (``oracle/``) is the plain definition of Eq. (1), (2), (4), (6) and (7).
+The oracle (``oracle/``) is the plain definition of Eq. (1), (2), (4), (6) and (7),
+and of attention formed from Q and K ahead of Eq. (7).
 Before it may judge the GPU path it is tied here to things other than itself:
 
 - hand-worked examples stored in ``tests/golden`` (exact values);
 - closed forms and special cases (K = 2, constant rows, one-hot scores, V = I);
-- library routines: ``torch.nn.functional.layer_norm``, ``rms_norm``, ``silu`` and ``torch.softmax``
+- library routines: ``torch.nn.functional.layer_norm``, ``rms_norm``, ``silu``,
+  ``scaled_dot_product_attention`` and ``torch.softmax``
   in fp64, which the oracle does not call;
 - the paper's fused forms, Eq. (5) and Eq. (8), evaluated independently here
   with numpy, which reach the same result by different arithmetic;
@@ -260,6 +262,37 @@ def test_eq6_deferred_rmsnorm_equals_oracle(M, K, N):
     fused = r[:, None] * (x @ (np.diag(gamma) @ W)) + beta @ W + bias
     np.testing.assert_allclose(oracle.rms_linear(x, gamma, W, bias, eps, beta=beta), fused, rtol=1e-11,
                                atol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_matches_torch_sdpa(causal):
+    rng = np.random.default_rng(24 + causal)
+    H, L, d = 3, 19, 8
+    Q, K, V = rng.normal(size=(H, L, d)), rng.normal(size=(H, L, d)), rng.normal(size=(H, L, d))
+    scale = 1 / math.sqrt(d)
+    want = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q), torch.from_numpy(K), torch.from_numpy(V), is_causal=causal, scale=scale).numpy()
+    head, qpos = np.repeat(np.arange(H), L), np.tile(np.arange(L), H)
+    got = oracle.attention(Q.reshape(-1, d), K, V, scale, head=head, qpos=qpos if causal else None)
+    np.testing.assert_allclose(got, want.reshape(-1, d), rtol=1e-12, atol=1e-13)
+    # and against the pinned softmax . V on scores formed independently
+    S = np.einsum("hqd,hkd->hqk", Q, K) * scale
+    ref = oracle.softmax_pv(S.reshape(-1, L), V, head=head, qpos=qpos if causal else None)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_attention_closed_forms():
+    # K = 0: every score is 0, so row i averages the kept values (causal: V[0..i])
+    rng = np.random.default_rng(25)
+    L, d = 7, 3
+    Q, V = rng.normal(size=(L, d)), rng.normal(size=(L, d))
+    got = oracle.attention(Q, np.zeros((L, d)), V, 0.5, qpos=np.arange(L))
+    want = np.cumsum(V, axis=0) / np.arange(1, L + 1)[:, None]
+    np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-14)
+    # one key aligned with the query and a huge scale: that key's value row
+    K = np.eye(L, d)
+    got = oracle.attention(np.eye(L, d)[2:3] * 50.0, K, V, 40.0)
+    np.testing.assert_allclose(got[0], V[2], rtol=1e-12)
 
 
 @pytest.mark.parametrize("causal", [False, True])
