@@ -46,6 +46,7 @@ PEAK_HBM_GBS = 8000.0       # HBM3E
 # the kernel source it was taken on: each entry carries the sha256 of its kernel's source files, and
 # the bench reports null once they differ.
 KERNEL_SOURCES = {"softmax_pv_deferred": ("softmax_pv.hip", "dn_device.hpp"),
+                  "attention_deferred": ("attention.hip", "dn_device.hpp"),
                   "ln_linear_deferred": ("ln_gemm.hip", "dn_device.hpp"),
                   "rms_linear_deferred": ("ln_gemm.hip", "dn_device.hpp"),
                   "rms_swiglu_deferred": ("ln_gemm.hip", "dn_device.hpp")}
@@ -89,7 +90,7 @@ def parse():
     ap.add_argument("--workload", default="layer",
                     choices=["layer", "small", "ln_qkv", "causal_softmax_pv", "ffn_prefill",
                              "ffn_decode_t1", "ffn_decode_t4", "ffn_decode_t16", "rms_qkv",
-                             "rms_ffn_decode_t1", "swiglu_prefill", "swiglu_decode_t1"])
+                             "rms_ffn_decode_t1", "swiglu_prefill", "swiglu_decode_t1", "causal_attention"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None)
@@ -267,6 +268,62 @@ class SMSite:
         return dt, kept / w.pairs(), f"{len(idx)} of {w.BH * w.L} Softmax->P.V rows"
 
 
+class AttnSite:
+    """Attention with the scores formed in the kernel (Q, K, V in; S never stored)."""
+    kernel = "attention_deferred"
+
+    def __init__(self, ops, I, w):
+        self.w = w
+        self.case = I.make_qkv(w)
+        c = self.case
+        self.Q, self.K, self.V = c["Q"].cuda(), c["K"].cuda(), c["V"].cuda()
+        self.out = torch.empty_like(self.Q)
+        # conventional comparators: S = (scale Q) K^T stored (the scale folded into Q once, untimed),
+        # then the deferred Softmax -> P.V on S, or softmax + P.V
+        self.Qs = (self.Q.float() * c["scale"]).to(torch.bfloat16)
+        self.S = torch.empty((w.BH, w.L, w.L), dtype=torch.bfloat16, device="cuda")
+        self.P = torch.empty_like(self.S)
+        self.ops = ops
+        torch.cuda.synchronize()
+
+    def fused(self):
+        self.ops.attention_deferred(self.Q, self.K, self.V, causal=self.w.causal, scale=self.case["scale"],
+                                    out=self.out)
+
+    def unfused(self):
+        # the materialized-score path: QK^T GEMM writes S, then deferred Softmax -> P.V reads it
+        self.ops.gemm(self.Qs, self.K, b_layout=1, out=self.S)
+        self.ops.softmax_pv_deferred(self.S, self.V, causal=self.w.causal, out=self.out)
+
+    def unfused_dense(self):
+        # the eager conventional chain: QK^T, softmax (dense P), P.V
+        self.ops.gemm(self.Qs, self.K, b_layout=1, out=self.S)
+        self.ops.softmax(self.S, causal=1 if self.w.causal else 0, out=self.P)
+        self.ops.gemm(self.P, self.V, out=self.out)
+
+    def flops(self):
+        return 2.0 * self.w.flops()
+
+    def bytes(self):
+        w = self.w
+        return 2.0 * 4 * w.BH * w.L * w.d
+
+    def peak_tflops(self):
+        return PEAK_BF16_TFLOPS
+
+    def oracle_sample(self, oracle, I, threads, rows):
+        w = self.w
+        idx = I.sample_rows(w.BH * w.L, rows, seed=10)
+        head, q = idx // w.L, idx % w.L
+        Qr = self.case["Q"].reshape(w.BH * w.L, w.d)[torch.as_tensor(idx)]
+        t0 = time.perf_counter()
+        oracle.attention(Qr, self.case["K"], self.case["V"], self.case["scale"], head=head,
+                         qpos=q if w.causal else None, nthreads=threads)
+        dt = time.perf_counter() - t0
+        kept = float(np.sum(q + 1)) if w.causal else float(len(idx) * w.L)
+        return dt, kept / w.pairs(), f"{len(idx)} of {w.BH * w.L} attention rows"
+
+
 def build_sites(ops, I, name):
     if name == "layer":
         return [LNSite(ops, I, I.LN_QKV), SMSite(ops, I, I.SM_CAUSAL)], \
@@ -282,6 +339,8 @@ def build_sites(ops, I, name):
         return [LNSite(ops, I, I.LN_FFN_PREFILL)], I.LN_FFN_PREFILL.name
     if name == "rms_qkv":
         return [LNSite(ops, I, I.RMS_QKV)], I.RMS_QKV.name
+    if name == "causal_attention":
+        return [AttnSite(ops, I, I.ATTN_CAUSAL)], I.ATTN_CAUSAL.name
     if name == "swiglu_prefill":
         return [SwiGLUSite(ops, I, I.SWIGLU_PREFILL)], I.SWIGLU_PREFILL.name
     if name == "swiglu_decode_t1":
@@ -365,7 +424,7 @@ def main():
     kernels = {}
     dom = max(range(len(sites)), key=lambda i: per[i])
     for i, s in enumerate(sites):
-        name = s.kernel if isinstance(s, (LNSite, SwiGLUSite)) else "softmax_pv_deferred"
+        name = s.kernel if isinstance(s, (LNSite, SwiGLUSite, AttnSite)) else "softmax_pv_deferred"
         tf = s.flops() / (per[i] * 1e-3) / 1e12
         gbs = s.bytes() / (per[i] * 1e-3) / 1e9
         k = {"workload": s.w.name, "ms": round(per[i], 4), "tflops": round(tf, 2),
@@ -384,7 +443,7 @@ def main():
             for _ in range(5):
                 fis.append(time_steps([s.fused], n, 2)[0][0])
                 us.append(time_steps([s.unfused], n, 2)[0][0])
-                if isinstance(s, SMSite) and s.w.causal:
+                if isinstance(s, (SMSite, AttnSite)) and s.w.causal:
                     uds.append(time_steps([s.unfused_dense], max(3, n // 2), 1)[0][0])
                 if serial:
                     sers.append(time_steps([s.serial], n, 2)[0][0])
@@ -427,7 +486,7 @@ def main():
             rows = 16 if isinstance(s, (LNSite, SwiGLUSite)) and s.w.K * s.w.N > 1e8 else 64
             if isinstance(s, (LNSite, SwiGLUSite)) and s.w.M <= 16:
                 rows = s.w.M
-            if isinstance(s, SMSite):
+            if isinstance(s, (SMSite, AttnSite)):
                 rows = 1024 if s.w.L >= 4096 else 2048
             dt, frac, desc = s.oracle_sample(oracle, I, threads, rows)
             extrap += dt / frac

@@ -207,6 +207,22 @@ DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, i
                               int64_t Lk, int64_t d, int causal, int dtype, void* out,
                               hipStream_t stream);
 
+/*
+ * The same deferred Softmax -> P.V with the scores formed in the kernel:
+ * out[BH][Lq][d] = softmax(scale * Q K^T) . V per head, Q[BH][Lq][d],
+ * K, V[BH][Lk][d] (Sec. II-B carried one operation earlier, so that S never
+ * exists in memory: Eq. (8)'s numerators exp(s - m) come straight from the
+ * Q.K^T product on the matrix core, the row max is kept online, the row sum
+ * reduced alongside, and out = acc / l once).  causal = 1 keeps key j for
+ * query i iff j <= i (Lq == Lk).  scale must be finite and > 0.  dtype must
+ * be DN_BF16; d 64 or 128; Lq * d * 2 and Lk * d * 2 < 2^31 per head (else
+ * DN_ERR_UNSUPPORTED).  A row whose scores are all -inf cannot occur (finite
+ * inputs); NaN inputs propagate.
+ */
+DN_API dn_status attention_deferred(const void* Q, const void* K, const void* V, int64_t BH,
+                             int64_t Lq, int64_t Lk, int64_t d, int causal, float scale,
+                             int dtype, void* out, hipStream_t stream);
+
 /* ======================================================================= */
 /* Unfused comparators: the conventional sub-graph of Fig. 1(a)             */
 /* ======================================================================= */

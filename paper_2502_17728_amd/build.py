@@ -22,7 +22,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdn.so")
-SOURCES = ["ln_gemm.hip", "softmax_pv.hip", "baselines.hip", "abi.cpp"]
+SOURCES = ["ln_gemm.hip", "softmax_pv.hip", "attention.hip", "baselines.hip", "abi.cpp"]
 ARCH = "gfx950"
 
 

@@ -210,6 +210,24 @@ DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, i
     return from_hip(dn::launch_softmax_pv_deferred(S, V, BH, Lq, Lk, d, causal, out, stream));
 }
 
+DN_API dn_status attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq, int64_t Lk,
+                                    int64_t d, int causal, float scale, int dtype, void* out, hipStream_t stream) {
+    if (!Q || !K || !V || !out || BH < 1 || Lq < 1 || Lk < 1 || d < 1 || !valid_dtype(dtype))
+        return DN_ERR_INVALID_ARG;
+    if (causal != 0 && causal != 1) return DN_ERR_INVALID_ARG;
+    if (causal && Lq != Lk) return DN_ERR_INVALID_ARG;
+    if (!isfinite(scale) || !(scale > 0.f)) return DN_ERR_INVALID_ARG;
+    size_t qb, kb, ob;
+    if (!bytes_of(BH, Lq, d * 2, &qb) || !bytes_of(BH, Lk, d * 2, &kb)) return DN_ERR_INVALID_ARG;
+    ob = qb;
+    if (dtype != DN_BF16 || (d != 64 && d != 128)) return DN_ERR_UNSUPPORTED;
+    if (Lq * d * 2 >= (int64_t(1) << 31) || Lk * d * 2 >= (int64_t(1) << 31)) return DN_ERR_UNSUPPORTED;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16)) return DN_ERR_MISALIGNED;
+    if (overlaps(out, ob, Q, qb) || overlaps(out, ob, K, kb) || overlaps(out, ob, V, kb)) return DN_ERR_INVALID_ARG;
+    if (BH * ((Lq + 255) / 256) > kMaxGridX) return DN_ERR_UNSUPPORTED;
+    return from_hip(dn::launch_attention_deferred(Q, K, V, BH, Lq, Lk, d, causal, scale, out, stream));
+}
+
 static dn_status row_norm(const void* x, const void* gamma, const void* beta, int64_t M, int64_t K, float eps,
                           int rms, int dtype, void* y, hipStream_t stream) {
     if (!x || !gamma || !y || M < 1 || K < 1 || !valid_dtype(dtype)) return DN_ERR_INVALID_ARG;

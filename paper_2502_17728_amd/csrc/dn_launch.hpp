@@ -53,6 +53,10 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
 hipError_t launch_softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq,
                                       int64_t Lk, int64_t d, int causal, void* out, hipStream_t s);
 
+// out[BH][Lq][d] = softmax(scale * Q K^T) V per head, the scores formed in the kernel.
+hipError_t launch_attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,
+                                     int64_t Lk, int64_t d, int causal, float scale, void* out, hipStream_t s);
+
 hipError_t launch_layernorm(const void* x, const void* gamma, const void* beta, int64_t M,
                             int64_t K, float eps, int rms, int dtype, void* y, hipStream_t s);
 

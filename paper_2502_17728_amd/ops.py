@@ -23,8 +23,8 @@ DN_SWIGLU_LAYOUT_VERSION = 0x102
 STATUS = {0: "DN_OK", 1: "DN_ERR_INVALID_ARG", 2: "DN_ERR_UNSUPPORTED", 3: "DN_ERR_MISALIGNED", 4: "DN_ERR_HIP"}
 SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linear_prepare",
            "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered", "ln_linear_serial",
-           "swiglu_packed_bytes", "swiglu_prepare",
-           "rms_swiglu_deferred", "softmax_pv_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm")
+           "swiglu_packed_bytes", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
+           "attention_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm")
 
 
 class DNError(RuntimeError):
@@ -60,13 +60,14 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.rms_swiglu_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
     lib.silu_mul.argtypes = [vp, vp, i64, i32, vp, vp]
     lib.softmax_pv_deferred.argtypes = [vp, vp, i64, i64, i64, i64, i32, i32, vp, vp]
+    lib.attention_deferred.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, f32, i32, vp, vp]
     lib.layernorm.argtypes = [vp, vp, vp, i64, i64, f32, i32, vp, vp]
     lib.rmsnorm.argtypes = [vp, vp, i64, i64, f32, i32, vp, vp]
     lib.softmax.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp]
     lib.gemm.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, i32, i32, vp, vp]
     for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered",
-              "ln_linear_serial", "swiglu_prepare",
-              "rms_swiglu_deferred", "softmax_pv_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm"):
+              "ln_linear_serial", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
+              "attention_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm"):
         getattr(lib, f).restype = i32
     return lib
 
@@ -221,6 +222,24 @@ def softmax_pv_deferred(S: torch.Tensor, V: torch.Tensor, causal: bool = False,
         out = torch.empty((BH, Lq, d), dtype=S.dtype, device=S.device)
     _check("softmax_pv_deferred", _lib.softmax_pv_deferred(
         _dev(S, "S"), _dev(V, "V"), BH, Lq, Lk, d, int(causal), _dt(S), _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def attention_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, causal: bool = False,
+                       scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                       stream=None) -> torch.Tensor:
+    """softmax(scale * Q K^T) V per head; Q[BH, Lq, d], K/V[BH, Lk, d]; scale defaults to 1/sqrt(d)."""
+    BH, Lq, d = Q.shape
+    Lk = K.shape[1]
+    if tuple(K.shape) != (BH, Lk, d) or tuple(V.shape) != (BH, Lk, d):
+        raise ValueError("K and V must be [BH, Lk, d] like Q")
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    if out is None:
+        out = torch.empty_like(Q)
+    _check("attention_deferred", _lib.attention_deferred(
+        _dev(Q, "Q"), _dev(K, "K"), _dev(V, "V"), BH, Lq, Lk, d, int(causal), float(scale), _dt(Q),
+        _dev(out, "out"), _stream(stream)))
     return out
 
 

@@ -138,6 +138,20 @@ def test_softmax_pv_deferred_validation():
     assert f(P, P2, 1, 64, 64, 64, 0, 1, P + 64, None) == INVALID        # out overlaps S
 
 
+def test_attention_deferred_validation():
+    f = ops._lib.attention_deferred
+    assert f(None, P2, P3, 1, 64, 64, 64, 0, 0.125, 1, P3 + (1 << 30), None) == INVALID
+    assert f(P, P2, P3, 1, 64, 64, 64, 2, 0.125, 1, P3 + (1 << 30), None) == INVALID      # causal 0/1
+    assert f(P, P2, P3, 1, 32, 64, 64, 1, 0.125, 1, P3 + (1 << 30), None) == INVALID      # causal: Lq == Lk
+    assert f(P, P2, P3, 1, 64, 64, 64, 0, 0.0, 1, P3 + (1 << 30), None) == INVALID        # scale > 0
+    assert f(P, P2, P3, 1, 64, 64, 64, 0, float("nan"), 1, P3 + (1 << 30), None) == INVALID
+    assert f(P, P2, P3, 1, 64, 64, 64, 0, 0.125, 0, P3 + (1 << 30), None) == UNSUPPORTED  # bf16 only
+    assert f(P, P2, P3, 1, 64, 64, 96, 0, 0.125, 1, P3 + (1 << 30), None) == UNSUPPORTED  # d 64 / 128
+    assert f(P, P2, P3, 1, 1 << 23, 64, 128, 0, 0.125, 1, P3 + (1 << 30), None) == UNSUPPORTED
+    assert f(P + 8, P2, P3, 1, 64, 64, 64, 0, 0.125, 1, P3 + (1 << 30), None) == MISALIGNED
+    assert f(P, P2, P3, 1, 64, 64, 64, 0, 0.125, 1, P + 64, None) == INVALID              # out overlaps Q
+
+
 def test_unfused_validation():
     ln, sm, gm = ops._lib.layernorm, ops._lib.softmax, ops._lib.gemm
     assert ln(None, P2, None, 4, 64, 1e-5, 1, P3, None) == INVALID

@@ -389,6 +389,57 @@ def test_softmax_pv_rejects_ragged_key_length(ops):
     assert e.value.status == 2  # DN_ERR_UNSUPPORTED: Lk must be a multiple of 8
 
 
+# ---------------------------------------------------------------------------- attention from Q, K
+def _attn_check(ops, case, rows=None, Lk=None):
+    Q, K, V = case["Q"], case["K"], case["V"]
+    BH, Lq, d = Q.shape
+    causal = case["causal"]
+    out = ops.attention_deferred(cuda(Q), cuda(K), cuda(V), causal=causal, scale=case["scale"])
+    torch.cuda.synchronize()
+    rows = np.arange(BH * Lq) if rows is None else np.asarray(rows)
+    head, q = rows // Lq, rows % Lq
+    ref = oracle.attention(Q.reshape(BH * Lq, d)[torch.as_tensor(rows)], K, V, case["scale"], head=head,
+                           qpos=q if causal else None)
+    got = out.cpu().reshape(BH * Lq, d)[torch.as_tensor(rows)]
+    err = rowwise_rel_err(got, ref)
+    print(f"attention_deferred Q{tuple(Q.shape)} K{tuple(K.shape)} causal={causal}: err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
+    return out
+
+
+@pytest.mark.parametrize("BH,L,d,causal", [(3, 200, 64, True), (2, 136, 128, False), (2, 8, 64, True),
+                                           (1, 1000, 128, True), (2, 64, 128, True), (1, 1, 64, True),
+                                           (2, 520, 64, False)])
+def test_attention_shapes(ops, BH, L, d, causal):
+    # ragged lengths (not multiples of the 64-key step or the 256-query block), one-key rows
+    _attn_check(ops, I.make_qkv_case(BH, L, d, causal, seed=L + d))
+
+
+@pytest.mark.parametrize("Lq,Lk,d", [(100, 300, 64), (300, 72, 128), (7, 1000, 128)])
+def test_attention_cross_lengths(ops, Lq, Lk, d):
+    # non-causal with different query and key lengths
+    a = I.make_qkv_case(2, Lq, d, False, seed=Lq)
+    b = I.make_qkv_case(2, Lk, d, False, seed=Lk + 1)
+    _attn_check(ops, dict(Q=a["Q"], K=b["K"], V=b["V"], causal=False, scale=a["scale"]))
+
+
+def test_attention_matches_softmax_pv_on_materialized_scores(ops):
+    # the same workload through S = Q K^T / sqrt(d) stored in bf16 and softmax_pv_deferred:
+    # the two differ only by the rounding of S to bf16
+    w = I.SMWorkload("attn_vs_sm", 202, 2, 384, 128, True, from_qk=True)
+    qkv, sm = I.make_qkv(w), I.make_sm(w)
+    a = ops.attention_deferred(cuda(qkv["Q"]), cuda(qkv["K"]), cuda(qkv["V"]), causal=True)
+    b = ops.softmax_pv_deferred(cuda(sm["S"]), cuda(sm["V"]), causal=True)
+    assert rowwise_rel_err(a.cpu().reshape(-1, 128), oracle.to_f64(b.cpu()).reshape(-1, 128)) <= TOL[torch.bfloat16]
+
+
+def test_attention_causal_workload_sampled(ops):
+    w = I.ATTN_CAUSAL
+    case = I.make_qkv(w)
+    rows = I.sample_rows(w.BH * w.L, 48, seed=11)
+    _attn_check(ops, case, rows=rows)
+
+
 # ---------------------------------------------------------------------------- unfused comparators
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_layernorm_unfused(ops, dtype):
