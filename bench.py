@@ -41,8 +41,8 @@ PEAK_HBM_GBS = 8000.0       # HBM3E
 
 # HBM traffic per launch, from two rocprofv3 --pmc runs of this script (FETCH_SIZE, then WRITE_SIZE,
 # KiB per dispatch, averaged over the timed launches), each scaled by what the same counter reads for
-# a plain device copy of 1 GiB in the same run (--calib-copy-mib 1024): FETCH_SIZE reads 524310 KiB
-# for its 1048576 KiB (x 1.99992), WRITE_SIZE reads 1048576 KiB (x 1.0).  A figure is only valid for
+# a plain device copy of 1 GiB in the same run (--calib-copy-mib 1024): FETCH_SIZE reads 524306 KiB
+# for its 1048576 KiB (x 1.99993), WRITE_SIZE reads 1048576 KiB (x 1.0).  A figure is only valid for
 # the kernel source it was taken on: each entry carries the sha256 of its kernel's source files, and
 # the bench reports null once they differ.
 KERNEL_SOURCES = {"softmax_pv_deferred": ("softmax_pv.hip", "dn_device.hpp"),
@@ -54,15 +54,19 @@ TRAFFIC = {
     ("softmax_pv_deferred", "causal_softmax_pv_bf16_32x8192x8192_d128"): {
         "sha256": ("4cb5880e7992356ce9815f38539bb72117dc54ee40675acb45549ac65f640d11",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 1150976, "fetch_scale": 1.99992, "write_kib": 66121, "write_scale": 1.0},
+        "fetch_kib": 1151051, "fetch_scale": 1.99993, "write_kib": 66101, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("f2ada0bd03f996f5cf64f20a33b9bb4976a138fb8888c1283f051d2eed70ca29",
+        "sha256": ("63ec905747a1507fefc8fc7815f05972b6145237c8cd467f4b565424b8969bb0",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 334012, "fetch_scale": 1.99992, "write_kib": 127488, "write_scale": 1.0},
+        "fetch_kib": 296661, "fetch_scale": 1.99993, "write_kib": 101380, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("f2ada0bd03f996f5cf64f20a33b9bb4976a138fb8888c1283f051d2eed70ca29",
+        "sha256": ("63ec905747a1507fefc8fc7815f05972b6145237c8cd467f4b565424b8969bb0",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 229804, "fetch_scale": 1.99992, "write_kib": 56, "write_scale": 1.0},
+        "fetch_kib": 229889, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
+    ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
+        "sha256": ("ab121a92cc11ed23f6564163328c1b99b04b11fe28476344ce74583bc7d16eb9",
+                   "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
+        "fetch_kib": 149377, "fetch_scale": 1.99993, "write_kib": 75087, "write_scale": 1.0},
 }
 
 
