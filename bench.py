@@ -454,6 +454,8 @@ def main():
             fi, u = float(np.median(fis)), float(np.median(us))
             k["isolated_ms"] = round(fi, 4)
             k["unfused_ms"] = round(u, 4)
+            k["isolated_spread_ms"] = [round(min(fis), 4), round(max(fis), 4)]  # over the 5 rounds
+            k["unfused_spread_ms"] = [round(min(us), 4), round(max(us), 4)]
             k["speedup_vs_unfused"] = round(u / fi, 3)
             if uds:
                 ud = float(np.median(uds))
