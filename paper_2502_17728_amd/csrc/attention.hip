@@ -186,19 +186,9 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
     const int qw0i = (int)qw0, kv_endi = (int)kv_end;  // positions fit 32 bits (checked by the host)
     const int qlast = qw0i + QW * 16 - 1;              // this wave's last query
 
-    for (int s = 0; s < NS - 1; ++s) issue_kv(s);
-    for (int s = 0; s < nsteps; ++s) {
-        wait_vmcnt_asm<(NS - 2) * KV_INS>();  // this wave's copies of step s have landed
-        wait_lgkm0();                         // its LDS reads of step s-1 are done
-        block_barrier();                      // ... and every wave's
-        issue_kv(s + NS - 1);                 // into the slot step s-1 vacated
-        const int k0 = s * BKV;
-        if (causal && k0 > qlast) continue;   // wholly above this wave's queries
-        const char* kb = smem + (s % NS) * SLOT;
-        const char* vb = kb + TILE;
-
-        // scores S^T: 4 blocks of 16 keys per query fragment
-        f32x4 st[QW][4];
+    // scores S^T of one step: 4 blocks of 16 keys per query fragment
+    auto scores = [&](int step, f32x4(&st)[QW][4]) {
+        const char* kb = smem + (step % NS) * SLOT;
 #pragma unroll
         for (int f = 0; f < QW; ++f)
 #pragma unroll
@@ -211,8 +201,11 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
 #pragma unroll
                 for (int f = 0; f < QW; ++f) st[f][b4] = mfma_chunk<__bf16>(kf, qf[f][c], st[f][b4]);
             }
-
-        // keys past the diagonal (causal) or past Lk are not part of the row
+    };
+    // numerators of one step (keys past the diagonal or past Lk masked first),
+    // with the reference max raised where needed; returns whether any lane raised it
+    auto numerators = [&](int step, f32x4(&st)[QW][4], u32x4(&pf)[QW][2], float(&alpha)[QW]) {
+        const int k0 = step * BKV;
         if ((causal && k0 + BKV - 1 > qw0i) || k0 + BKV > kv_endi) {
 #pragma unroll
             for (int f = 0; f < QW; ++f) {
@@ -224,10 +217,6 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
                         if (k0 + 16 * b4 + 4 * G + e > lim) st[f][b4][e] = -__builtin_inff();
             }
         }
-
-        // numerators, the reference max raised where needed
-        u32x4 pf[QW][2];
-        float alpha[QW];
         bool raised = false;
 #pragma unroll
         for (int f = 0; f < QW; ++f) {
@@ -254,16 +243,11 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
                                   pack_bf16(p[2 * kc + 1][0], p[2 * kc + 1][1]),
                                   pack_bf16(p[2 * kc + 1][2], p[2 * kc + 1][3])};
         }
-        if (__any(raised)) {
-#pragma unroll
-            for (int f = 0; f < QW; ++f) {
-#pragma unroll
-                for (int b = 0; b < DB; ++b) acc[f][b] *= alpha[f];
-                accl[f] *= alpha[f];
-            }
-        }
-
-        // out^T += V^T . P~^T, keys of chunk kc in the order of the numerators
+        return raised;
+    };
+    // out^T += V^T . P~^T, keys of chunk kc in the order of the numerators
+    auto products = [&](int step, const u32x4(&pf)[QW][2]) {
+        const char* vb = smem + (step % NS) * SLOT + TILE;
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) {
             u32x4 vf[DB];
@@ -280,6 +264,33 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
 #pragma unroll
             for (int f = 0; f < QW; ++f) accl[f] = mfma_chunk<__bf16>(ones, pf[f][kc], accl[f]);
         }
+    };
+    auto rescale = [&](bool raised, const float(&alpha)[QW]) {
+        if (__any(raised)) {
+#pragma unroll
+            for (int f = 0; f < QW; ++f) {
+#pragma unroll
+                for (int b = 0; b < DB; ++b) acc[f][b] *= alpha[f];
+                accl[f] *= alpha[f];
+            }
+        }
+    };
+    auto active = [&](int step) { return step < nsteps && !(causal && step * BKV > qlast); };
+
+    for (int s = 0; s < NS - 1; ++s) issue_kv(s);
+    for (int s = 0; s < nsteps; ++s) {
+        wait_vmcnt_asm<(NS - 2) * KV_INS>();  // this wave's copies of step s have landed
+        wait_lgkm0();                         // its LDS reads of step s-1 are done
+        block_barrier();                      // ... and every wave's
+        issue_kv(s + NS - 1);                 // into the slot step s-1 vacated
+        if (!active(s)) continue;             // wholly above this wave's queries
+        f32x4 st[QW][4];
+        scores(s, st);
+        u32x4 pf[QW][2];
+        float alpha[QW];
+        const bool raised = numerators(s, st, pf, alpha);
+        rescale(raised, alpha);
+        products(s, pf);
     }
     wait_vmcnt_asm<0>();  // no copy into LDS may outlive the workgroup
 
@@ -312,6 +323,8 @@ static hipError_t run_attention(const void* Q, const void* K, const void* V, int
 
 hipError_t launch_attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,
                                      int64_t Lk, int64_t d, int causal, float scale, void* out, hipStream_t s) {
+    // 8 waves x 2 query fragments (256 queries per workgroup), two ring slots: measured fastest
+    // against 3 slots, 1 or 3 fragments, and 4 waves on the causal 32 x 8192 x 8192, d = 128
     if (d == 64) return run_attention<64, 8, 2, 2>(Q, K, V, BH, Lq, Lk, causal, scale, out, s);
     return run_attention<128, 8, 2, 2>(Q, K, V, BH, Lq, Lk, causal, scale, out, s);
 }
