@@ -22,7 +22,7 @@
 // one more MFMA per chunk with A = all ones.
 //
 // Data movement.  One workgroup owns NW x QW x 16 queries of one head and walks
-// the keys in steps of 64.  K and V tiles ([64 keys][d], row-major) share an
+// the keys in steps of BKV (128).  K and V tiles ([BKV keys][d], row-major) share an
 // NS-slot ring in LDS filled by global->LDS copies of whole KiB (one barrier
 // per step); 16-byte pieces are XOR-swizzled per key row so that the K
 // fragment reads (16 rows at one piece) and the transposing V^T reads
@@ -71,7 +71,7 @@ __device__ __forceinline__ uint2 lds_tr16(const char* p) {
 }
 }  // namespace fa
 
-template <int D, int NW, int QW, int NS>
+template <int D, int NW, int QW, int NS, int BKV>
 __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __restrict__ Q,
                                                             const __bf16* __restrict__ K,
                                                             const __bf16* __restrict__ V, int64_t Lq,
@@ -79,7 +79,8 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
                                                             __bf16* __restrict__ out) {
     using namespace fa;
     constexpr int BQ = NW * QW * 16;   // queries per workgroup
-    constexpr int BKV = 64;            // keys per step
+    constexpr int NKB = BKV / 16;      // 16-key S^T blocks per step
+    constexpr int NKC = BKV / 32;      // 32-key chunks of the P.V product per step
     constexpr int ROW = D * 2;         // bytes per K or V row
     constexpr int TILE = BKV * ROW;    // one K (or V) tile
     constexpr int SLOT = 2 * TILE;     // ring slot: K tile, then V tile
@@ -187,14 +188,14 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
     const int qlast = qw0i + QW * 16 - 1;              // this wave's last query
 
     // scores S^T of one step: 4 blocks of 16 keys per query fragment
-    auto scores = [&](int step, f32x4(&st)[QW][4]) {
+    auto scores = [&](int step, f32x4(&st)[QW][NKB]) {
         const char* kb = smem + (step % NS) * SLOT;
 #pragma unroll
         for (int f = 0; f < QW; ++f)
 #pragma unroll
-            for (int b4 = 0; b4 < 4; ++b4) st[f][b4] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int b4 = 0; b4 < NKB; ++b4) st[f][b4] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int b4 = 0; b4 < 4; ++b4)
+        for (int b4 = 0; b4 < NKB; ++b4)
 #pragma unroll
             for (int c = 0; c < DC; ++c) {
                 const u32x4 kf = lds_ld16(lds_ptr((char*)kb + b4 * 16 * ROW + k_rd[c]));
@@ -204,14 +205,14 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
     };
     // numerators of one step (keys past the diagonal or past Lk masked first),
     // with the reference max raised where needed; returns whether any lane raised it
-    auto numerators = [&](int step, f32x4(&st)[QW][4], u32x4(&pf)[QW][2], float(&alpha)[QW]) {
+    auto numerators = [&](int step, f32x4(&st)[QW][NKB], u32x4(&pf)[QW][NKC], float(&alpha)[QW]) {
         const int k0 = step * BKV;
         if ((causal && k0 + BKV - 1 > qw0i) || k0 + BKV > kv_endi) {
 #pragma unroll
             for (int f = 0; f < QW; ++f) {
                 const int lim = causal ? min((int)qrow[f], kv_endi - 1) : kv_endi - 1;
 #pragma unroll
-                for (int b4 = 0; b4 < 4; ++b4)
+                for (int b4 = 0; b4 < NKB; ++b4)
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         if (k0 + 16 * b4 + 4 * G + e > lim) st[f][b4][e] = -__builtin_inff();
@@ -222,7 +223,7 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
         for (int f = 0; f < QW; ++f) {
             float tmax = st[f][0][0];
 #pragma unroll
-            for (int b4 = 0; b4 < 4; ++b4)
+            for (int b4 = 0; b4 < NKB; ++b4)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) tmax = __builtin_fmaxf(tmax, st[f][b4][e]);
             const float tmax2 = max_lane_groups(tmax) * sl2;
@@ -232,13 +233,13 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
             mref[f] = mnew;
             raised |= raise;
             const float nb = mnew == -__builtin_inff() ? 0.f : -mnew;
-            float p[4][4];
+            float p[NKB][4];
 #pragma unroll
-            for (int b4 = 0; b4 < 4; ++b4)
+            for (int b4 = 0; b4 < NKB; ++b4)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) p[b4][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(st[f][b4][e], sl2, nb));
 #pragma unroll
-            for (int kc = 0; kc < 2; ++kc)
+            for (int kc = 0; kc < NKC; ++kc)
                 pf[f][kc] = u32x4{pack_bf16(p[2 * kc][0], p[2 * kc][1]), pack_bf16(p[2 * kc][2], p[2 * kc][3]),
                                   pack_bf16(p[2 * kc + 1][0], p[2 * kc + 1][1]),
                                   pack_bf16(p[2 * kc + 1][2], p[2 * kc + 1][3])};
@@ -246,10 +247,10 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
         return raised;
     };
     // out^T += V^T . P~^T, keys of chunk kc in the order of the numerators
-    auto products = [&](int step, const u32x4(&pf)[QW][2]) {
+    auto products = [&](int step, const u32x4(&pf)[QW][NKC]) {
         const char* vb = smem + (step % NS) * SLOT + TILE;
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
+        for (int kc = 0; kc < NKC; ++kc) {
             u32x4 vf[DB];
 #pragma unroll
             for (int b = 0; b < DB; ++b) {
@@ -284,9 +285,9 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
         block_barrier();                      // ... and every wave's
         issue_kv(s + NS - 1);                 // into the slot step s-1 vacated
         if (!active(s)) continue;             // wholly above this wave's queries
-        f32x4 st[QW][4];
+        f32x4 st[QW][NKB];
         scores(s, st);
-        u32x4 pf[QW][2];
+        u32x4 pf[QW][NKC];
         float alpha[QW];
         const bool raised = numerators(s, st, pf, alpha);
         rescale(raised, alpha);
@@ -310,12 +311,12 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
     }
 }
 
-template <int D, int NW, int QW, int NS>
+template <int D, int NW, int QW, int NS, int BKV>
 static hipError_t run_attention(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq, int64_t Lk,
                                 int causal, float scale, void* out, hipStream_t s) {
     constexpr int BQ = NW * QW * 16;
     const int nqb = (int)((Lq + BQ - 1) / BQ);
-    attention_kernel<D, NW, QW, NS><<<dim3((unsigned)(BH * nqb)), NW * 64, 0, s>>>(
+    attention_kernel<D, NW, QW, NS, BKV><<<dim3((unsigned)(BH * nqb)), NW * 64, 0, s>>>(
         (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, causal, scale * fa::kLog2e, nqb,
         (__bf16*)out);
     return hipGetLastError();
@@ -323,10 +324,11 @@ static hipError_t run_attention(const void* Q, const void* K, const void* V, int
 
 hipError_t launch_attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,
                                      int64_t Lk, int64_t d, int causal, float scale, void* out, hipStream_t s) {
-    // 8 waves x 2 query fragments (256 queries per workgroup), two ring slots: measured fastest
-    // against 3 slots, 1 or 3 fragments, and 4 waves on the causal 32 x 8192 x 8192, d = 128
-    if (d == 64) return run_attention<64, 8, 2, 2>(Q, K, V, BH, Lq, Lk, causal, scale, out, s);
-    return run_attention<128, 8, 2, 2>(Q, K, V, BH, Lq, Lk, causal, scale, out, s);
+    // 8 waves x 2 query fragments (256 queries per workgroup), two ring slots of 128 keys
+    // (128 KiB of LDS at d = 128): measured fastest against 64-key steps, 3 slots, 1 or 3
+    // fragments, and 4 waves on the causal 32 x 8192 x 8192, d = 128
+    if (d == 64) return run_attention<64, 8, 2, 2, 128>(Q, K, V, BH, Lq, Lk, causal, scale, out, s);
+    return run_attention<128, 8, 2, 2, 128>(Q, K, V, BH, Lq, Lk, causal, scale, out, s);
 }
 
 }  // namespace dn
