@@ -47,6 +47,7 @@ PEAK_HBM_GBS = 8000.0       # HBM3E
 # the bench reports null once they differ.
 KERNEL_SOURCES = {"softmax_pv_deferred": ("softmax_pv.hip", "dn_device.hpp"),
                   "attention_deferred": ("attention.hip", "dn_device.hpp"),
+                  "attention_decode_deferred": ("attention.hip", "dn_device.hpp"),
                   "ln_linear_deferred": ("ln_gemm.hip", "dn_device.hpp"),
                   "rms_linear_deferred": ("ln_gemm.hip", "dn_device.hpp"),
                   "rms_swiglu_deferred": ("ln_gemm.hip", "dn_device.hpp")}
@@ -94,7 +95,8 @@ def parse():
     ap.add_argument("--workload", default="layer",
                     choices=["layer", "small", "ln_qkv", "causal_softmax_pv", "ffn_prefill",
                              "ffn_decode_t1", "ffn_decode_t4", "ffn_decode_t16", "rms_qkv",
-                             "rms_ffn_decode_t1", "swiglu_prefill", "swiglu_decode_t1", "causal_attention"])
+                             "rms_ffn_decode_t1", "swiglu_prefill", "swiglu_decode_t1", "causal_attention",
+                             "decode_attention"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None)
@@ -328,6 +330,56 @@ class AttnSite:
         return dt, kept / w.pairs(), f"{len(idx)} of {w.BH * w.L} attention rows"
 
 
+class DecodeAttnSite:
+    """Decode attention: the keys split over workgroups, partials merged (Eq. (8) over key ranges)."""
+    kernel = "attention_decode_deferred"
+
+    def __init__(self, ops, I, w):
+        self.w = w
+        self.case = I.make_decode(w)
+        c = self.case
+        self.Q, self.K, self.V = c["Q"].cuda(), c["K"].cuda(), c["V"].cuda()
+        self.out = torch.empty_like(self.Q)
+        self.ws = torch.empty(ops.attention_decode_workspace_bytes(w.BH, w.Lq, w.Lk, w.d), dtype=torch.uint8,
+                              device="cuda")
+        # conventional comparator: S = (scale Q) K^T stored, then deferred Softmax -> P.V on S
+        self.Qs = (self.Q.float() * c["scale"]).to(torch.bfloat16)
+        self.S = torch.empty((w.BH, w.Lq, w.Lk), dtype=torch.bfloat16, device="cuda")
+        self.ops = ops
+        torch.cuda.synchronize()
+
+    def fused(self):
+        self.ops.attention_decode_deferred(self.Q, self.K, self.V, scale=self.case["scale"], workspace=self.ws,
+                                           out=self.out)
+
+    def unfused(self):
+        self.ops.gemm(self.Qs, self.K, b_layout=1, out=self.S)
+        self.ops.softmax_pv_deferred(self.S, self.V, out=self.out)
+
+    def single_pass(self):
+        # ablation: the same computation without the key split (one workgroup per head)
+        self.ops.attention_deferred(self.Q, self.K, self.V, causal=False, scale=self.case["scale"], out=self.out)
+
+    def flops(self):
+        return self.w.flops()
+
+    def bytes(self):
+        return self.w.bytes()
+
+    def peak_tflops(self):
+        return PEAK_BF16_TFLOPS
+
+    def oracle_sample(self, oracle, I, threads, rows):
+        w = self.w
+        heads = I.sample_rows(w.BH, max(1, rows // w.Lq), seed=12)
+        hsel = torch.as_tensor(heads)
+        t0 = time.perf_counter()
+        oracle.attention(self.case["Q"][hsel].reshape(-1, w.d), self.case["K"][hsel], self.case["V"][hsel],
+                         self.case["scale"], head=np.repeat(np.arange(len(heads)), w.Lq), nthreads=threads)
+        dt = time.perf_counter() - t0
+        return dt, len(heads) / w.BH, f"{len(heads)} of {w.BH} decode heads"
+
+
 def build_sites(ops, I, name):
     if name == "layer":
         return [LNSite(ops, I, I.LN_QKV), SMSite(ops, I, I.SM_CAUSAL)], \
@@ -345,6 +397,8 @@ def build_sites(ops, I, name):
         return [LNSite(ops, I, I.RMS_QKV)], I.RMS_QKV.name
     if name == "causal_attention":
         return [AttnSite(ops, I, I.ATTN_CAUSAL)], I.ATTN_CAUSAL.name
+    if name == "decode_attention":
+        return [DecodeAttnSite(ops, I, I.ATTN_DECODE)], I.ATTN_DECODE.name
     if name == "swiglu_prefill":
         return [SwiGLUSite(ops, I, I.SWIGLU_PREFILL)], I.SWIGLU_PREFILL.name
     if name == "swiglu_decode_t1":
@@ -428,7 +482,7 @@ def main():
     kernels = {}
     dom = max(range(len(sites)), key=lambda i: per[i])
     for i, s in enumerate(sites):
-        name = s.kernel if isinstance(s, (LNSite, SwiGLUSite, AttnSite)) else "softmax_pv_deferred"
+        name = s.kernel if isinstance(s, (LNSite, SwiGLUSite, AttnSite, DecodeAttnSite)) else "softmax_pv_deferred"
         tf = s.flops() / (per[i] * 1e-3) / 1e12
         gbs = s.bytes() / (per[i] * 1e-3) / 1e9
         k = {"workload": s.w.name, "ms": round(per[i], 4), "tflops": round(tf, 2),
@@ -442,7 +496,7 @@ def main():
             # (inside the step the kernel follows the other site, whose traffic evicts the caches);
             # the two alternate over 5 rounds and each reports its median
             n = max(3, args.steps // 2)
-            fis, us, uds, sers = [], [], [], []
+            fis, us, uds, sers, sps = [], [], [], [], []
             serial = isinstance(s, LNSite) and not s.rms and s.w.K <= 16384
             for _ in range(5):
                 fis.append(time_steps([s.fused], n, 2)[0][0])
@@ -451,6 +505,8 @@ def main():
                     uds.append(time_steps([s.unfused_dense], max(3, n // 2), 1)[0][0])
                 if serial:
                     sers.append(time_steps([s.serial], n, 2)[0][0])
+                if isinstance(s, DecodeAttnSite):
+                    sps.append(time_steps([s.single_pass], n, 2)[0][0])
             fi, u = float(np.median(fis)), float(np.median(us))
             k["isolated_ms"] = round(fi, 4)
             k["unfused_ms"] = round(u, 4)
@@ -465,11 +521,15 @@ def main():
                 se = float(np.median(sers))
                 k["serial_stats_ms"] = round(se, 4)
                 k["speedup_vs_serial_stats"] = round(se / fi, 3)
+            if sps:  # ablation: no key split (one workgroup per head)
+                sp = float(np.median(sps))
+                k["single_pass_ms"] = round(sp, 4)
+                k["speedup_vs_single_pass"] = round(sp / fi, 3)
         kernels[name] = k
 
     d = sites[dom]
     dname = list(kernels)[dom]
-    hbm_bound = isinstance(d, SMSite) or (isinstance(d, (LNSite, SwiGLUSite)) and d.w.M <= 16)
+    hbm_bound = isinstance(d, (SMSite, DecodeAttnSite)) or (isinstance(d, (LNSite, SwiGLUSite)) and d.w.M <= 16)
     if hbm_bound:
         ach = d.bytes() / (per[dom] * 1e-3) / 1e9
         roof = {"kernel": dname, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
@@ -494,6 +554,8 @@ def main():
                 rows = s.w.M
             if isinstance(s, (SMSite, AttnSite)):
                 rows = 1024 if s.w.L >= 4096 else 2048
+            if isinstance(s, DecodeAttnSite):
+                rows = 128
             dt, frac, desc = s.oracle_sample(oracle, I, threads, rows)
             extrap += dt / frac
             descs.append(desc)

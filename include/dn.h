@@ -223,6 +223,27 @@ DN_API dn_status attention_deferred(const void* Q, const void* K, const void* V,
                              int64_t Lq, int64_t Lk, int64_t d, int causal, float scale,
                              int dtype, void* out, hipStream_t stream);
 
+/*
+ * Decode-shaped attention: Lq <= 16 query rows per head against all Lk keys
+ * (the key/value cache holds exactly the visible keys, so no mask).  The keys
+ * are cut into ranges, one workgroup each, that leave their un-normalized
+ * partial sums (acc, l and the reference max m, fp32) in `workspace`; one
+ * merge kernel then combines them, m = max m_g, out = sum 2^(m_g - m) acc_g /
+ * sum 2^(m_g - m) l_g -- the deferred division of Eq. (8) once more, across
+ * key ranges.  workspace: caller-owned device memory of
+ * attention_decode_workspace_bytes(BH, Lq, Lk, d) bytes, 16-byte aligned, not
+ * overlapping the other arguments; its contents are scratch.  Q[BH][Lq][d],
+ * K, V[BH][Lk][d], out[BH][Lq][d]; other rules as attention_deferred
+ * (DN_ERR_UNSUPPORTED for Lq > 16).  attention_decode_workspace_bytes
+ * returns 0 for an invalid request.
+ */
+DN_API size_t attention_decode_workspace_bytes(int64_t BH, int64_t Lq, int64_t Lk, int64_t d);
+
+DN_API dn_status attention_decode_deferred(const void* Q, const void* K, const void* V, int64_t BH,
+                                    int64_t Lq, int64_t Lk, int64_t d, float scale, int dtype,
+                                    void* workspace, size_t workspace_bytes, void* out,
+                                    hipStream_t stream);
+
 /* ======================================================================= */
 /* Unfused comparators: the conventional sub-graph of Fig. 1(a)             */
 /* ======================================================================= */

@@ -228,6 +228,35 @@ DN_API dn_status attention_deferred(const void* Q, const void* K, const void* V,
     return from_hip(dn::launch_attention_deferred(Q, K, V, BH, Lq, Lk, d, causal, scale, out, stream));
 }
 
+DN_API size_t attention_decode_workspace_bytes(int64_t BH, int64_t Lq, int64_t Lk, int64_t d) {
+    size_t b;
+    if (BH < 1 || Lq < 1 || Lq > 16 || Lk < 1 || (d != 64 && d != 128) || !bytes_of(BH, Lk, d * 2, &b))
+        return 0;
+    return dn::attention_decode_workspace_bytes(BH, Lq, Lk, d);
+}
+
+DN_API dn_status attention_decode_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,
+                                           int64_t Lk, int64_t d, float scale, int dtype, void* workspace,
+                                           size_t workspace_bytes, void* out, hipStream_t stream) {
+    if (!Q || !K || !V || !out || !workspace || BH < 1 || Lq < 1 || Lk < 1 || d < 1 || !valid_dtype(dtype))
+        return DN_ERR_INVALID_ARG;
+    if (!isfinite(scale) || !(scale > 0.f)) return DN_ERR_INVALID_ARG;
+    size_t qb, kb;
+    if (!bytes_of(BH, Lq, d * 2, &qb) || !bytes_of(BH, Lk, d * 2, &kb)) return DN_ERR_INVALID_ARG;
+    if (dtype != DN_BF16 || (d != 64 && d != 128) || Lq > 16) return DN_ERR_UNSUPPORTED;
+    if (Lk * d * 2 >= (int64_t(1) << 31)) return DN_ERR_UNSUPPORTED;
+    const size_t need = attention_decode_workspace_bytes(BH, Lq, Lk, d);
+    if (need == 0 || workspace_bytes < need) return DN_ERR_INVALID_ARG;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(workspace, 16))
+        return DN_ERR_MISALIGNED;
+    if (overlaps(out, qb, Q, qb) || overlaps(out, qb, K, kb) || overlaps(out, qb, V, kb) ||
+        overlaps(workspace, need, Q, qb) || overlaps(workspace, need, K, kb) || overlaps(workspace, need, V, kb) ||
+        overlaps(workspace, need, out, qb))
+        return DN_ERR_INVALID_ARG;
+    if (BH * 1024 > kMaxGridX) return DN_ERR_UNSUPPORTED;
+    return from_hip(dn::launch_attention_decode(Q, K, V, BH, Lq, Lk, d, scale, workspace, out, stream));
+}
+
 static dn_status row_norm(const void* x, const void* gamma, const void* beta, int64_t M, int64_t K, float eps,
                           int rms, int dtype, void* y, hipStream_t stream) {
     if (!x || !gamma || !y || M < 1 || K < 1 || !valid_dtype(dtype)) return DN_ERR_INVALID_ARG;

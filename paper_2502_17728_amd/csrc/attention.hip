@@ -30,6 +30,8 @@
 // above the workgroup's queries are never read; a wave skips the products of
 // steps wholly above its own queries; keys above the diagonal inside a step
 // are masked to -inf before the exponentials.
+#include <algorithm>
+
 #include "dn_device.hpp"
 #include "dn_launch.hpp"
 
@@ -76,6 +78,7 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
                                                             const __bf16* __restrict__ K,
                                                             const __bf16* __restrict__ V, int64_t Lq,
                                                             int64_t Lk, int causal, float sl2, int nqb,
+                                                            int nsplit, int64_t kchunk, float* __restrict__ part,
                                                             __bf16* __restrict__ out) {
     using namespace fa;
     constexpr int BQ = NW * QW * 16;   // queries per workgroup
@@ -96,13 +99,18 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // logical id: XCD-contiguous; each XCD walks whole heads, longest query blocks first
-    const int t = xcd_contiguous(blockIdx.x, gridDim.x);
+    // logical id: XCD-contiguous; each XCD walks whole heads, longest query blocks first.
+    // Split mode (part != null): the keys are cut into nsplit ranges of kchunk, one per
+    // workgroup, each leaving its un-normalized partial sums for the merge kernel.
+    const int t0 = xcd_contiguous(blockIdx.x, gridDim.x);
+    const int sp = t0 % nsplit, t = t0 / nsplit;
     const int h = t / nqb;
     const int qb = causal ? (nqb - 1 - t % nqb) : (t % nqb);
     const int64_t q0 = (int64_t)qb * BQ;
     const int64_t kv_end = causal ? min(Lk, q0 + BQ) : Lk;
-    const int nsteps = (int)((kv_end + BKV - 1) / BKV);
+    const int64_t k_lo = (int64_t)sp * kchunk;                  // this workgroup's keys: [k_lo, k_hi)
+    const int64_t k_hi = min(kv_end, k_lo + kchunk);
+    const int nsteps = (int)((k_hi - k_lo + BKV - 1) / BKV);
 
     const __bf16* Qh = Q + (int64_t)h * Lq * D;
     const __bf16* Kh = K + (int64_t)h * Lk * D;
@@ -143,7 +151,7 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
     const uint32_t smem_addr = lds_addr32(smem);
     auto issue_kv = [&](int step) {
         const uint32_t base = smem_addr + (uint32_t)((step % NS) * SLOT);
-        const uint32_t k0 = (uint32_t)step * BKV;
+        const uint32_t k0 = (uint32_t)k_lo + (uint32_t)step * BKV;
 #pragma unroll
         for (int j = 0; j < T_INS; ++j) {
             const uint32_t key = k0 + c_row[j] < last ? k0 + c_row[j] : last;  // a select, no branch
@@ -184,7 +192,7 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
 #pragma unroll
     for (int f = 0; f < QW; ++f) mref[f] = -__builtin_inff();
 
-    const int qw0i = (int)qw0, kv_endi = (int)kv_end;  // positions fit 32 bits (checked by the host)
+    const int qw0i = (int)qw0, kv_endi = (int)k_hi;  // positions fit 32 bits (checked by the host)
     const int qlast = qw0i + QW * 16 - 1;              // this wave's last query
 
     // scores S^T of one step: 4 blocks of 16 keys per query fragment
@@ -206,7 +214,7 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
     // numerators of one step (keys past the diagonal or past Lk masked first),
     // with the reference max raised where needed; returns whether any lane raised it
     auto numerators = [&](int step, f32x4(&st)[QW][NKB], u32x4(&pf)[QW][NKC], float(&alpha)[QW]) {
-        const int k0 = step * BKV;
+        const int k0 = (int)k_lo + step * BKV;
         if ((causal && k0 + BKV - 1 > qw0i) || k0 + BKV > kv_endi) {
 #pragma unroll
             for (int f = 0; f < QW; ++f) {
@@ -276,7 +284,7 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
             }
         }
     };
-    auto active = [&](int step) { return step < nsteps && !(causal && step * BKV > qlast); };
+    auto active = [&](int step) { return step < nsteps && !(causal && (int)k_lo + step * BKV > qlast); };
 
     for (int s = 0; s < NS - 1; ++s) issue_kv(s);
     for (int s = 0; s < nsteps; ++s) {
@@ -294,6 +302,23 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
         products(s, pf);
     }
     wait_vmcnt_asm<0>();  // no copy into LDS may outlive the workgroup
+
+    if (part) {
+        // split mode: the partial (acc[d], l, m, 2 pad) of each query row, fp32, for the merge
+#pragma unroll
+        for (int f = 0; f < QW; ++f) {
+            if (qrow[f] >= Lq) continue;
+            float* pr = part + (((int64_t)h * Lq + qrow[f]) * nsplit + sp) * (D + 4);  // 16-byte rows
+#pragma unroll
+            for (int b = 0; b < DB; ++b)
+                *reinterpret_cast<f32x4*>(pr + b * 16 + 4 * G) = acc[f][b];
+            if (G == 0) {
+                pr[D] = accl[f][0];
+                pr[D + 1] = mref[f];
+            }
+        }
+        return;
+    }
 
     // ---- epilogue: the single deferred division, one rounding to bf16
 #pragma unroll
@@ -317,9 +342,74 @@ static hipError_t run_attention(const void* Q, const void* K, const void* V, int
     constexpr int BQ = NW * QW * 16;
     const int nqb = (int)((Lq + BQ - 1) / BQ);
     attention_kernel<D, NW, QW, NS, BKV><<<dim3((unsigned)(BH * nqb)), NW * 64, 0, s>>>(
-        (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, causal, scale * fa::kLog2e, nqb,
-        (__bf16*)out);
+        (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, causal, scale * fa::kLog2e, nqb, 1, Lk,
+        nullptr, (__bf16*)out);
     return hipGetLastError();
+}
+
+// Merge of the split partials (the log-sum-exp combination of Eq. (8) over key
+// ranges): m = max_g m_g, out = sum_g 2^(m_g - m) acc_g / sum_g 2^(m_g - m) l_g,
+// one wave per query row.
+template <int D>
+__global__ __launch_bounds__(256) void attention_merge_kernel(const float* __restrict__ part, int nsplit,
+                                                              int64_t rows, __bf16* __restrict__ out) {
+    constexpr int PER = D / 64;
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const float* pr = part + row * nsplit * (D + 4);
+    float m = -__builtin_inff();
+    for (int g = 0; g < nsplit; ++g) m = __builtin_fmaxf(m, pr[g * (D + 4) + D + 1]);
+    float l = 0.f, acc[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) acc[j] = 0.f;
+    for (int g = 0; g < nsplit; ++g) {
+        const float* pg = pr + g * (D + 4);
+        const float w = __builtin_amdgcn_exp2f(pg[D + 1] - m);
+        l = __builtin_fmaf(w, pg[D], l);
+#pragma unroll
+        for (int j = 0; j < PER; ++j) acc[j] = __builtin_fmaf(w, pg[lane + 64 * j], acc[j]);
+    }
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) out[row * D + lane + 64 * j] = (__bf16)(acc[j] * inv);
+}
+
+// Decode split: about 1024 workgroups over the heads, each a whole number of 64-key steps.
+void attention_decode_split(int64_t BH, int64_t Lk, int* nsplit, int64_t* kchunk) {
+    const int64_t steps = (Lk + 63) / 64;
+    const int64_t want = std::max<int64_t>(1, std::min<int64_t>(steps, (1024 + BH - 1) / BH));
+    const int64_t per = (steps + want - 1) / want;  // steps per split
+    *kchunk = per * 64;
+    *nsplit = (int)((Lk + *kchunk - 1) / *kchunk);
+}
+
+template <int D>
+static hipError_t run_attention_decode(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,
+                                       int64_t Lk, float scale, float* part, void* out, hipStream_t s) {
+    int nsplit;
+    int64_t kchunk;
+    attention_decode_split(BH, Lk, &nsplit, &kchunk);
+    // one wave of 16 queries per workgroup (Lq <= 16), 64-key steps, two ring slots
+    attention_kernel<D, 1, 1, 2, 64><<<dim3((unsigned)(BH * nsplit)), 64, 0, s>>>(
+        (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, 0, scale * fa::kLog2e, 1, nsplit, kchunk,
+        part, nullptr);
+    const int64_t rows = BH * Lq;
+    attention_merge_kernel<D><<<dim3((unsigned)((rows + 3) / 4)), 256, 0, s>>>(part, nsplit, rows, (__bf16*)out);
+    return hipGetLastError();
+}
+
+size_t attention_decode_workspace_bytes(int64_t BH, int64_t Lq, int64_t Lk, int64_t d) {
+    int nsplit;
+    int64_t kchunk;
+    attention_decode_split(BH, Lk, &nsplit, &kchunk);
+    return (size_t)BH * (size_t)Lq * (size_t)nsplit * (size_t)(d + 4) * sizeof(float);
+}
+
+hipError_t launch_attention_decode(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq, int64_t Lk,
+                                   int64_t d, float scale, void* workspace, void* out, hipStream_t s) {
+    if (d == 64) return run_attention_decode<64>(Q, K, V, BH, Lq, Lk, scale, (float*)workspace, out, s);
+    return run_attention_decode<128>(Q, K, V, BH, Lq, Lk, scale, (float*)workspace, out, s);
 }
 
 hipError_t launch_attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,

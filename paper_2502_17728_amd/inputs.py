@@ -23,6 +23,8 @@ variance v):
 - Softmax -> P.V: either S ~ N(0, s^2) directly (no mask), or S = Q K^T /
   sqrt(d) in fp32 from bf16-rounded Q, K ~ N(0, 1) with keys j > i set to
   -inf (causal); V ~ N(0, 1).
+- Attention from Q, K, V: Q, K, V ~ N(0, 1) rounded to bf16, scale 1/sqrt(d);
+  decode attention draws Q[Lq] and the cache K, V[Lk] the same way.
 """
 from __future__ import annotations
 
@@ -93,6 +95,34 @@ def ln_ffn_decode(t: int) -> LNWorkload:
 # workload's own tensors, 32 heads x 8192 tokens, d = 128.
 ATTN_CAUSAL = SMWorkload("causal_attention_bf16_32x8192x8192_d128", 4, 32, 8192, 128, causal=True, from_qk=True)
 
+
+
+@dataclasses.dataclass(frozen=True)
+class DecodeAttnWorkload:
+    """Attention of a few new query tokens against a cache of Lk keys (every key visible)."""
+    name: str
+    wid: int
+    BH: int            # sequences x heads
+    Lq: int            # new tokens per sequence (<= 16)
+    Lk: int            # cached keys
+    d: int             # head dim
+
+    def pairs(self) -> float:
+        return float(self.BH) * self.Lq * self.Lk
+
+    def flops(self) -> float:
+        return 4.0 * self.pairs() * self.d  # both products
+
+    def bytes(self) -> float:
+        """Algorithmic HBM bytes: K and V read once, Q read and the output written (bf16)."""
+        return 2.0 * (2.0 * self.BH * self.Lk * self.d + 2.0 * self.BH * self.Lq * self.d)
+
+
+# Decode attention: 8 sequences x 32 heads, one new token each against 8192 cached
+# keys of d = 128 (1 GiB of K and V, larger than the last-level cache).
+ATTN_DECODE = DecodeAttnWorkload("decode_attention_bf16_256x1x8192_d128", 10, 256, 1, 8192, 128)
+
+
 # RMSNorm -> Linear with Llama shapes: the fused QKV projection of an 8B-class
 # model with grouped-query attention (32 query + 2 x 8 key/value heads of 128
 # over hidden 4096), and the 70B-class FFN up-projection at decode.
@@ -118,7 +148,8 @@ def swiglu_decode(t: int) -> LNWorkload:
 
 WORKLOADS = {w.name: w for w in (LN_F32_SMALL, SM_BF16_SMALL, LN_QKV, SM_CAUSAL, LN_FFN_PREFILL,
                                  ln_ffn_decode(1), ln_ffn_decode(4), ln_ffn_decode(16),
-                                 RMS_QKV, rms_ffn_decode(1), SWIGLU_PREFILL, swiglu_decode(1), ATTN_CAUSAL)}
+                                 RMS_QKV, rms_ffn_decode(1), SWIGLU_PREFILL, swiglu_decode(1), ATTN_CAUSAL,
+                                 ATTN_DECODE)}
 
 # tensor ids inside a workload's seed
 _X, _GAMMA, _BETA, _W, _OUTLIER_CH, _S, _Q, _KEY, _V, _W_UP = range(10)
@@ -242,6 +273,23 @@ def make_qkv(w: SMWorkload, seed: int = 0, heads: Optional[Sequence[int]] = None
 def make_qkv_case(BH: int, L: int, d: int, causal: bool, seed: int = 0) -> dict:
     """Q, K, V of any size with the same recipe (for parity tests)."""
     return make_qkv(SMWorkload(f"attn_{BH}x{L}_d{d}", 201, BH, L, d, causal, from_qk=True), seed)
+
+
+def make_decode(w: DecodeAttnWorkload, seed: int = 0, heads: Optional[Sequence[int]] = None) -> dict:
+    """Q[n, Lq, d] and the cache K, V[n, Lk, d] (bf16 CPU tensors) of the listed heads."""
+    heads = list(range(w.BH)) if heads is None else list(heads)
+    Q = torch.empty((len(heads), w.Lq, w.d), dtype=torch.bfloat16)
+    K, V = (torch.empty((len(heads), w.Lk, w.d), dtype=torch.bfloat16) for _ in range(2))
+    for i, h in enumerate(heads):
+        Q[i] = to_storage(_normal(_rng(seed, w.wid, _Q, h), (w.Lq, w.d), 1.0), "bf16")
+        K[i] = to_storage(_normal(_rng(seed, w.wid, _KEY, h), (w.Lk, w.d), 1.0), "bf16")
+        V[i] = to_storage(_normal(_rng(seed, w.wid, _V, h), (w.Lk, w.d), 1.0), "bf16")
+    return dict(Q=Q, K=K, V=V, causal=False, scale=1.0 / math.sqrt(w.d))
+
+
+def make_decode_case(BH: int, Lq: int, Lk: int, d: int, seed: int = 0) -> dict:
+    """A decode-attention case of any size with the same recipe (for parity tests)."""
+    return make_decode(DecodeAttnWorkload(f"decode_{BH}x{Lq}x{Lk}_d{d}", 203, BH, Lq, Lk, d), seed)
 
 
 def make_sm_case(BH: int, L: int, d: int, causal: bool, seed: int = 0, s_std: float = 2.0,

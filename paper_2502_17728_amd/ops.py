@@ -24,7 +24,8 @@ STATUS = {0: "DN_OK", 1: "DN_ERR_INVALID_ARG", 2: "DN_ERR_UNSUPPORTED", 3: "DN_E
 SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linear_prepare",
            "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered", "ln_linear_serial",
            "swiglu_packed_bytes", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
-           "attention_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm")
+           "attention_deferred", "attention_decode_workspace_bytes", "attention_decode_deferred", "layernorm",
+           "rmsnorm", "silu_mul", "softmax", "gemm")
 
 
 class DNError(RuntimeError):
@@ -61,13 +62,17 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.silu_mul.argtypes = [vp, vp, i64, i32, vp, vp]
     lib.softmax_pv_deferred.argtypes = [vp, vp, i64, i64, i64, i64, i32, i32, vp, vp]
     lib.attention_deferred.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, f32, i32, vp, vp]
+    lib.attention_decode_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.attention_decode_workspace_bytes.restype = ctypes.c_size_t
+    lib.attention_decode_deferred.argtypes = [vp, vp, vp, i64, i64, i64, i64, f32, i32, vp, ctypes.c_size_t, vp, vp]
     lib.layernorm.argtypes = [vp, vp, vp, i64, i64, f32, i32, vp, vp]
     lib.rmsnorm.argtypes = [vp, vp, i64, i64, f32, i32, vp, vp]
     lib.softmax.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp]
     lib.gemm.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, i32, i32, vp, vp]
     for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered",
               "ln_linear_serial", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
-              "attention_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax", "gemm"):
+              "attention_deferred", "attention_decode_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax",
+              "gemm"):
         getattr(lib, f).restype = i32
     return lib
 
@@ -240,6 +245,31 @@ def attention_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, causal
     _check("attention_deferred", _lib.attention_deferred(
         _dev(Q, "Q"), _dev(K, "K"), _dev(V, "V"), BH, Lq, Lk, d, int(causal), float(scale), _dt(Q),
         _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def attention_decode_workspace_bytes(BH: int, Lq: int, Lk: int, d: int) -> int:
+    return int(_lib.attention_decode_workspace_bytes(BH, Lq, Lk, d))
+
+
+def attention_decode_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, scale: Optional[float] = None,
+                              workspace: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                              stream=None) -> torch.Tensor:
+    """Decode attention (Lq <= 16, every key visible) split over key ranges, then merged."""
+    BH, Lq, d = Q.shape
+    Lk = K.shape[1]
+    if tuple(K.shape) != (BH, Lk, d) or tuple(V.shape) != (BH, Lk, d):
+        raise ValueError("K and V must be [BH, Lk, d] like Q")
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    nbytes = attention_decode_workspace_bytes(BH, Lq, Lk, d)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=Q.device)
+    if out is None:
+        out = torch.empty_like(Q)
+    _check("attention_decode_deferred", _lib.attention_decode_deferred(
+        _dev(Q, "Q"), _dev(K, "K"), _dev(V, "V"), BH, Lq, Lk, d, float(scale), _dt(Q), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _dev(out, "out"), _stream(stream)))
     return out
 
 

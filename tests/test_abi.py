@@ -152,6 +152,20 @@ def test_attention_deferred_validation():
     assert f(P, P2, P3, 1, 64, 64, 64, 0, 0.125, 1, P + 64, None) == INVALID              # out overlaps Q
 
 
+def test_attention_decode_validation():
+    f, wb = ops._lib.attention_decode_deferred, ops._lib.attention_decode_workspace_bytes
+    assert wb(32, 1, 8192, 128) > 0
+    assert wb(32, 17, 8192, 128) == 0 and wb(32, 1, 8192, 96) == 0 and wb(0, 1, 8, 64) == 0
+    n = wb(2, 4, 1000, 64)
+    W = P3 + (1 << 30)
+    assert f(P, P2, P3, 2, 4, 1000, 64, 0.125, 1, None, n, P + (1 << 32), None) == INVALID   # workspace required
+    assert f(P, P2, P3, 2, 4, 1000, 64, 0.125, 1, W, n - 1, P + (1 << 32), None) == INVALID  # too small
+    assert f(P, P2, P3, 2, 17, 1000, 64, 0.125, 1, W, 1 << 20, P + (1 << 32), None) == UNSUPPORTED
+    assert f(P, P2, P3, 2, 4, 1000, 64, -1.0, 1, W, n, P + (1 << 32), None) == INVALID
+    assert f(P, P2, P3, 2, 4, 1000, 64, 0.125, 1, W + 4, n, P + (1 << 32), None) == MISALIGNED
+    assert f(P, P2, P3, 2, 4, 1000, 64, 0.125, 1, P2, n, P + (1 << 32), None) == INVALID     # workspace over K
+
+
 def test_unfused_validation():
     ln, sm, gm = ops._lib.layernorm, ops._lib.softmax, ops._lib.gemm
     assert ln(None, P2, None, 4, 64, 1e-5, 1, P3, None) == INVALID

@@ -440,6 +440,70 @@ def test_attention_causal_workload_sampled(ops):
     _attn_check(ops, case, rows=rows)
 
 
+# ---------------------------------------------------------------------------- decode attention (split keys + merge)
+def _decode_check(ops, case, heads=None):
+    Q, K, V = case["Q"], case["K"], case["V"]
+    BH, Lq, d = Q.shape
+    out = ops.attention_decode_deferred(cuda(Q), cuda(K), cuda(V), scale=case["scale"])
+    torch.cuda.synchronize()
+    heads = np.arange(BH) if heads is None else np.asarray(heads)
+    rows = (heads[:, None] * Lq + np.arange(Lq)[None, :]).reshape(-1)
+    hsel = torch.as_tensor(heads)
+    # the oracle sees only the sampled heads' caches (row r belongs to sampled head r // Lq)
+    ref = oracle.attention(Q[hsel].reshape(-1, d), K[hsel], V[hsel], case["scale"],
+                           head=np.repeat(np.arange(len(heads)), Lq))
+    got = out.cpu().reshape(BH * Lq, d)[torch.as_tensor(rows)]
+    err = rowwise_rel_err(got, ref)
+    print(f"attention_decode_deferred Q{tuple(Q.shape)} K{tuple(K.shape)}: err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
+    return out
+
+
+@pytest.mark.parametrize("BH,Lq,Lk,d", [(1, 1, 1, 64), (3, 1, 100, 128), (2, 4, 8200, 128), (5, 16, 8192, 64),
+                                        (1, 7, 70001, 128), (2048, 1, 130, 64), (8, 3, 64, 128)])
+def test_attention_decode_shapes(ops, BH, Lq, Lk, d):
+    # single key; ragged caches (not whole 64-key steps); splits of one step (many heads) and of
+    # many steps (one head, long cache); partial query tiles
+    _decode_check(ops, I.make_decode_case(BH, Lq, Lk, d, seed=Lk + Lq))
+
+
+def test_attention_decode_matches_single_pass(ops):
+    # the split + merge against the single-pass kernel on the same inputs: both bf16 outputs
+    # of the same exact quantity, so they agree to twice the bf16 output rounding
+    case = I.make_decode_case(4, 16, 3000, 128, seed=12)
+    q, k, v = cuda(case["Q"]), cuda(case["K"]), cuda(case["V"])
+    a = ops.attention_decode_deferred(q, k, v)
+    b = ops.attention_deferred(q, k, v, causal=False)
+    assert rowwise_rel_err(a.cpu().reshape(-1, 128), oracle.to_f64(b.cpu()).reshape(-1, 128)) <= 2 ** -7
+
+
+def test_attention_decode_workspace_reuse(ops):
+    # one workspace serves a large call and then a smaller one; a caller-provided output is used
+    big = I.make_decode_case(16, 2, 5000, 128, seed=13)
+    ws = torch.empty(ops.attention_decode_workspace_bytes(16, 2, 5000, 128), dtype=torch.uint8, device="cuda")
+    out = torch.empty((16, 2, 128), dtype=torch.bfloat16, device="cuda")
+    ops.attention_decode_deferred(cuda(big["Q"]), cuda(big["K"]), cuda(big["V"]), workspace=ws, out=out)
+    small = I.make_decode_case(3, 1, 700, 128, seed=14)
+    assert ops.attention_decode_workspace_bytes(3, 1, 700, 128) <= ws.numel()
+    got = ops.attention_decode_deferred(cuda(small["Q"]), cuda(small["K"]), cuda(small["V"]), workspace=ws)
+    torch.cuda.synchronize()
+    ref = oracle.attention(small["Q"].reshape(-1, 128), small["K"], small["V"], small["scale"],
+                           head=np.arange(3))
+    assert rowwise_rel_err(got.cpu().reshape(-1, 128), ref) <= TOL[torch.bfloat16]
+    refb = oracle.attention(big["Q"].reshape(-1, 128), big["K"], big["V"], big["scale"],
+                            head=np.repeat(np.arange(16), 2))
+    assert rowwise_rel_err(out.cpu().reshape(-1, 128), refb) <= TOL[torch.bfloat16]
+
+
+def test_attention_decode_workload_sampled(ops):
+    # the benchmarked decode workload at full size, in its own launch configuration; the
+    # oracle computes a sample of heads (the GPU runs every head)
+    w = I.ATTN_DECODE
+    heads = [0, 1, 77, 128, 200, w.BH - 1]
+    case = I.make_decode(w)
+    _decode_check(ops, case, heads=heads)
+
+
 # ---------------------------------------------------------------------------- unfused comparators
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_layernorm_unfused(ops, dtype):
@@ -468,10 +532,11 @@ def test_softmax_unfused(ops, causal):
     assert rowwise_rel_err(P.cpu().reshape(-1, L), ref) <= 1e-2
 
 
-@pytest.mark.parametrize("b_layout", [0, 1])
-def test_gemm_unfused(ops, b_layout):
+@pytest.mark.parametrize("b_layout,M", [(0, 136), (1, 136), (1, 1)])
+def test_gemm_unfused(ops, b_layout, M):
+    # M = 1: one row per batch entry (the score product of a decode step)
     g = torch.Generator().manual_seed(1)
-    A = torch.randn(3, 136, 200, generator=g).to(torch.bfloat16)
+    A = torch.randn(3, M, 200, generator=g).to(torch.bfloat16)
     B = torch.randn(3, 200, 72, generator=g).to(torch.bfloat16)
     bias = torch.randn(72, generator=g).to(torch.bfloat16)
     Bd = B if b_layout == 0 else B.transpose(1, 2).contiguous()
