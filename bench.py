@@ -65,9 +65,14 @@ TRAFFIC = {
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
         "fetch_kib": 229889, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
-        "sha256": ("ab121a92cc11ed23f6564163328c1b99b04b11fe28476344ce74583bc7d16eb9",
+        "sha256": ("1d236d3287681b9f665236910169ce2d264f983bf71b6c6a4e562073e8cd2777",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 149377, "fetch_scale": 1.99993, "write_kib": 75087, "write_scale": 1.0},
+        "fetch_kib": 134810, "fetch_scale": 1.99993, "write_kib": 65536, "write_scale": 1.0},
+    # the split kernel and the merge kernel together (530515 + 145 KiB read, 266 + 64 KiB written)
+    ("attention_decode_deferred", "decode_attention_bf16_256x1x8192_d128"): {
+        "sha256": ("1d236d3287681b9f665236910169ce2d264f983bf71b6c6a4e562073e8cd2777",
+                   "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
+        "fetch_kib": 530660, "fetch_scale": 1.99993, "write_kib": 330, "write_scale": 1.0},
 }
 
 

@@ -253,7 +253,7 @@ DN_API dn_status attention_decode_deferred(const void* Q, const void* K, const v
         overlaps(workspace, need, Q, qb) || overlaps(workspace, need, K, kb) || overlaps(workspace, need, V, kb) ||
         overlaps(workspace, need, out, qb))
         return DN_ERR_INVALID_ARG;
-    if (BH * 1024 > kMaxGridX) return DN_ERR_UNSUPPORTED;
+    if (BH * 16 > kMaxGridX) return DN_ERR_UNSUPPORTED;  // grids: BH + 1280 splits, BH * Lq / 4 merges
     return from_hip(dn::launch_attention_decode(Q, K, V, BH, Lq, Lk, d, scale, workspace, out, stream));
 }
 

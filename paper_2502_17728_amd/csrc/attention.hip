@@ -93,7 +93,7 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
     constexpr int RPI = kChunkBytes / ROW;  // rows per copy instruction
     constexpr int DB = D / 16, DC = D / 32;
     static_assert(TILE % (kChunkBytes * NW) == 0, "tiles split evenly over the waves");
-    static_assert(NS >= 2 && NS <= 4, "ring depth");
+    static_assert(NS >= 2 && (NS - 2) * KV_INS < 64, "ring depth: the copies in flight fit vmcnt");
 
     __shared__ __attribute__((aligned(1024))) char smem[NS * SLOT];
 
@@ -375,12 +375,22 @@ __global__ __launch_bounds__(256) void attention_merge_kernel(const float* __res
     for (int j = 0; j < PER; ++j) out[row * D + lane + 64 * j] = (__bf16)(acc[j] * inv);
 }
 
-// Decode split: about 1024 workgroups over the heads, each a whole number of 64-key steps.
-void attention_decode_split(int64_t BH, int64_t Lk, int* nsplit, int64_t* kchunk) {
-    const int64_t steps = (Lk + 63) / 64;
-    const int64_t want = std::max<int64_t>(1, std::min<int64_t>(steps, (1024 + BH - 1) / BH));
+// Decode kernel: one wave of 16 query slots per workgroup (Lq <= 16), 32-key steps, a
+// ring of 4 slots (three steps in flight while one is computed): 512 d bytes of LDS.
+constexpr int kDecNS = 4, kDecBKV = 32;
+constexpr int64_t kCUs = 256, kLdsPerCU = 160 * 1024;
+inline int64_t decode_lds_bytes(int64_t d) { return (int64_t)kDecNS * 2 * kDecBKV * d * 2; }
+
+// Decode split: as many workgroups as fit on the chip at once (LDS-bound: 2 per CU at
+// d = 128, 5 at d = 64), spread over the heads; each split a whole number of steps.
+// Measured on 256 heads x 8192 keys, d = 128: one resident round beats 2 and 4 rounds
+// (their tails) and the 64-key, 2-slot ring (fewer bytes in flight per CU).
+void attention_decode_split(int64_t BH, int64_t Lk, int64_t d, int* nsplit, int64_t* kchunk) {
+    const int64_t wgs = kCUs * (kLdsPerCU / decode_lds_bytes(d));
+    const int64_t steps = (Lk + kDecBKV - 1) / kDecBKV;
+    const int64_t want = std::max<int64_t>(1, std::min<int64_t>(steps, (wgs + BH - 1) / BH));
     const int64_t per = (steps + want - 1) / want;  // steps per split
-    *kchunk = per * 64;
+    *kchunk = per * kDecBKV;
     *nsplit = (int)((Lk + *kchunk - 1) / *kchunk);
 }
 
@@ -389,9 +399,8 @@ static hipError_t run_attention_decode(const void* Q, const void* K, const void*
                                        int64_t Lk, float scale, float* part, void* out, hipStream_t s) {
     int nsplit;
     int64_t kchunk;
-    attention_decode_split(BH, Lk, &nsplit, &kchunk);
-    // one wave of 16 queries per workgroup (Lq <= 16), 64-key steps, two ring slots
-    attention_kernel<D, 1, 1, 2, 64><<<dim3((unsigned)(BH * nsplit)), 64, 0, s>>>(
+    attention_decode_split(BH, Lk, D, &nsplit, &kchunk);
+    attention_kernel<D, 1, 1, kDecNS, kDecBKV><<<dim3((unsigned)(BH * nsplit)), 64, 0, s>>>(
         (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, 0, scale * fa::kLog2e, 1, nsplit, kchunk,
         part, nullptr);
     const int64_t rows = BH * Lq;
@@ -402,7 +411,7 @@ static hipError_t run_attention_decode(const void* Q, const void* K, const void*
 size_t attention_decode_workspace_bytes(int64_t BH, int64_t Lq, int64_t Lk, int64_t d) {
     int nsplit;
     int64_t kchunk;
-    attention_decode_split(BH, Lk, &nsplit, &kchunk);
+    attention_decode_split(BH, Lk, d, &nsplit, &kchunk);
     return (size_t)BH * (size_t)Lq * (size_t)nsplit * (size_t)(d + 4) * sizeof(float);
 }
 
