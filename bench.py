@@ -151,6 +151,14 @@ class LNSite:
         # ablation: the row statistics in a pre-pass kernel, then the same deferred epilogue
         self.ops.ln_linear_serial(self.x, self.prep, self.w.eps, stats=self.stats, out=self.out)
 
+    def on_load_supported(self):
+        return (not self.rms and self.w.dtype == "bf16" and self.w.K % 64 == 0
+                and ((self.w.M + 255) // 256) * ((self.w.N + 255) // 256) >= 256)
+
+    def norm_on_load(self):
+        # ablation without deferral: pre-pass statistics, x normalized on load into the product
+        self.ops.ln_linear_norm_on_load(self.x, self.prep, self.w.eps, stats=self.stats, out=self.out)
+
     def fused(self):
         f = self.ops.rms_linear_deferred if self.rms else self.ops.ln_linear_deferred
         f(self.x, self.prep, self.w.eps, out=self.out)
@@ -501,8 +509,9 @@ def main():
             # (inside the step the kernel follows the other site, whose traffic evicts the caches);
             # the two alternate over 5 rounds and each reports its median
             n = max(3, args.steps // 2)
-            fis, us, uds, sers, sps = [], [], [], [], []
+            fis, us, uds, sers, sps, nols = [], [], [], [], [], []
             serial = isinstance(s, LNSite) and not s.rms and s.w.K <= 16384
+            on_load = serial and s.on_load_supported()
             for _ in range(5):
                 fis.append(time_steps([s.fused], n, 2)[0][0])
                 us.append(time_steps([s.unfused], n, 2)[0][0])
@@ -512,6 +521,8 @@ def main():
                     sers.append(time_steps([s.serial], n, 2)[0][0])
                 if isinstance(s, DecodeAttnSite):
                     sps.append(time_steps([s.single_pass], n, 2)[0][0])
+                if on_load:
+                    nols.append(time_steps([s.norm_on_load], n, 2)[0][0])
             fi, u = float(np.median(fis)), float(np.median(us))
             k["isolated_ms"] = round(fi, 4)
             k["unfused_ms"] = round(u, 4)
@@ -526,6 +537,10 @@ def main():
                 se = float(np.median(sers))
                 k["serial_stats_ms"] = round(se, 4)
                 k["speedup_vs_serial_stats"] = round(se / fi, 3)
+            if nols:  # ablation: fused without deferral (normalize on load)
+                nl = float(np.median(nols))
+                k["norm_on_load_ms"] = round(nl, 4)
+                k["speedup_vs_norm_on_load"] = round(nl / fi, 3)
             if sps:  # ablation: no key split (one workgroup per head)
                 sp = float(np.median(sps))
                 k["single_pass_ms"] = round(sp, 4)

@@ -151,6 +151,21 @@ DN_API dn_status ln_linear_prepare_centered(const void* W, const void* gamma, co
 DN_API dn_status ln_linear_serial(const void* x, const ln_linear_weights* w, int64_t M, float eps,
                            float* stats, void* out, hipStream_t stream);
 
+/*
+ * Fused without deferral (ablation of Eq. (5)): the same statistics pre-pass
+ * as ln_linear_serial into stats[2 M], then one kernel that normalizes each x
+ * fragment as it is loaded, xh = (x - mean) / sqrt(var + eps) rounded to the
+ * GEMM dtype, and runs xh . W' + b (W' = Diag(gamma) W and b = beta W + bias
+ * from ln_linear_prepare, so this is y F of Eq. (4) with y formed in
+ * registers).  The normalization sits on the product's input path instead of
+ * after it, which isolates what deferral buys over plain fusion.  bf16 only,
+ * and only for the large-tile shapes (K % 64 == 0, at least 256 tiles of
+ * 256 x 256, N < 2^22); other shapes give DN_ERR_UNSUPPORTED.  Otherwise as
+ * ln_linear_serial.
+ */
+DN_API dn_status ln_linear_norm_on_load(const void* x, const ln_linear_weights* w, int64_t M, float eps,
+                                 float* stats, void* out, hipStream_t stream);
+
 /* ======================================================================= */
 /* RMSNorm -> gated MLP input (SwiGLU), deferred                            */
 /* ======================================================================= */

@@ -96,7 +96,7 @@ DN_API dn_status ln_linear_prepare_centered(const void* W, const void* gamma, co
 }
 
 static dn_status deferred_linear(const void* x, const ln_linear_weights* w, int64_t M, float eps, int rms,
-                                 float* stats, void* out, hipStream_t stream) {
+                                 float* stats, void* out, hipStream_t stream, bool on_load = false) {
     if (!x || !w || !out || !w->packed || M < 1) return DN_ERR_INVALID_ARG;
     if (w->layout_version != DN_LN_LAYOUT_VERSION || w->K < 1 || w->N < 1 || !valid_dtype(w->dtype))
         return DN_ERR_INVALID_ARG;
@@ -111,6 +111,7 @@ static dn_status deferred_linear(const void* x, const ln_linear_weights* w, int6
     const size_t pb = ln_linear_packed_bytes(K, N, dt);
     if (overlaps(out, ob, x, xb) || overlaps(out, ob, w->packed, pb)) return DN_ERR_INVALID_ARG;
     if (((M + 15) / 16) * ((N + 15) / 16) > kMaxGridX) return DN_ERR_UNSUPPORTED;
+    if (on_load && !dn::ln_on_load_supported(M, K, N, dt)) return DN_ERR_UNSUPPORTED;
     if (stats) {
         if (!aligned(stats, 16)) return DN_ERR_MISALIGNED;
         const size_t sb = (size_t)M * 8;
@@ -121,6 +122,7 @@ static dn_status deferred_linear(const void* x, const ln_linear_weights* w, int6
         const dn_status st = from_hip(dn::launch_row_stats(x, M, K, eps, dt, stats, stream));
         if (st != DN_OK) return st;
     }
+    if (on_load) return from_hip(dn::launch_ln_linear_on_load(x, w->packed, M, K, N, stats, out, stream));
     return from_hip(dn::launch_ln_linear_deferred(x, w->packed, M, K, N, dt, eps, rms, stats, out, stream));
 }
 
@@ -133,6 +135,12 @@ DN_API dn_status ln_linear_serial(const void* x, const ln_linear_weights* w, int
                                   void* out, hipStream_t stream) {
     if (!stats) return DN_ERR_INVALID_ARG;
     return deferred_linear(x, w, M, eps, 0, stats, out, stream);
+}
+
+DN_API dn_status ln_linear_norm_on_load(const void* x, const ln_linear_weights* w, int64_t M, float eps,
+                                        float* stats, void* out, hipStream_t stream) {
+    if (!stats) return DN_ERR_INVALID_ARG;
+    return deferred_linear(x, w, M, eps, 0, stats, out, stream, true);
 }
 
 DN_API dn_status rms_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M, float eps, void* out,

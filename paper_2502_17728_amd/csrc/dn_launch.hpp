@@ -42,6 +42,12 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
                                      int64_t N, int dtype, float eps, int rms, const float* row_stats,
                                      void* out, hipStream_t s);
 
+// Normalize-on-load ablation (bf16, large-tile shapes only): xh = (x - mean) rstd on the
+// product's input path from pre-pass row_stats, out = xh . W' + b.
+bool ln_on_load_supported(int64_t M, int64_t K, int64_t N, int dtype);
+hipError_t launch_ln_linear_on_load(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
+                                    const float* row_stats, void* out, hipStream_t s);
+
 // stats[2 r], stats[2 r + 1] = mean, 1/sqrt(var + eps) of row r of x (two-pass, Eq. (1)-(2)).
 hipError_t launch_row_stats(const void* x, int64_t M, int64_t K, float eps, int dtype, float* stats,
                             hipStream_t s);

@@ -33,7 +33,10 @@ namespace dn {
 // kLnDeferred: out = rstd (acc - mean c) + b.  kSwiGlu: the same for the gate
 // and up columns, which the packed weights interleave in 16-column blocks (gate
 // block j, then up block j), combined as h = SiLU(gate) * up.  kGemm: acc + bias.
-enum class Epi { kLnDeferred, kGemm, kSwiGlu };
+// kLnOnLoad (ablation, no deferral): statistics from a pre-pass, each x fragment
+// normalized as it is loaded, xh = (x - mean) rstd rounded to bf16, then out =
+// xh . W' + b -- the plain fused LayerNorm -> Linear the deferred form replaces.
+enum class Epi { kLnDeferred, kGemm, kSwiGlu, kLnOnLoad };
 enum class BMode { kKN, kNK, kPacked };
 
 struct MainArgs {
@@ -409,6 +412,16 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
 // =============================================================================
 constexpr int kSgMfma = 0x008, kSgDsRead = 0x100;
 
+// xh = x r + nb for the 8 bf16 of a fragment chunk, rounded once to bf16.
+__device__ __forceinline__ u32x4 normalize_chunk(const u32x4& a, float r, float nb) {
+    const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        o[j] = pack_bf16(__builtin_fmaf(bf_lo(w[j]), r, nb), __builtin_fmaf(bf_hi(w[j]), r, nb));
+    return u32x4{o[0], o[1], o[2], o[3]};
+}
+
 __device__ __forceinline__ int a_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 template <Epi EPI, int WM, int WN>
@@ -424,6 +437,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
     constexpr int PER = A_INS + B_INS;
     constexpr bool LN = EPI != Epi::kGemm;
     constexpr bool SW = EPI == Epi::kSwiGlu;
+    constexpr bool NOL = EPI == Epi::kLnOnLoad;
     static_assert(!SW || FN % 2 == 0, "gate/up fragment pairs");
     constexpr int FMW = FM / WN;                  // row blocks whose moments each wave column owns
     constexpr int NMF = FM * FN, NRD = FM + FN;
@@ -492,6 +506,19 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
 #pragma unroll
     for (int i = 0; i < FMW; ++i) s1[i] = s2[i] = 0.f;
 
+    // Normalize-on-load: the statistics of the lane's row in each row fragment
+    // (A operand: lane l holds row l & 15 of the fragment), as xh = x r + (-mean r).
+    float nl_r[NOL ? FM : 1], nl_b[NOL ? FM : 1];
+    if constexpr (NOL) {
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) {
+            const int64_t row = min(m0 + wm * WTM + fm * 16 + (lane & 15), M - 1);
+            const float mean = p.row_stats[2 * row], rstd = p.row_stats[2 * row + 1];
+            nl_r[fm] = rstd;
+            nl_b[fm] = -mean * rstd;
+        }
+    }
+
     for (int tt = 0; tt < group; ++tt) {
         const int pn = gn * group + tt;
         if (pn >= tiles_n) break;
@@ -531,6 +558,10 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
             if constexpr (LN && OWN >= 0) {
 #pragma unroll
                 for (int i = 0; i < FMW; ++i) chunk_moments<__bf16>(fa[OWN * FMW + i], s1[i], s2[i]);
+            }
+            if constexpr (NOL) {
+#pragma unroll
+                for (int fm = 0; fm < FM; ++fm) fa[fm] = normalize_chunk(fa[fm], nl_r[fm], nl_b[fm]);
             }
 #pragma unroll
             for (int fm = 0; fm < FM; ++fm)
@@ -575,7 +606,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
         }
         wait_lgkm0();
 
-        if (LN && tt == 0 && p.row_stats) {  // serial ablation: the pre-pass statistics
+        if (LN && !NOL && tt == 0 && p.row_stats) {  // serial ablation: the pre-pass statistics
             for (int r = tid; r < BM; r += NW * kWave) {
                 const int64_t rr = min(m0 + r, M - 1);
                 row_s1[r] = p.row_stats[2 * rr];
@@ -629,12 +660,14 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
         for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                mu[fm][i] = LN ? row_s1[lr + fm * 16 + i] : 0.f;
-                rs[fm][i] = LN ? row_s2[lr + fm * 16 + i] : 1.f;
+                mu[fm][i] = LN && !NOL ? row_s1[lr + fm * 16 + i] : 0.f;
+                rs[fm][i] = LN && !NOL ? row_s2[lr + fm * 16 + i] : 1.f;
             }
         auto value = [&](int fm, int fn, int i) {
             const float v = acc[fm][fn][i];
-            if constexpr (LN)
+            if constexpr (NOL)
+                return v + bn[fn];
+            else if constexpr (LN)
                 return __builtin_fmaf(rs[fm][i], __builtin_fmaf(-mu[fm][i], cn[fn], v), bn[fn]);
             else
                 return v + bn[fn];
@@ -1052,6 +1085,17 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
     if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
     if (use_big_tiles(M, N, K)) return run_pipe<Epi::kLnDeferred>(a, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
+}
+
+bool ln_on_load_supported(int64_t M, int64_t K, int64_t N, int dtype) {
+    return dtype == 1 && use_big_tiles(M, N, K);
+}
+
+hipError_t launch_ln_linear_on_load(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
+                                    const float* row_stats, void* out, hipStream_t s) {
+    MainArgs a = packed_args(x, packed, M, K, N, 1, out);
+    a.row_stats = row_stats;
+    return run_pipe<Epi::kLnOnLoad>(a, s);
 }
 
 hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N, int dtype,

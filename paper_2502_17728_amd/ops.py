@@ -23,6 +23,7 @@ DN_SWIGLU_LAYOUT_VERSION = 0x102
 STATUS = {0: "DN_OK", 1: "DN_ERR_INVALID_ARG", 2: "DN_ERR_UNSUPPORTED", 3: "DN_ERR_MISALIGNED", 4: "DN_ERR_HIP"}
 SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linear_prepare",
            "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered", "ln_linear_serial",
+           "ln_linear_norm_on_load",
            "swiglu_packed_bytes", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
            "attention_deferred", "attention_decode_workspace_bytes", "attention_decode_deferred", "layernorm",
            "rmsnorm", "silu_mul", "softmax", "gemm")
@@ -54,6 +55,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.ln_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
     lib.ln_linear_prepare_centered.argtypes = lib.ln_linear_prepare.argtypes
     lib.ln_linear_serial.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp, vp]
+    lib.ln_linear_norm_on_load.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp, vp]
     lib.rms_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
     lib.swiglu_packed_bytes.argtypes, lib.swiglu_packed_bytes.restype = [i64, i64, i32], ctypes.c_size_t
     lib.swiglu_prepare.argtypes = [vp, vp, vp, i64, i64, i32, vp, ctypes.c_size_t, ctypes.POINTER(LnLinearWeights),
@@ -70,7 +72,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.softmax.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp]
     lib.gemm.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, i32, i32, vp, vp]
     for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered",
-              "ln_linear_serial", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
+              "ln_linear_serial", "ln_linear_norm_on_load", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
               "attention_deferred", "attention_decode_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax",
               "gemm"):
         getattr(lib, f).restype = i32
@@ -171,6 +173,22 @@ def ln_linear_serial(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5, stat
     if _dt(x) != w.desc.dtype:
         raise TypeError("x dtype differs from the prepared weights")
     _check("ln_linear_serial", _lib.ln_linear_serial(
+        _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(stats, "stats"), _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def ln_linear_norm_on_load(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
+                           stats: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                           stream=None) -> torch.Tensor:
+    """Ablation: statistics pre-pass, then x normalized on load into the product (no deferral)."""
+    M = x.shape[0]
+    if out is None:
+        out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
+    if stats is None:
+        stats = torch.empty(2 * M, dtype=torch.float32, device=x.device)
+    if _dt(x) != w.desc.dtype:
+        raise TypeError("x dtype differs from the prepared weights")
+    _check("ln_linear_norm_on_load", _lib.ln_linear_norm_on_load(
         _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(stats, "stats"), _dev(out, "out"), _stream(stream)))
     return out
 

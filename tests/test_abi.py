@@ -109,6 +109,18 @@ def test_ln_linear_serial_validation():
     assert f(P, ctypes.byref(_w(version=0)), 4, 1e-5, P3 + (1 << 30), P2, None) == INVALID
 
 
+def test_ln_linear_norm_on_load_validation():
+    f = ops._lib.ln_linear_norm_on_load
+    S = P3 + (1 << 34)
+    big = _w(K=4096, N=4096)
+    assert f(P, ctypes.byref(big), 4096, 1e-5, None, P2, None) == INVALID            # stats required
+    assert f(P, ctypes.byref(_w()), 4, 1e-5, S, P2, None) == UNSUPPORTED            # below the large tiles
+    assert f(P, ctypes.byref(_w(K=4096, N=4096, dtype=0)), 4096, 1e-5, S, P2, None) == UNSUPPORTED  # fp32
+    assert f(P, ctypes.byref(_w(K=4104, N=4096)), 4096, 1e-5, S, P2, None) == UNSUPPORTED  # K % 64
+    assert f(P, ctypes.byref(big), 4096, 1e-5, S + 4, P2, None) == MISALIGNED
+    assert f(P, ctypes.byref(big), 4096, -1.0, S, P2, None) == INVALID
+
+
 @pytest.mark.parametrize("entry", ["ln_linear_prepare", "ln_linear_prepare_centered"])
 def test_ln_linear_prepare_validation(entry):
     f = getattr(ops._lib, entry)

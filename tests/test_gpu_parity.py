@@ -197,6 +197,42 @@ def test_ln_linear_serial_stats(ops, M, K, N, dtype):
     np.testing.assert_allclose(st[:, 1], 1 / np.sqrt(xd.var(1) + case["eps"]), rtol=1e-4)
 
 
+@pytest.mark.parametrize("M,K,N,offset", [(4000, 576, 4104, 0.0), (4104, 320, 4096, 0.0), (4096, 256, 4096, 4.0)])
+def test_ln_linear_norm_on_load(ops, M, K, N, offset):
+    # ablation without deferral: pre-pass statistics, x normalized on load into the product;
+    # ragged M and N over the large tiles, and rows with a large mean (normalized before the
+    # product, so no cancellation)
+    case = I.make_ln_case(M, K, N, "bf16", seed=M + K, outliers=2, mean_offset=offset)
+    w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
+    stats = torch.empty(2 * M, dtype=torch.float32, device="cuda")
+    out = ops.ln_linear_norm_on_load(cuda(case["x"]), w, case["eps"], stats=stats)
+    rows = I.sample_rows(M, 32, seed=10)
+    ref = oracle.ln_linear(case["x"][torch.as_tensor(rows)], case["gamma"], case["beta"], case["W"], None,
+                           case["eps"])
+    err = rowwise_rel_err(out.cpu()[torch.as_tensor(rows)], ref)
+    print(f"ln_linear_norm_on_load {M}x{K}x{N} offset {offset}: err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
+
+
+def test_ln_linear_norm_on_load_qkv_workload_sampled(ops):
+    w = I.LN_QKV
+    case = I.make_ln(w)
+    prep = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
+    out = ops.ln_linear_norm_on_load(cuda(case["x"]), prep, case["eps"])
+    rows = I.sample_rows(w.M, 24, seed=13)
+    ref = oracle.ln_linear(case["x"][torch.as_tensor(rows)], case["gamma"], case["beta"], case["W"], None,
+                           case["eps"])
+    assert rowwise_rel_err(out.cpu()[torch.as_tensor(rows)], ref) <= TOL[torch.bfloat16]
+
+
+def test_ln_linear_norm_on_load_rejects_small_shapes(ops):
+    case = I.make_ln_case(64, 256, 256, "bf16", seed=3)
+    w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
+    with pytest.raises(ops.DNError) as e:
+        ops.ln_linear_norm_on_load(cuda(case["x"]), w, case["eps"])
+    assert e.value.status == 2  # DN_ERR_UNSUPPORTED: the ablation runs on the large tiles only
+
+
 # ---------------------------------------------------------------------------- RMSNorm -> Linear
 @pytest.mark.parametrize("M,K,N", [(37, 104, 72), (1, 8, 8), (300, 512, 200)])
 def test_rms_linear_f32_ragged(ops, M, K, N):
