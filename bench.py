@@ -155,6 +155,11 @@ class LNSite:
         return (not self.rms and self.w.dtype == "bf16" and self.w.K % 64 == 0
                 and ((self.w.M + 255) // 256) * ((self.w.N + 255) // 256) >= 256)
 
+    def post(self):
+        # post-LN placement: the deferred product plus the normalized rows (the residual branch)
+        self.ops.linear_deferred_post(self.x, self.prep, self.g, None if self.rms else self.b, self.w.eps,
+                                      rms=self.rms, stats=self.stats, y=self.y, out=self.out)
+
     def norm_on_load(self):
         # ablation without deferral: pre-pass statistics, x normalized on load into the product
         self.ops.ln_linear_norm_on_load(self.x, self.prep, self.w.eps, stats=self.stats, out=self.out)
@@ -509,7 +514,7 @@ def main():
             # (inside the step the kernel follows the other site, whose traffic evicts the caches);
             # the two alternate over 5 rounds and each reports its median
             n = max(3, args.steps // 2)
-            fis, us, uds, sers, sps, nols = [], [], [], [], [], []
+            fis, us, uds, sers, sps, nols, posts = [], [], [], [], [], [], []
             serial = isinstance(s, LNSite) and not s.rms and s.w.K <= 16384
             on_load = serial and s.on_load_supported()
             for _ in range(5):
@@ -523,6 +528,8 @@ def main():
                     sps.append(time_steps([s.single_pass], n, 2)[0][0])
                 if on_load:
                     nols.append(time_steps([s.norm_on_load], n, 2)[0][0])
+                if isinstance(s, LNSite):
+                    posts.append(time_steps([s.post], n, 2)[0][0])
             fi, u = float(np.median(fis)), float(np.median(us))
             k["isolated_ms"] = round(fi, 4)
             k["unfused_ms"] = round(u, 4)
@@ -537,6 +544,10 @@ def main():
                 se = float(np.median(sers))
                 k["serial_stats_ms"] = round(se, 4)
                 k["speedup_vs_serial_stats"] = round(se / fi, 3)
+            if posts:  # post-LN placement: deferred product + normalized rows, against the unfused pair
+                po = float(np.median(posts))
+                k["post_ln_ms"] = round(po, 4)
+                k["post_ln_speedup_vs_unfused"] = round(u / po, 3)
             if nols:  # ablation: fused without deferral (normalize on load)
                 nl = float(np.median(nols))
                 k["norm_on_load_ms"] = round(nl, 4)

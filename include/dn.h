@@ -118,6 +118,28 @@ DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, i
 DN_API dn_status rms_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M,
                               float eps, void* out, hipStream_t stream);
 
+/*
+ * Post-LN placement (Sec. II-A: the residual branch taken right after the
+ * normalization instead of before it).  There the normalized rows y are needed
+ * twice -- as the input of the next linear layer and as the residual -- so the
+ * call returns both: out[M][N] = y . W + bias the deferred way (exactly as
+ * ln_linear_deferred / rms_linear_deferred, the product never waiting for the
+ * statistics), and y[M][K] = (x - mean) rstd gamma + beta (RMS: x rstd gamma)
+ * applied afterwards from the statistics the product's kernel reduced, which
+ * it exports to stats[2 M] (fp32 (mean, rstd) pairs; RMS: mean = 0).  gamma
+ * (and beta, nullable, LayerNorm only) are the [K] vectors that were folded
+ * into w, in w->dtype.  stats and y: caller-owned device memory, 16-byte
+ * aligned, overlapping no other argument.  Status codes as ln_linear_deferred;
+ * DN_ERR_UNSUPPORTED also when y is too large for one launch.
+ */
+DN_API dn_status ln_linear_deferred_post(const void* x, const ln_linear_weights* w, int64_t M, float eps,
+                                  const void* gamma, const void* beta, float* stats, void* y,
+                                  void* out, hipStream_t stream);
+
+DN_API dn_status rms_linear_deferred_post(const void* x, const ln_linear_weights* w, int64_t M, float eps,
+                                   const void* gamma, float* stats, void* y, void* out,
+                                   hipStream_t stream);
+
 /* ----------------------------------------------------------------------- */
 /* Ablations of the LayerNorm -> Linear fusion                              */
 /* ----------------------------------------------------------------------- */

@@ -96,7 +96,8 @@ DN_API dn_status ln_linear_prepare_centered(const void* W, const void* gamma, co
 }
 
 static dn_status deferred_linear(const void* x, const ln_linear_weights* w, int64_t M, float eps, int rms,
-                                 float* stats, void* out, hipStream_t stream, bool on_load = false) {
+                                 float* stats, void* out, hipStream_t stream, bool on_load = false,
+                                 float* stats_out = nullptr) {
     if (!x || !w || !out || !w->packed || M < 1) return DN_ERR_INVALID_ARG;
     if (w->layout_version != DN_LN_LAYOUT_VERSION || w->K < 1 || w->N < 1 || !valid_dtype(w->dtype))
         return DN_ERR_INVALID_ARG;
@@ -123,7 +124,8 @@ static dn_status deferred_linear(const void* x, const ln_linear_weights* w, int6
         if (st != DN_OK) return st;
     }
     if (on_load) return from_hip(dn::launch_ln_linear_on_load(x, w->packed, M, K, N, stats, out, stream));
-    return from_hip(dn::launch_ln_linear_deferred(x, w->packed, M, K, N, dt, eps, rms, stats, out, stream));
+    return from_hip(dn::launch_ln_linear_deferred(x, w->packed, M, K, N, dt, eps, rms, stats, out, stream,
+                                                  stats_out));
 }
 
 DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M, float eps, void* out,
@@ -141,6 +143,46 @@ DN_API dn_status ln_linear_norm_on_load(const void* x, const ln_linear_weights* 
                                         float* stats, void* out, hipStream_t stream) {
     if (!stats) return DN_ERR_INVALID_ARG;
     return deferred_linear(x, w, M, eps, 0, stats, out, stream, true);
+}
+
+// Post-LN placement: the deferred product plus the normalized rows themselves
+// (the residual branch), from the statistics the product's kernel reduced.
+static dn_status post_linear(const void* x, const ln_linear_weights* w, int64_t M, float eps, int rms,
+                             const void* gamma, const void* beta, float* stats, void* y, void* out,
+                             hipStream_t stream) {
+    if (!x || !w || !gamma || !stats || !y || !out || M < 1) return DN_ERR_INVALID_ARG;
+    if (w->layout_version != DN_LN_LAYOUT_VERSION || w->K < 1 || w->N < 1 || !valid_dtype(w->dtype))
+        return DN_ERR_INVALID_ARG;
+    const int64_t K = w->K;
+    const size_t es = esize(w->dtype);
+    size_t xb, sb, ob;
+    if (!bytes_of(M, K, (int64_t)es, &xb) || !bytes_of(M, 2, 4, &sb) || !bytes_of(M, w->N, (int64_t)es, &ob))
+        return DN_ERR_INVALID_ARG;
+    if (K % 8) return DN_ERR_UNSUPPORTED;
+    if (!aligned(gamma, 16) || !aligned(beta, 16) || !aligned(stats, 16) || !aligned(y, 16))
+        return DN_ERR_MISALIGNED;
+    const size_t pb = ln_linear_packed_bytes(K, w->N, w->dtype);
+    if (overlaps(y, xb, x, xb) || overlaps(y, xb, out, ob) || overlaps(y, xb, stats, sb) ||
+        overlaps(y, xb, w->packed, pb) || overlaps(y, xb, gamma, K * es) || overlaps(y, xb, beta, K * es) ||
+        overlaps(stats, sb, x, xb) || overlaps(stats, sb, out, ob) || overlaps(stats, sb, w->packed, pb) ||
+        overlaps(stats, sb, gamma, K * es) || overlaps(stats, sb, beta, K * es))
+        return DN_ERR_INVALID_ARG;
+    if ((M * K / (w->dtype == DN_F32 ? 4 : 8) + 255) / 256 > kMaxGridX) return DN_ERR_UNSUPPORTED;
+    // the product with its concurrent statistics (validated as ln_linear_deferred), exporting them
+    const dn_status st = deferred_linear(x, w, M, eps, rms, nullptr, out, stream, false, stats);
+    if (st != DN_OK) return st;
+    return from_hip(dn::launch_apply_norm(x, stats, gamma, rms ? nullptr : beta, M, K, w->dtype, y, stream));
+}
+
+DN_API dn_status ln_linear_deferred_post(const void* x, const ln_linear_weights* w, int64_t M, float eps,
+                                         const void* gamma, const void* beta, float* stats, void* y, void* out,
+                                         hipStream_t stream) {
+    return post_linear(x, w, M, eps, 0, gamma, beta, stats, y, out, stream);
+}
+
+DN_API dn_status rms_linear_deferred_post(const void* x, const ln_linear_weights* w, int64_t M, float eps,
+                                          const void* gamma, float* stats, void* y, void* out, hipStream_t stream) {
+    return post_linear(x, w, M, eps, 1, gamma, nullptr, stats, y, out, stream);
 }
 
 DN_API dn_status rms_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M, float eps, void* out,

@@ -1,7 +1,10 @@
 // baselines.hip -- the unfused comparators of Fig. 1(a): LayerNorm (Eq. (1)-(2))
 // and Softmax (Eq. (7) with the max subtraction), each materializing its full
 // output before the separate GEMM.  One wave per row; the row stays in
-// registers, so each element is read once and written once.
+// registers, so each element is read once and written once.  Also the
+// element-wise pieces around the deferred path: the statistics pre-pass of the
+// serial ablation, SiLU * up, and the normalized output of the post-LN
+// placement (applied from statistics the deferred kernel has already reduced).
 #include "dn_device.hpp"
 #include "dn_launch.hpp"
 
@@ -288,6 +291,44 @@ hipError_t launch_silu_mul(const void* g, const void* u, int64_t count, int dtyp
         silu_mul_kernel<float><<<grid, 256, 0, s>>>((const float*)g, (const float*)u, count, (float*)h);
     else
         silu_mul_kernel<__bf16><<<grid, 256, 0, s>>>((const __bf16*)g, (const __bf16*)u, count, (__bf16*)h);
+    return hipGetLastError();
+}
+
+// y = (x - mean) rstd gamma + beta (beta nullable) from per-row (mean, rstd):
+// Eq. (2) with the statistics already reduced, one 16-byte piece per lane.
+template <class T>
+__global__ __launch_bounds__(256) void apply_norm_kernel(const T* __restrict__ x, const float* __restrict__ stats,
+                                                         const T* __restrict__ gamma, const T* __restrict__ beta,
+                                                         int64_t M, int64_t K, T* __restrict__ y) {
+    constexpr int EPL = elem<T>::per16;
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * EPL;
+    if (i >= M * K) return;
+    const int64_t r = i / K, k = i - r * K;  // K % EPL == 0: a piece never straddles rows
+    const float mean = stats[2 * r], rstd = stats[2 * r + 1];
+    float v[EPL], g[EPL], b[EPL], o[EPL];
+    unpack16<T>(ld16(x + i), v);
+    unpack16<T>(ld16(gamma + k), g);
+    if (beta) {
+        unpack16<T>(ld16(beta + k), b);
+    } else {
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) b[e] = 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) o[e] = __builtin_fmaf((v[e] - mean) * rstd, g[e], b[e]);
+    *reinterpret_cast<u32x4*>(y + i) = pack16<T>(o);
+}
+
+hipError_t launch_apply_norm(const void* x, const float* stats, const void* gamma, const void* beta, int64_t M,
+                             int64_t K, int dtype, void* y, hipStream_t s) {
+    const int64_t epl = dtype == 0 ? 4 : 8;
+    const dim3 grid((unsigned)((M * K / epl + 255) / 256));
+    if (dtype == 0)
+        apply_norm_kernel<float><<<grid, 256, 0, s>>>((const float*)x, stats, (const float*)gamma,
+                                                      (const float*)beta, M, K, (float*)y);
+    else
+        apply_norm_kernel<__bf16><<<grid, 256, 0, s>>>((const __bf16*)x, stats, (const __bf16*)gamma,
+                                                       (const __bf16*)beta, M, K, (__bf16*)y);
     return hipGetLastError();
 }
 

@@ -38,9 +38,14 @@ hipError_t launch_ln_prepare(const void* W, const void* gamma, const void* beta,
 
 // rms = 1: RMSNorm statistics (Eq. (6)), the mean taken as zero.  row_stats (nullable):
 // (mean, rstd) per row from a pre-pass, used instead of the concurrent moments.
+// stats_out (nullable): the concurrently reduced (mean, rstd) of every row, exported.
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K,
                                      int64_t N, int dtype, float eps, int rms, const float* row_stats,
-                                     void* out, hipStream_t s);
+                                     void* out, hipStream_t s, float* stats_out = nullptr);
+
+// y = (x - mean) rstd gamma + beta from per-row (mean, rstd); beta nullable.
+hipError_t launch_apply_norm(const void* x, const float* stats, const void* gamma, const void* beta, int64_t M,
+                             int64_t K, int dtype, void* y, hipStream_t s);
 
 // Normalize-on-load ablation (bf16, large-tile shapes only): xh = (x - mean) rstd on the
 // product's input path from pre-pass row_stats, out = xh . W' + b.

@@ -53,6 +53,7 @@ struct MainArgs {
     int rms;              // LN: RMSNorm statistics (Eq. (6)): mean taken as 0
     int64_t n_out;        // kSwiGlu: output features (row stride of C); N counts packed columns
     const float* row_stats;  // LN, serial ablation: (mean, rstd) per row from a pre-pass, or null
+    float* stats_out;        // LN: (mean, rstd) per row as reduced by the kernel, written once per row, or null
     const void* bias;     // GEMM: bias[N] in the element type, or null
     int a_causal;         // GEMM: A lower-triangular, skip k > row
 };
@@ -334,6 +335,10 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
             const float var = __builtin_fmaxf(b / (float)K - mean * mean, 0.f);
             row_mean[r] = mean;
             row_rstd[r] = 1.0f / __builtin_sqrtf(var + p.eps);
+            if (p.stats_out && pn == 0 && m0 + r < M) {  // one tile per row block exports them
+                p.stats_out[2 * (m0 + r)] = mean;
+                p.stats_out[2 * (m0 + r) + 1] = row_rstd[r];
+            }
         }
         __syncthreads();
     }
@@ -631,6 +636,10 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
                 const float var = __builtin_fmaxf(row_s2[r] / (float)K - mean * mean, 0.f);
                 row_s1[r] = mean;
                 row_s2[r] = 1.0f / __builtin_sqrtf(var + p.eps);
+                if (p.stats_out && gn == 0 && m0 + r < M) {  // the row block's first group exports them
+                    p.stats_out[2 * (m0 + r)] = mean;
+                    p.stats_out[2 * (m0 + r) + 1] = row_s2[r];
+                }
             }
             __syncthreads();
         }
@@ -743,15 +752,20 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
 // =============================================================================
 // SW: the packed columns interleave gate and up blocks (NC even, blocks 2j and
 // 2j+1 of the group form output block j), out[M][n_out] = SiLU(gate) * up.
-template <int KS, int NC, int U, bool SW = false>
+// PLAIN: the plain product out = x . W' + bias (bias: [N] bf16, nullable), no
+// moments -- the decode-shaped GEMM of the unfused comparators.
+template <int KS, int NC, int U, bool SW = false, bool PLAIN = false>
 __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16* __restrict__ x,
                                                              const char* __restrict__ Wp, int64_t kchunks,
                                                              int64_t nblocks, const float* __restrict__ c_col,
                                                              const float* __restrict__ b_col, int M, int64_t K,
                                                              int64_t N, float eps, int rms, int64_t n_out,
                                                              const float* __restrict__ row_stats,
-                                                             __bf16* __restrict__ out) {
+                                                             float* __restrict__ stats_out,
+                                                             __bf16* __restrict__ out,
+                                                             const __bf16* __restrict__ bias) {
     static_assert(!SW || NC % 2 == 0, "gate/up block pairs");
+    static_assert(!(SW && PLAIN), "the plain product has no gate");
     __shared__ f32x4 part[2 + NC][KS][kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t nb0 = (int64_t)blockIdx.x * NC;
@@ -797,8 +811,10 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
         for (int u = 0; u < U; ++u) {
 #pragma unroll
             for (int q = 0; q < NC; ++q) acc[q] = mfma_chunk<__bf16>(a[u], b[u][q], acc[q]);
-            sx = mfma_chunk<__bf16>(a[u], ones, sx);
-            sxx = mfma_chunk<__bf16>(a[u], a[u], sxx);
+            if constexpr (!PLAIN) {
+                sx = mfma_chunk<__bf16>(a[u], ones, sx);
+                sxx = mfma_chunk<__bf16>(a[u], a[u], sxx);
+            }
         }
     };
     if (ngroups > 0) {
@@ -836,6 +852,15 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
         for (int i = 0; i < 4; ++i) diag[i] = __shfl(tot[2][i], 20 * (lane >> 4) + i);
         const int64_t col = (nb0 + q0) * 16 + (lane & 15);
         const int64_t n = min(col, N - 1), nu = min(col + 16, N - 1);
+        if constexpr (PLAIN) {
+            const float bn = bias ? (float)bias[n] : 0.f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = 4 * (lane >> 4) + i;
+                if (r < M && col < N) out[(int64_t)r * N + col] = (__bf16)(tot[0][i] + bn);
+            }
+            continue;
+        }
         const float cn = c_col[n], bn = b_col[n];
         const float cu = SW ? c_col[nu] : 0.f, bu = SW ? b_col[nu] : 0.f;
         const int64_t o = SW ? (nb0 / 2 + j) * 16 + (lane & 15) : col;
@@ -848,6 +873,10 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
             if (row_stats) {  // serial ablation (the moment products above are then unused)
                 mean = row_stats[2 * min(r, M - 1)];
                 rstd = row_stats[2 * min(r, M - 1) + 1];
+            }
+            if (stats_out && blockIdx.x == 0 && j == 0 && (lane & 15) == 0 && r < M) {
+                stats_out[2 * r] = mean;  // the first column block's lanes export them, once per row
+                stats_out[2 * r + 1] = rstd;
             }
             float v = __builtin_fmaf(rstd, __builtin_fmaf(-mean, cn, tot[0][i]), bn);
             if constexpr (SW) v = silu(v) * __builtin_fmaf(rstd, __builtin_fmaf(-mean, cu, tot[3][i]), bu);
@@ -1058,11 +1087,12 @@ static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_
 
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
                                      int dtype, float eps, int rms, const float* row_stats, void* out,
-                                     hipStream_t s) {
+                                     hipStream_t s, float* stats_out) {
     MainArgs a = packed_args(x, packed, M, K, N, dtype, out);
     a.eps = eps;
     a.rms = rms;
     a.row_stats = row_stats;
+    a.stats_out = stats_out;
     if (dtype == 1 && M <= 16) {
         // Layouts measured on the 8192 x 28672 up-projection: up to 4 tokens the x
         // fragments are nearly free and 4 K-slices per column block stream best;
@@ -1072,7 +1102,7 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks,
                                                             a.nblocks, a.c_col, a.b_col, (int)M, K, N, eps, rms,
-                                                            N, a.row_stats, (__bf16*)out);
+                                                            N, a.row_stats, a.stats_out, (__bf16*)out, nullptr);
         };
         if (M <= 4)
             launch(ln_decode_bf16_kernel<4, 1, 8>, 4, 1);
@@ -1110,7 +1140,7 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks, a.nblocks,
                                                            a.c_col, a.b_col, (int)M, K, np, eps, rms, N,
-                                                           nullptr, (__bf16*)out);
+                                                           nullptr, nullptr, (__bf16*)out, nullptr);
         };
         // one gate/up block pair per workgroup, 4 K-slices, 2-chunk groups: measured
         // flat at 69 % of HBM for 1-16 tokens on the 8192 x 2 x 28672 weights
@@ -1141,6 +1171,24 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
     a.bias = bias;
     a.a_causal = a_causal;
     if (b_layout == 2) {
+        if (dtype == 1 && M <= 16) {
+            // decode shapes: the streaming kernel of the deferred path without its moments,
+            // in the same layouts (so the unfused comparison is like for like)
+            auto launch = [&](auto kern, int ks, int cols) {
+                const int64_t wgs = (a.nblocks + cols - 1) / cols;
+                kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)A, (const char*)a.B, a.kchunks,
+                                                                a.nblocks, nullptr, nullptr, (int)M, K, N, 0.f, 0,
+                                                                N, nullptr, nullptr, (__bf16*)C,
+                                                                (const __bf16*)bias);
+            };
+            if (M <= 4)
+                launch(ln_decode_bf16_kernel<4, 1, 8, false, true>, 4, 1);
+            else if (M <= 8)
+                launch(ln_decode_bf16_kernel<1, 1, 8, false, true>, 1, 1);
+            else
+                launch(ln_decode_bf16_kernel<4, 4, 2, false, true>, 4, 4);
+            return hipGetLastError();
+        }
         if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);
         if (use_big_tiles(M, N, K)) return run_pipe<Epi::kGemm>(a, s);
         return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);

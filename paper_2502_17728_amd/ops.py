@@ -23,7 +23,7 @@ DN_SWIGLU_LAYOUT_VERSION = 0x102
 STATUS = {0: "DN_OK", 1: "DN_ERR_INVALID_ARG", 2: "DN_ERR_UNSUPPORTED", 3: "DN_ERR_MISALIGNED", 4: "DN_ERR_HIP"}
 SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linear_prepare",
            "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered", "ln_linear_serial",
-           "ln_linear_norm_on_load",
+           "ln_linear_norm_on_load", "ln_linear_deferred_post", "rms_linear_deferred_post",
            "swiglu_packed_bytes", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
            "attention_deferred", "attention_decode_workspace_bytes", "attention_decode_deferred", "layernorm",
            "rmsnorm", "silu_mul", "softmax", "gemm")
@@ -56,6 +56,8 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.ln_linear_prepare_centered.argtypes = lib.ln_linear_prepare.argtypes
     lib.ln_linear_serial.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp, vp]
     lib.ln_linear_norm_on_load.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp, vp]
+    lib.ln_linear_deferred_post.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp, vp, vp, vp, vp]
+    lib.rms_linear_deferred_post.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp, vp, vp, vp]
     lib.rms_linear_deferred.argtypes = [vp, ctypes.POINTER(LnLinearWeights), i64, f32, vp, vp]
     lib.swiglu_packed_bytes.argtypes, lib.swiglu_packed_bytes.restype = [i64, i64, i32], ctypes.c_size_t
     lib.swiglu_prepare.argtypes = [vp, vp, vp, i64, i64, i32, vp, ctypes.c_size_t, ctypes.POINTER(LnLinearWeights),
@@ -72,7 +74,8 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.softmax.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp]
     lib.gemm.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, i32, i32, vp, vp]
     for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered",
-              "ln_linear_serial", "ln_linear_norm_on_load", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
+              "ln_linear_serial", "ln_linear_norm_on_load", "ln_linear_deferred_post",
+              "rms_linear_deferred_post", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
               "attention_deferred", "attention_decode_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax",
               "gemm"):
         getattr(lib, f).restype = i32
@@ -191,6 +194,34 @@ def ln_linear_norm_on_load(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5
     _check("ln_linear_norm_on_load", _lib.ln_linear_norm_on_load(
         _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(stats, "stats"), _dev(out, "out"), _stream(stream)))
     return out
+
+
+def linear_deferred_post(x: torch.Tensor, w: PreparedLinear, gamma: torch.Tensor, beta: Optional[torch.Tensor] = None,
+                         eps: float = 1e-5, rms: bool = False, stats: Optional[torch.Tensor] = None,
+                         y: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                         stream=None):
+    """Post-LN placement: (out, y, stats) -- the deferred product and the normalized rows."""
+    M, K = x.shape
+    if out is None:
+        out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
+    if y is None:
+        y = torch.empty_like(x)
+    if stats is None:
+        stats = torch.empty(2 * M, dtype=torch.float32, device=x.device)
+    if _dt(x) != w.desc.dtype or gamma.dtype != x.dtype or (beta is not None and beta.dtype != x.dtype):
+        raise TypeError("x, gamma, beta and the prepared weights must share one dtype")
+    if rms:
+        if beta is not None:
+            raise ValueError("RMSNorm has no shift")
+        st = _lib.rms_linear_deferred_post(_dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(gamma, "gamma"),
+                                           _dev(stats, "stats"), _dev(y, "y"), _dev(out, "out"), _stream(stream))
+        _check("rms_linear_deferred_post", st)
+    else:
+        st = _lib.ln_linear_deferred_post(_dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(gamma, "gamma"),
+                                          _dev(beta, "beta"), _dev(stats, "stats"), _dev(y, "y"), _dev(out, "out"),
+                                          _stream(stream))
+        _check("ln_linear_deferred_post", st)
+    return out, y, stats
 
 
 def rms_linear_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,

@@ -109,6 +109,28 @@ def test_ln_linear_serial_validation():
     assert f(P, ctypes.byref(_w(version=0)), 4, 1e-5, P3 + (1 << 30), P2, None) == INVALID
 
 
+@pytest.mark.parametrize("rms", [False, True])
+def test_linear_deferred_post_validation(rms):
+    S, Y = P3 + (1 << 34), P3 + (1 << 35)
+    w = _w()
+
+    def f(x, g, b, st, y, out, ww=w, eps=1e-5):
+        if rms:
+            return ops._lib.rms_linear_deferred_post(x, ctypes.byref(ww), 4, eps, g, st, y, out, None)
+        return ops._lib.ln_linear_deferred_post(x, ctypes.byref(ww), 4, eps, g, b, st, y, out, None)
+    G = P + (1 << 33)
+    assert f(P, None, None, S, Y, P2) == INVALID          # gamma required
+    assert f(P, G, None, None, Y, P2) == INVALID          # stats required
+    assert f(P, G, None, S, None, P2) == INVALID          # y required
+    assert f(P, G, None, S, Y + 8, P2) == MISALIGNED
+    assert f(P, G, None, S + 4, Y, P2) == MISALIGNED
+    assert f(P, G, None, S, P + 64, P2) == INVALID        # y overlaps x
+    assert f(P, G, None, P2 + 16, Y, P2) == INVALID       # stats overlap out
+    assert f(P, G, None, S, Y, P2, ww=_w(K=68)) == UNSUPPORTED
+    assert f(P, G, None, S, Y, P2, ww=_w(version=0)) == INVALID
+    assert f(P, G, None, S, Y, P2, eps=-1.0) == INVALID  # the product's own checks still apply
+
+
 def test_ln_linear_norm_on_load_validation():
     f = ops._lib.ln_linear_norm_on_load
     S = P3 + (1 << 34)

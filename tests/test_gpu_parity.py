@@ -112,6 +112,19 @@ def test_gemm_sampled(ops, M, K, N, layout):
     assert rowwise_rel_err(C.cpu()[torch.as_tensor(rows)], ref) <= TOL[torch.bfloat16]
 
 
+@pytest.mark.parametrize("M,K,N", [(1, 1024, 520), (5, 8200, 264), (16, 512, 72), (3, 8, 8)])
+def test_gemm_packed_decode(ops, M, K, N):
+    # decode shapes with packed weights: the streaming kernel without moments (the unfused
+    # comparators' GEMM at M <= 16), bias added once; ragged N and K
+    g = torch.Generator().manual_seed(M + K)
+    A = torch.randn(M, K, generator=g).to(torch.bfloat16)
+    B = (torch.randn(K, N, generator=g) / K ** 0.5).to(torch.bfloat16)
+    bias = torch.randn(N, generator=g).to(torch.bfloat16)
+    Bd = ops.ln_linear_prepare(cuda(B), torch.ones(K, dtype=torch.bfloat16, device="cuda"))
+    C = ops.gemm(cuda(A), Bd, cuda(bias), b_layout=2)
+    assert rowwise_rel_err(C.cpu(), oracle.linear(A, B, bias)) <= TOL[torch.bfloat16]
+
+
 def test_gemm_packed_f32(ops):
     g = torch.Generator().manual_seed(6)
     A, B = torch.randn(45, 72, generator=g), torch.randn(72, 40, generator=g)
@@ -231,6 +244,40 @@ def test_ln_linear_norm_on_load_rejects_small_shapes(ops):
     with pytest.raises(ops.DNError) as e:
         ops.ln_linear_norm_on_load(cuda(case["x"]), w, case["eps"])
     assert e.value.status == 2  # DN_ERR_UNSUPPORTED: the ablation runs on the large tiles only
+
+
+@pytest.mark.parametrize("M,K,N,dtype,norm", [(37, 104, 72, "f32", "layernorm"), (257, 1024, 264, "bf16", "layernorm"),
+                                              (5, 1024, 520, "bf16", "layernorm"), (4104, 320, 4096, "bf16", "layernorm"),
+                                              (300, 512, 200, "bf16", "rms"), (3, 8200, 64, "bf16", "rms")])
+def test_linear_deferred_post(ops, M, K, N, dtype, norm):
+    # post-LN placement: the deferred product and the normalized rows (the residual branch) from
+    # the statistics the product's kernel reduced; covers the fp32, 128x128, decode and 256x256
+    # kernels, each exporting the statistics once per row
+    rms = norm == "rms"
+    case = I.make_ln_case(M, K, N, dtype, seed=M + K + 7, outliers=2, norm=norm)
+    g, b = cuda(case["gamma"]), cuda(case["beta"])
+    w = ops.ln_linear_prepare(cuda(case["W"]), g, b, cuda(case["bias"]))
+    out, y, st = ops.linear_deferred_post(cuda(case["x"]), w, g, None if rms else b, case["eps"], rms=rms)
+    torch.cuda.synchronize()
+    rows = None if M < 1000 else I.sample_rows(M, 24, seed=8)
+    pick = (lambda t: t) if rows is None else (lambda t: t[torch.as_tensor(rows)])
+    xs = pick(case["x"])
+    if rms:
+        ref = oracle.rms_linear(xs, case["gamma"], case["W"], case["bias"], case["eps"])
+        yref = oracle.rmsnorm(xs, case["gamma"], case["eps"])
+    else:
+        ref = oracle.ln_linear(xs, case["gamma"], case["beta"], case["W"], case["bias"], case["eps"])
+        yref = oracle.layernorm(xs, case["gamma"], case["beta"], case["eps"])
+    tol = TOL[case["x"].dtype]
+    e_out, e_y = rowwise_rel_err(pick(out.cpu()), ref), rowwise_rel_err(pick(y.cpu()), yref)
+    print(f"linear_deferred_post {M}x{K}x{N} {dtype} {norm}: out err={e_out:.3e}, y err={e_y:.3e}")
+    assert e_out <= tol and e_y <= (tol if dtype == "f32" else tol / 4)
+    sd = pick(st.cpu().double().reshape(M, 2)).numpy()
+    xd = oracle.to_f64(xs)
+    mean = np.zeros(len(xd)) if rms else xd.mean(1)
+    var = (xd * xd).mean(1) if rms else xd.var(1)
+    np.testing.assert_allclose(sd[:, 0], mean, rtol=1e-4, atol=1e-5)
+    np.testing.assert_allclose(sd[:, 1], 1 / np.sqrt(var + case["eps"]), rtol=1e-4)
 
 
 # ---------------------------------------------------------------------------- RMSNorm -> Linear
