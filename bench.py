@@ -57,13 +57,13 @@ TRAFFIC = {
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
         "fetch_kib": 1151051, "fetch_scale": 1.99993, "write_kib": 66101, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("ba3f876de916cf46db9dbbce201fe0de48d8ea4f7fa9f23c602698dac510b8f7",
+        "sha256": ("f696cada9dc6f28f3770ef8112c1a25e65819baa4e5e0657c2c103f1eec3130e",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 296665, "fetch_scale": 1.99993, "write_kib": 102404, "write_scale": 1.0},
+        "fetch_kib": 296632, "fetch_scale": 1.99993, "write_kib": 102403, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("ba3f876de916cf46db9dbbce201fe0de48d8ea4f7fa9f23c602698dac510b8f7",
+        "sha256": ("f696cada9dc6f28f3770ef8112c1a25e65819baa4e5e0657c2c103f1eec3130e",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 229894, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
+        "fetch_kib": 229642, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
         "sha256": ("1d236d3287681b9f665236910169ce2d264f983bf71b6c6a4e562073e8cd2777",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),

@@ -1085,6 +1085,26 @@ static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_
     return a;
 }
 
+// Decode-shaped launches (M <= 16): 16 waves split K (16 waves per CU hide the
+// HBM latency of the W' stream) and each workgroup owns nc column blocks, nc
+// chosen so the grid is about one workgroup per CU (at most 7: 144 KiB of LDS
+// for the partial sums).  Measured on the 8192 x 28672 up-projection (1792
+// blocks, nc = 7): 78.5-78.8 us for 1-16 tokens, against 81-91 us for the
+// 4- and 8-wave layouts with 1-4 blocks per workgroup.
+template <bool PLAIN, class F>
+static void decode_dispatch(int64_t nblocks, F&& launch) {
+    const int64_t nc = std::min<int64_t>(7, std::max<int64_t>(1, (nblocks + 255) / 256));
+    switch (nc) {
+        case 1: launch(ln_decode_bf16_kernel<16, 1, 1, false, PLAIN>, 16, 1); break;
+        case 2: launch(ln_decode_bf16_kernel<16, 2, 1, false, PLAIN>, 16, 2); break;
+        case 3: launch(ln_decode_bf16_kernel<16, 3, 1, false, PLAIN>, 16, 3); break;
+        case 4: launch(ln_decode_bf16_kernel<16, 4, 1, false, PLAIN>, 16, 4); break;
+        case 5: launch(ln_decode_bf16_kernel<16, 5, 1, false, PLAIN>, 16, 5); break;
+        case 6: launch(ln_decode_bf16_kernel<16, 6, 1, false, PLAIN>, 16, 6); break;
+        default: launch(ln_decode_bf16_kernel<16, 7, 1, false, PLAIN>, 16, 7); break;
+    }
+}
+
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
                                      int dtype, float eps, int rms, const float* row_stats, void* out,
                                      hipStream_t s, float* stats_out) {
@@ -1094,22 +1114,13 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
     a.row_stats = row_stats;
     a.stats_out = stats_out;
     if (dtype == 1 && M <= 16) {
-        // Layouts measured on the 8192 x 28672 up-projection: up to 4 tokens the x
-        // fragments are nearly free and 4 K-slices per column block stream best;
-        // at 5-8 one wave per column block (the whole K) does; beyond that x is
-        // re-read from L2 often enough that each wave shares it across 4 blocks.
         auto launch = [&](auto kern, int ks, int cols) {
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks,
                                                             a.nblocks, a.c_col, a.b_col, (int)M, K, N, eps, rms,
                                                             N, a.row_stats, a.stats_out, (__bf16*)out, nullptr);
         };
-        if (M <= 4)
-            launch(ln_decode_bf16_kernel<4, 1, 8>, 4, 1);
-        else if (M <= 8)
-            launch(ln_decode_bf16_kernel<1, 1, 8>, 1, 1);
-        else
-            launch(ln_decode_bf16_kernel<4, 4, 2>, 4, 4);
+        decode_dispatch<false>(a.nblocks, launch);
         return hipGetLastError();
     }
     if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
@@ -1181,12 +1192,7 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
                                                                 N, nullptr, nullptr, (__bf16*)C,
                                                                 (const __bf16*)bias);
             };
-            if (M <= 4)
-                launch(ln_decode_bf16_kernel<4, 1, 8, false, true>, 4, 1);
-            else if (M <= 8)
-                launch(ln_decode_bf16_kernel<1, 1, 8, false, true>, 1, 1);
-            else
-                launch(ln_decode_bf16_kernel<4, 4, 2, false, true>, 4, 4);
+            decode_dispatch<true>(a.nblocks, launch);
             return hipGetLastError();
         }
         if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);
