@@ -133,6 +133,13 @@ def test_gemm_packed_f32(ops):
     assert rowwise_rel_err(C.cpu(), oracle.linear(A, B)) <= TOL[torch.float32]
 
 
+def test_ln_linear_ffn_prefill_workload_sampled(ops):
+    # the 8192 x 8192 x 28672 up-projection at full size (the 256x256 kernel, 14 waves of tiles)
+    w = I.LN_FFN_PREFILL
+    case = I.make_ln(w)
+    _ln_check(ops, case, rows=I.sample_rows(w.M, 16, seed=5))
+
+
 def test_ln_linear_qkv_workload_sampled(ops):
     w = I.LN_QKV
     case = I.make_ln(w)
