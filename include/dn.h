@@ -271,7 +271,9 @@ DN_API dn_status attention_deferred(const void* Q, const void* K, const void* V,
  * attention_decode_workspace_bytes(BH, Lq, Lk, d) bytes, 16-byte aligned, not
  * overlapping the other arguments; its contents are scratch.  Q[BH][Lq][d],
  * K, V[BH][Lk][d], out[BH][Lq][d]; other rules as attention_deferred
- * (DN_ERR_UNSUPPORTED for Lq > 16).  attention_decode_workspace_bytes
+ * (DN_ERR_UNSUPPORTED for Lq > 16).  With enough heads to fill the chip the
+ * keys are not split and one pass writes out directly (the workspace is then
+ * not touched).  attention_decode_workspace_bytes
  * returns 0 for an invalid request.
  */
 DN_API size_t attention_decode_workspace_bytes(int64_t BH, int64_t Lq, int64_t Lk, int64_t d);

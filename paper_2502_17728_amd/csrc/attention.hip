@@ -400,6 +400,12 @@ static hipError_t run_attention_decode(const void* Q, const void* K, const void*
     int nsplit;
     int64_t kchunk;
     attention_decode_split(BH, Lk, D, &nsplit, &kchunk);
+    if (nsplit == 1) {  // enough heads to fill the chip: one pass, the division in the kernel's epilogue
+        attention_kernel<D, 1, 1, kDecNS, kDecBKV><<<dim3((unsigned)BH), 64, 0, s>>>(
+            (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, 0, scale * fa::kLog2e, 1, 1, Lk,
+            nullptr, (__bf16*)out);
+        return hipGetLastError();
+    }
     attention_kernel<D, 1, 1, kDecNS, kDecBKV><<<dim3((unsigned)(BH * nsplit)), 64, 0, s>>>(
         (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, 0, scale * fa::kLog2e, 1, nsplit, kchunk,
         part, nullptr);
