@@ -105,6 +105,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time of the oracle sample behind cpu_baseline")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, copy a buffer of this many MiB twice (a plain copy "
                          "kernel of known size, to scale hardware traffic counters)")
@@ -587,9 +589,16 @@ def main():
                 rows = 1024 if s.w.L >= 4096 else 2048
             if isinstance(s, DecodeAttnSite):
                 rows = 128
+            # a short calibration sample, then one sized to about cpu_seconds / sites of work
             dt, frac, desc = s.oracle_sample(oracle, I, threads, rows)
+            budget = args.cpu_seconds / len(sites)
+            for _ in range(3):  # fixed costs make small samples look slow per row: refine
+                if dt >= 0.5 * budget or frac >= 1.0:
+                    break
+                rows = max(rows + 1, int(rows * min(budget / max(dt, 1e-3), 1.0 / frac)))
+                dt, frac, desc = s.oracle_sample(oracle, I, threads, rows)
             extrap += dt / frac
-            descs.append(desc)
+            descs.append(f"{desc} ({dt:.1f} s)")
         cpu = {"value": round(flops / extrap / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
                "sample": "; ".join(descs) + f"; time extrapolated by work to the whole step "
                          f"({extrap:.1f} s per step on {threads} threads)"}
