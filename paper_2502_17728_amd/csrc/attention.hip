@@ -30,6 +30,13 @@
 // above the workgroup's queries are never read; a wave skips the products of
 // steps wholly above its own queries; keys above the diagonal inside a step
 // are masked to -inf before the exponentials.
+//
+// Decode (a few new queries against a long key/value cache).  One workgroup
+// per head would leave most CUs idle, so the keys of each head are cut into
+// ranges, one single-wave workgroup each, sized so that the grid is one
+// resident round; every range leaves (acc, l, m) in fp32 and a merge kernel
+// combines them with weights 2^(m_g - m) -- the deferred division of Eq. (8)
+// postponed once more, past the reduction over key ranges.
 #include <algorithm>
 
 #include "dn_device.hpp"
@@ -385,7 +392,7 @@ inline int64_t decode_lds_bytes(int64_t d) { return (int64_t)kDecNS * 2 * kDecBK
 // d = 128, 5 at d = 64), spread over the heads; each split a whole number of steps.
 // Measured on 256 heads x 8192 keys, d = 128: one resident round beats 2 and 4 rounds
 // (their tails) and the 64-key, 2-slot ring (fewer bytes in flight per CU).
-void attention_decode_split(int64_t BH, int64_t Lk, int64_t d, int* nsplit, int64_t* kchunk) {
+static void attention_decode_split(int64_t BH, int64_t Lk, int64_t d, int* nsplit, int64_t* kchunk) {
     const int64_t wgs = kCUs * (kLdsPerCU / decode_lds_bytes(d));
     const int64_t steps = (Lk + kDecBKV - 1) / kDecBKV;
     const int64_t want = std::max<int64_t>(1, std::min<int64_t>(steps, (wgs + BH - 1) / BH));

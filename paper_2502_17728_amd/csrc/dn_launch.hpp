@@ -69,7 +69,8 @@ hipError_t launch_attention_deferred(const void* Q, const void* K, const void* V
                                      int64_t Lk, int64_t d, int causal, float scale, void* out, hipStream_t s);
 
 // Decode attention (Lq <= 16, all Lk keys visible): key ranges split over workgroups
-// (partials in `workspace`, attention_decode_workspace_bytes of them), then one merge.
+// (partials in `workspace`, attention_decode_workspace_bytes of them), then one merge;
+// a single pass straight to `out` when the heads alone fill the chip.
 size_t attention_decode_workspace_bytes(int64_t BH, int64_t Lq, int64_t Lk, int64_t d);
 hipError_t launch_attention_decode(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq, int64_t Lk,
                                    int64_t d, float scale, void* workspace, void* out, hipStream_t s);
