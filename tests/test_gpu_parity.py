@@ -287,6 +287,16 @@ def test_linear_deferred_post(ops, M, K, N, dtype, norm):
     np.testing.assert_allclose(sd[:, 1], 1 / np.sqrt(var + case["eps"]), rtol=1e-4)
 
 
+def test_linear_deferred_post_deterministic(ops):
+    case = I.make_ln_case(4104, 320, 4096, "bf16", seed=23)
+    g, b = cuda(case["gamma"]), cuda(case["beta"])
+    w = ops.ln_linear_prepare(cuda(case["W"]), g, b)
+    x = cuda(case["x"])
+    r1 = ops.linear_deferred_post(x, w, g, b, case["eps"])
+    r2 = ops.linear_deferred_post(x, w, g, b, case["eps"])
+    assert all(torch.equal(p, q) for p, q in zip(r1, r2))
+
+
 # ---------------------------------------------------------------------------- RMSNorm -> Linear
 @pytest.mark.parametrize("M,K,N", [(37, 104, 72), (1, 8, 8), (300, 512, 200)])
 def test_rms_linear_f32_ragged(ops, M, K, N):
@@ -584,6 +594,16 @@ def test_attention_decode_workspace_reuse(ops):
     refb = oracle.attention(big["Q"].reshape(-1, 128), big["K"], big["V"], big["scale"],
                             head=np.repeat(np.arange(16), 2))
     assert rowwise_rel_err(out.cpu().reshape(-1, 128), refb) <= TOL[torch.bfloat16]
+
+
+def test_attention_deterministic(ops):
+    # no atomics anywhere: the same inputs give the same bits, causal and decode
+    case = I.make_qkv_case(2, 700, 128, True, seed=21)
+    q, k, v = cuda(case["Q"]), cuda(case["K"]), cuda(case["V"])
+    assert torch.equal(ops.attention_deferred(q, k, v, causal=True), ops.attention_deferred(q, k, v, causal=True))
+    dec = I.make_decode_case(4, 3, 5000, 128, seed=22)
+    q, k, v = cuda(dec["Q"]), cuda(dec["K"]), cuda(dec["V"])
+    assert torch.equal(ops.attention_decode_deferred(q, k, v), ops.attention_decode_deferred(q, k, v))
 
 
 def test_attention_decode_workload_sampled(ops):
