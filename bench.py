@@ -101,7 +101,7 @@ def parse():
                     choices=["layer", "small", "ln_qkv", "causal_softmax_pv", "ffn_prefill",
                              "ffn_decode_t1", "ffn_decode_t4", "ffn_decode_t16", "rms_qkv",
                              "rms_ffn_decode_t1", "swiglu_prefill", "swiglu_decode_t1", "causal_attention",
-                             "decode_attention"])
+                             "decode_attention", "decode_attention_gqa"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None)
@@ -360,11 +360,14 @@ class DecodeAttnSite:
         c = self.case
         self.Q, self.K, self.V = c["Q"].cuda(), c["K"].cuda(), c["V"].cuda()
         self.out = torch.empty_like(self.Q)
-        self.ws = torch.empty(ops.attention_decode_workspace_bytes(w.BH, w.Lq, w.Lk, w.d), dtype=torch.uint8,
-                              device="cuda")
-        # conventional comparator: S = (scale Q) K^T stored, then deferred Softmax -> P.V on S
-        self.Qs = (self.Q.float() * c["scale"]).to(torch.bfloat16)
-        self.S = torch.empty((w.BH, w.Lq, w.Lk), dtype=torch.bfloat16, device="cuda")
+        self.ws = torch.empty(ops.attention_decode_workspace_bytes(w.BH, w.group * w.Lq, w.Lk, w.d),
+                              dtype=torch.uint8, device="cuda")
+        # conventional comparator: S = (scale Q) K^T stored, then deferred Softmax -> P.V on S (the
+        # query heads of one key/value head batched together as its rows)
+        gq = w.group * w.Lq
+        self.Qs = (self.Q.float() * c["scale"]).to(torch.bfloat16).reshape(w.BH, gq, w.d)
+        self.S = torch.empty((w.BH, gq, w.Lk), dtype=torch.bfloat16, device="cuda")
+        self.Qg, self.out_g = self.Q.reshape(w.BH, gq, w.d), self.out.view(w.BH, gq, w.d)
         self.ops = ops
         torch.cuda.synchronize()
 
@@ -374,11 +377,11 @@ class DecodeAttnSite:
 
     def unfused(self):
         self.ops.gemm(self.Qs, self.K, b_layout=1, out=self.S)
-        self.ops.softmax_pv_deferred(self.S, self.V, out=self.out)
+        self.ops.softmax_pv_deferred(self.S, self.V, out=self.out_g)
 
     def single_pass(self):
-        # ablation: the same computation without the key split (one workgroup per head)
-        self.ops.attention_deferred(self.Q, self.K, self.V, causal=False, scale=self.case["scale"], out=self.out)
+        # ablation: the same computation without the key split (one workgroup per key/value head)
+        self.ops.attention_deferred(self.Qg, self.K, self.V, causal=False, scale=self.case["scale"], out=self.out_g)
 
     def flops(self):
         return self.w.flops()
@@ -391,13 +394,15 @@ class DecodeAttnSite:
 
     def oracle_sample(self, oracle, I, threads, rows):
         w = self.w
-        heads = I.sample_rows(w.BH, max(1, rows // w.Lq), seed=12)
+        gq = w.group * w.Lq
+        heads = I.sample_rows(w.BH, max(1, rows // gq), seed=12)
         hsel = torch.as_tensor(heads)
+        Qg = self.case["Q"].reshape(w.BH, gq, w.d)[hsel].reshape(-1, w.d)
         t0 = time.perf_counter()
-        oracle.attention(self.case["Q"][hsel].reshape(-1, w.d), self.case["K"][hsel], self.case["V"][hsel],
-                         self.case["scale"], head=np.repeat(np.arange(len(heads)), w.Lq), nthreads=threads)
+        oracle.attention(Qg, self.case["K"][hsel], self.case["V"][hsel], self.case["scale"],
+                         head=np.repeat(np.arange(len(heads)), gq), nthreads=threads)
         dt = time.perf_counter() - t0
-        return dt, len(heads) / w.BH, f"{len(heads)} of {w.BH} decode heads"
+        return dt, len(heads) / w.BH, f"{len(heads)} of {w.BH} decode key/value heads"
 
 
 def build_sites(ops, I, name):
@@ -419,6 +424,8 @@ def build_sites(ops, I, name):
         return [AttnSite(ops, I, I.ATTN_CAUSAL)], I.ATTN_CAUSAL.name
     if name == "decode_attention":
         return [DecodeAttnSite(ops, I, I.ATTN_DECODE)], I.ATTN_DECODE.name
+    if name == "decode_attention_gqa":
+        return [DecodeAttnSite(ops, I, I.ATTN_DECODE_GQA)], I.ATTN_DECODE_GQA.name
     if name == "swiglu_prefill":
         return [SwiGLUSite(ops, I, I.SWIGLU_PREFILL)], I.SWIGLU_PREFILL.name
     if name == "swiglu_decode_t1":

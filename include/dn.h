@@ -271,7 +271,11 @@ DN_API dn_status attention_deferred(const void* Q, const void* K, const void* V,
  * attention_decode_workspace_bytes(BH, Lq, Lk, d) bytes, 16-byte aligned, not
  * overlapping the other arguments; its contents are scratch.  Q[BH][Lq][d],
  * K, V[BH][Lk][d], out[BH][Lq][d]; other rules as attention_deferred
- * (DN_ERR_UNSUPPORTED for Lq > 16).  With enough heads to fill the chip the
+ * (DN_ERR_UNSUPPORTED for Lq > 16).  Grouped-query attention (g query heads
+ * sharing each key/value head, the g heads consecutive): pass Q and out as
+ * [BH][g * Lq][d] -- the same memory as [BH * g][Lq][d] -- with Lq := g * Lq
+ * (<= 16), so each key/value tile read from HBM serves all g heads at once.
+ * With enough heads to fill the chip the
  * keys are not split and one pass writes out directly (the workspace is then
  * not touched).  attention_decode_workspace_bytes
  * returns 0 for an invalid request.

@@ -99,28 +99,37 @@ ATTN_CAUSAL = SMWorkload("causal_attention_bf16_32x8192x8192_d128", 4, 32, 8192,
 
 @dataclasses.dataclass(frozen=True)
 class DecodeAttnWorkload:
-    """Attention of a few new query tokens against a cache of Lk keys (every key visible)."""
+    """Attention of a few new query tokens against a cache of Lk keys (every key visible).
+
+    ``group`` query heads share each key/value head (grouped-query attention; 1 = one
+    query head per key/value head); query head h * group + r reads key/value head h.
+    """
     name: str
     wid: int
-    BH: int            # sequences x heads
-    Lq: int            # new tokens per sequence (<= 16)
+    BH: int            # sequences x key/value heads
+    Lq: int            # new tokens per sequence (group * Lq <= 16)
     Lk: int            # cached keys
     d: int             # head dim
+    group: int = 1     # query heads per key/value head
 
     def pairs(self) -> float:
-        return float(self.BH) * self.Lq * self.Lk
+        return float(self.BH) * self.group * self.Lq * self.Lk
 
     def flops(self) -> float:
         return 4.0 * self.pairs() * self.d  # both products
 
     def bytes(self) -> float:
         """Algorithmic HBM bytes: K and V read once, Q read and the output written (bf16)."""
-        return 2.0 * (2.0 * self.BH * self.Lk * self.d + 2.0 * self.BH * self.Lq * self.d)
+        return 2.0 * (2.0 * self.BH * self.Lk * self.d + 2.0 * self.BH * self.group * self.Lq * self.d)
 
 
 # Decode attention: 8 sequences x 32 heads, one new token each against 8192 cached
 # keys of d = 128 (1 GiB of K and V, larger than the last-level cache).
 ATTN_DECODE = DecodeAttnWorkload("decode_attention_bf16_256x1x8192_d128", 10, 256, 1, 8192, 128)
+# The same cache read by grouped queries, as in 8B-class Llama 3 models: 32 sequences x
+# 8 key/value heads, each shared by 4 of the 32 query heads, one new token.
+ATTN_DECODE_GQA = DecodeAttnWorkload("decode_attention_gqa4_bf16_256kv_x1x8192_d128", 11, 256, 1, 8192, 128,
+                                     group=4)
 
 
 # RMSNorm -> Linear with Llama shapes: the fused QKV projection of an 8B-class
@@ -149,7 +158,7 @@ def swiglu_decode(t: int) -> LNWorkload:
 WORKLOADS = {w.name: w for w in (LN_F32_SMALL, SM_BF16_SMALL, LN_QKV, SM_CAUSAL, LN_FFN_PREFILL,
                                  ln_ffn_decode(1), ln_ffn_decode(4), ln_ffn_decode(16),
                                  RMS_QKV, rms_ffn_decode(1), SWIGLU_PREFILL, swiglu_decode(1), ATTN_CAUSAL,
-                                 ATTN_DECODE)}
+                                 ATTN_DECODE, ATTN_DECODE_GQA)}
 
 # tensor ids inside a workload's seed
 _X, _GAMMA, _BETA, _W, _OUTLIER_CH, _S, _Q, _KEY, _V, _W_UP = range(10)
@@ -276,20 +285,23 @@ def make_qkv_case(BH: int, L: int, d: int, causal: bool, seed: int = 0) -> dict:
 
 
 def make_decode(w: DecodeAttnWorkload, seed: int = 0, heads: Optional[Sequence[int]] = None) -> dict:
-    """Q[n, Lq, d] and the cache K, V[n, Lk, d] (bf16 CPU tensors) of the listed heads."""
+    """Q[n * group, Lq, d] and the cache K, V[n, Lk, d] (bf16 CPU tensors) of the listed
+    key/value heads (query heads h * group .. h * group + group - 1 for head h)."""
     heads = list(range(w.BH)) if heads is None else list(heads)
-    Q = torch.empty((len(heads), w.Lq, w.d), dtype=torch.bfloat16)
+    g = w.group
+    Q = torch.empty((len(heads) * g, w.Lq, w.d), dtype=torch.bfloat16)
     K, V = (torch.empty((len(heads), w.Lk, w.d), dtype=torch.bfloat16) for _ in range(2))
     for i, h in enumerate(heads):
-        Q[i] = to_storage(_normal(_rng(seed, w.wid, _Q, h), (w.Lq, w.d), 1.0), "bf16")
+        for r in range(g):
+            Q[i * g + r] = to_storage(_normal(_rng(seed, w.wid, _Q, h * g + r), (w.Lq, w.d), 1.0), "bf16")
         K[i] = to_storage(_normal(_rng(seed, w.wid, _KEY, h), (w.Lk, w.d), 1.0), "bf16")
         V[i] = to_storage(_normal(_rng(seed, w.wid, _V, h), (w.Lk, w.d), 1.0), "bf16")
     return dict(Q=Q, K=K, V=V, causal=False, scale=1.0 / math.sqrt(w.d))
 
 
-def make_decode_case(BH: int, Lq: int, Lk: int, d: int, seed: int = 0) -> dict:
+def make_decode_case(BH: int, Lq: int, Lk: int, d: int, seed: int = 0, group: int = 1) -> dict:
     """A decode-attention case of any size with the same recipe (for parity tests)."""
-    return make_decode(DecodeAttnWorkload(f"decode_{BH}x{Lq}x{Lk}_d{d}", 203, BH, Lq, Lk, d), seed)
+    return make_decode(DecodeAttnWorkload(f"decode_{BH}x{Lq}x{Lk}_d{d}_g{group}", 203, BH, Lq, Lk, d, group), seed)
 
 
 def make_sm_case(BH: int, L: int, d: int, causal: bool, seed: int = 0, s_std: float = 2.0,

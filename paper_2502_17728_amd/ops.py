@@ -304,21 +304,29 @@ def attention_decode_workspace_bytes(BH: int, Lq: int, Lk: int, d: int) -> int:
 def attention_decode_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, scale: Optional[float] = None,
                               workspace: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
                               stream=None) -> torch.Tensor:
-    """Decode attention (Lq <= 16, every key visible) split over key ranges, then merged."""
-    BH, Lq, d = Q.shape
-    Lk = K.shape[1]
-    if tuple(K.shape) != (BH, Lk, d) or tuple(V.shape) != (BH, Lk, d):
-        raise ValueError("K and V must be [BH, Lk, d] like Q")
+    """Decode attention (every key visible) split over key ranges, then merged.
+
+    Q[BH * g, Lq, d] against K, V[BH, Lk, d]: with g > 1 (grouped-query attention) query
+    heads h * g .. h * g + g - 1 share key/value head h, and the g heads' rows go through
+    the kernel together as g * Lq (<= 16) queries of that head.
+    """
+    BHq, Lq, d = Q.shape
+    BH, Lk = K.shape[0], K.shape[1]
+    if K.shape[2] != d or tuple(V.shape) != tuple(K.shape) or BHq % BH:
+        raise ValueError("K and V must be [BH, Lk, d] with the query heads a multiple of BH")
+    g = BHq // BH
+    if out is None:
+        out = torch.empty_like(Q)
+    Q, out_k = Q.reshape(BH, g * Lq, d), out.view(BH, g * Lq, d)
+    Lq = g * Lq
     if scale is None:
         scale = 1.0 / float(d) ** 0.5
     nbytes = attention_decode_workspace_bytes(BH, Lq, Lk, d)
     if workspace is None:
         workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=Q.device)
-    if out is None:
-        out = torch.empty_like(Q)
     _check("attention_decode_deferred", _lib.attention_decode_deferred(
         _dev(Q, "Q"), _dev(K, "K"), _dev(V, "V"), BH, Lq, Lk, d, float(scale), _dt(Q), _dev(workspace, "workspace"),
-        workspace.numel() * workspace.element_size(), _dev(out, "out"), _stream(stream)))
+        workspace.numel() * workspace.element_size(), _dev(out_k, "out"), _stream(stream)))
     return out
 
 

@@ -596,6 +596,33 @@ def test_attention_decode_workspace_reuse(ops):
     assert rowwise_rel_err(out.cpu().reshape(-1, 128), refb) <= TOL[torch.bfloat16]
 
 
+def _decode_gqa_check(ops, case, heads=None):
+    Q, K, V = case["Q"], case["K"], case["V"]
+    BH, d = K.shape[0], K.shape[2]
+    gq = Q.shape[0] // BH * Q.shape[1]  # query rows per key/value head
+    out = ops.attention_decode_deferred(cuda(Q), cuda(K), cuda(V), scale=case["scale"])
+    torch.cuda.synchronize()
+    hs = torch.as_tensor(np.arange(BH) if heads is None else np.asarray(heads))
+    ref = oracle.attention(Q.reshape(BH, gq, d)[hs].reshape(-1, d), K[hs], V[hs], case["scale"],
+                           head=np.repeat(np.arange(len(hs)), gq))
+    got = out.cpu().reshape(BH, gq, d)[hs].reshape(-1, d)
+    err = rowwise_rel_err(got, ref)
+    print(f"attention_decode_deferred GQA Q{tuple(Q.shape)} K{tuple(K.shape)}: err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
+
+
+@pytest.mark.parametrize("BH,g,Lq,Lk,d", [(8, 4, 1, 3000, 128), (3, 8, 2, 777, 64), (2, 16, 1, 64, 128),
+                                          (600, 4, 1, 1000, 128)])
+def test_attention_decode_grouped_query(ops, BH, g, Lq, Lk, d):
+    # g query heads per key/value head go through the kernel as g * Lq rows of that head
+    _decode_gqa_check(ops, I.make_decode_case(BH, Lq, Lk, d, seed=BH + g, group=g))
+
+
+def test_attention_decode_gqa_workload_sampled(ops):
+    w = I.ATTN_DECODE_GQA
+    _decode_gqa_check(ops, I.make_decode(w), heads=[0, 5, 100, 200, w.BH - 1])
+
+
 def test_attention_deterministic(ops):
     # no atomics anywhere: the same inputs give the same bits, causal and decode
     case = I.make_qkv_case(2, 700, 128, True, seed=21)
