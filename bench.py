@@ -522,7 +522,7 @@ def main():
             # speedups compare like with like: each path timed alone, back to back on its own inputs
             # (inside the step the kernel follows the other site, whose traffic evicts the caches);
             # the two alternate over 5 rounds and each reports its median
-            n = max(3, args.steps // 2)
+            n = max(20, args.steps)  # iterations per round (each round: every path, in turn)
             fis, us, uds, sers, sps, nols, posts = [], [], [], [], [], [], []
             serial = isinstance(s, LNSite) and not s.rms and s.w.K <= 16384
             on_load = serial and s.on_load_supported()
