@@ -19,6 +19,16 @@ unfused comparators (LayerNorm + GEMM; Softmax + GEMM) run in the same process
 on the same inputs; speedups compare each path timed on its own, back to back.
 `cpu_baseline` times the fp64 oracle on a bounded row sample of the same
 workload on this host's cores and extrapolates by work.
+
+Other workloads (--workload): ln_qkv, causal_softmax_pv, ffn_prefill,
+ffn_decode_t{1,4,16} (LayerNorm -> FFN up-projection, 8192 x 28672), rms_qkv,
+rms_ffn_decode_t1 (RMSNorm, Eq. (6)), swiglu_prefill, swiglu_decode_t1
+(RMSNorm -> gated MLP input), causal_attention (scores formed in the kernel),
+decode_attention, decode_attention_gqa (split keys + merge), small.  Per kernel
+the line also carries the ablations the workload supports: statistics from a
+pre-pass (serial_stats_ms), normalize-on-load without deferral
+(norm_on_load_ms), the post-LN placement (post_ln_ms), the eager dense softmax
+pair (unfused_dense_ms), decode without the key split (single_pass_ms).
 """
 from __future__ import annotations
 
