@@ -46,6 +46,23 @@ def test_head_subsets_equal_full_slices():
     assert torch.equal(part["S"][0], full["S"][2]) and torch.equal(part["V"][1], full["V"][0])
 
 
+def test_decode_head_subsets_and_query_groups():
+    # key/value head h carries query heads h*g .. h*g+g-1, each from its own stream, so a head
+    # subset reproduces the matching slices of the full draw and g = 1 is the plain layout
+    w = I.DecodeAttnWorkload("t", 12, 5, 2, 40, 16, group=3)
+    full = I.make_decode(w)
+    assert full["Q"].shape == (15, 2, 16) and full["K"].shape == (5, 40, 16)
+    part = I.make_decode(w, heads=[4, 1])
+    assert torch.equal(part["Q"][0:3], full["Q"][12:15]) and torch.equal(part["Q"][3:6], full["Q"][3:6])
+    assert torch.equal(part["K"][0], full["K"][4]) and torch.equal(part["V"][1], full["V"][1])
+    w1 = I.DecodeAttnWorkload("t1", 12, 5, 2, 40, 16)
+    assert torch.equal(I.make_decode(w1)["Q"][1], full["Q"][1])  # query head 1 draws stream 1 in both layouts
+    assert not torch.equal(full["Q"][0], full["Q"][1])
+    g = I.ATTN_DECODE_GQA
+    assert (g.BH, g.group, g.Lq, g.Lk, g.d) == (256, 4, 1, 8192, 128)
+    assert g.bytes() == 2.0 * (2 * 256 * 8192 * 128 + 2 * 1024 * 128)
+
+
 def test_ln_distributions():
     w = I.LNWorkload("t", 7, 512, 1024, 256, "f32", outliers=8)
     c = I.make_ln(w)
