@@ -75,12 +75,12 @@ TRAFFIC = {
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
         "fetch_kib": 229642, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
-        "sha256": ("770f55fdcc8ac10033ddd5304423b8b39c3acf5a704feabd6941916fe2c6d8d6",
+        "sha256": ("76dc4fc2b2825ebd51688a01e9472cb45cd21d7dbf8e43ec98ab907f8cf91adf",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 134877, "fetch_scale": 1.99993, "write_kib": 65536, "write_scale": 1.0},
+        "fetch_kib": 134669, "fetch_scale": 1.99993, "write_kib": 65536, "write_scale": 1.0},
     # the split kernel and the merge kernel together (530515 + 145 KiB read, 266 + 64 KiB written)
     ("attention_decode_deferred", "decode_attention_bf16_256x1x8192_d128"): {
-        "sha256": ("770f55fdcc8ac10033ddd5304423b8b39c3acf5a704feabd6941916fe2c6d8d6",
+        "sha256": ("76dc4fc2b2825ebd51688a01e9472cb45cd21d7dbf8e43ec98ab907f8cf91adf",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
         "fetch_kib": 530660, "fetch_scale": 1.99993, "write_kib": 330, "write_scale": 1.0},
 }

@@ -261,6 +261,18 @@ DN_API dn_status attention_deferred(const void* Q, const void* K, const void* V,
                              int dtype, void* out, hipStream_t stream);
 
 /*
+ * attention_deferred with grouped-query attention (as in the Llama 3 models
+ * the paper evaluates): K, V hold BH_kv heads [BH_kv][Lk][d], and Q, out
+ * hold BH_kv * group query heads [BH_kv * group][Lq][d]; query head h reads
+ * key/value head h / group (the group's query heads are consecutive).  Each
+ * query head is computed exactly as by attention_deferred.  group >= 1;
+ * other rules and status codes as attention_deferred.
+ */
+DN_API dn_status attention_gqa_deferred(const void* Q, const void* K, const void* V, int64_t BH_kv,
+                                 int64_t group, int64_t Lq, int64_t Lk, int64_t d, int causal,
+                                 float scale, int dtype, void* out, hipStream_t stream);
+
+/*
  * Decode-shaped attention: Lq <= 16 query rows per head against all Lk keys
  * (the key/value cache holds exactly the visible keys, so no mask).  The keys
  * are cut into ranges, one workgroup each, that leave their un-normalized

@@ -260,22 +260,38 @@ DN_API dn_status softmax_pv_deferred(const void* S, const void* V, int64_t BH, i
     return from_hip(dn::launch_softmax_pv_deferred(S, V, BH, Lq, Lk, d, causal, out, stream));
 }
 
-DN_API dn_status attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq, int64_t Lk,
-                                    int64_t d, int causal, float scale, int dtype, void* out, hipStream_t stream) {
-    if (!Q || !K || !V || !out || BH < 1 || Lq < 1 || Lk < 1 || d < 1 || !valid_dtype(dtype))
+// BH key/value heads, each read by `group` consecutive query heads (group = 1: one each).
+static dn_status attention_grouped(const void* Q, const void* K, const void* V, int64_t BH, int64_t group,
+                                   int64_t Lq, int64_t Lk, int64_t d, int causal, float scale, int dtype, void* out,
+                                   hipStream_t stream) {
+    if (!Q || !K || !V || !out || BH < 1 || group < 1 || Lq < 1 || Lk < 1 || d < 1 || !valid_dtype(dtype))
         return DN_ERR_INVALID_ARG;
     if (causal != 0 && causal != 1) return DN_ERR_INVALID_ARG;
     if (causal && Lq != Lk) return DN_ERR_INVALID_ARG;
     if (!isfinite(scale) || !(scale > 0.f)) return DN_ERR_INVALID_ARG;
-    size_t qb, kb, ob;
-    if (!bytes_of(BH, Lq, d * 2, &qb) || !bytes_of(BH, Lk, d * 2, &kb)) return DN_ERR_INVALID_ARG;
-    ob = qb;
+    int64_t BHq;
+    size_t qb, kb;
+    if (__builtin_mul_overflow(BH, group, &BHq) || !bytes_of(BHq, Lq, d * 2, &qb) || !bytes_of(BH, Lk, d * 2, &kb))
+        return DN_ERR_INVALID_ARG;
+    const size_t ob = qb;
     if (dtype != DN_BF16 || (d != 64 && d != 128)) return DN_ERR_UNSUPPORTED;
     if (Lq * d * 2 >= (int64_t(1) << 31) || Lk * d * 2 >= (int64_t(1) << 31)) return DN_ERR_UNSUPPORTED;
+    if (group > (int64_t(1) << 20)) return DN_ERR_UNSUPPORTED;
     if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16)) return DN_ERR_MISALIGNED;
     if (overlaps(out, ob, Q, qb) || overlaps(out, ob, K, kb) || overlaps(out, ob, V, kb)) return DN_ERR_INVALID_ARG;
-    if (BH * ((Lq + 255) / 256) > kMaxGridX) return DN_ERR_UNSUPPORTED;
-    return from_hip(dn::launch_attention_deferred(Q, K, V, BH, Lq, Lk, d, causal, scale, out, stream));
+    if (BHq * ((Lq + 255) / 256) > kMaxGridX) return DN_ERR_UNSUPPORTED;
+    return from_hip(dn::launch_attention_deferred(Q, K, V, BHq, Lq, Lk, d, causal, scale, out, stream, (int)group));
+}
+
+DN_API dn_status attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq, int64_t Lk,
+                                    int64_t d, int causal, float scale, int dtype, void* out, hipStream_t stream) {
+    return attention_grouped(Q, K, V, BH, 1, Lq, Lk, d, causal, scale, dtype, out, stream);
+}
+
+DN_API dn_status attention_gqa_deferred(const void* Q, const void* K, const void* V, int64_t BH_kv, int64_t group,
+                                        int64_t Lq, int64_t Lk, int64_t d, int causal, float scale, int dtype,
+                                        void* out, hipStream_t stream) {
+    return attention_grouped(Q, K, V, BH_kv, group, Lq, Lk, d, causal, scale, dtype, out, stream);
 }
 
 DN_API size_t attention_decode_workspace_bytes(int64_t BH, int64_t Lq, int64_t Lk, int64_t d) {

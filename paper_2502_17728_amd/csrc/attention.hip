@@ -86,7 +86,7 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
                                                             const __bf16* __restrict__ V, int64_t Lq,
                                                             int64_t Lk, int causal, float sl2, int nqb,
                                                             int nsplit, int64_t kchunk, float* __restrict__ part,
-                                                            __bf16* __restrict__ out) {
+                                                            __bf16* __restrict__ out, int group) {
     using namespace fa;
     constexpr int BQ = NW * QW * 16;   // queries per workgroup
     constexpr int NKB = BKV / 16;      // 16-key S^T blocks per step
@@ -120,8 +120,9 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
     const int nsteps = (int)((k_hi - k_lo + BKV - 1) / BKV);
 
     const __bf16* Qh = Q + (int64_t)h * Lq * D;
-    const __bf16* Kh = K + (int64_t)h * Lk * D;
-    const __bf16* Vh = V + (int64_t)h * Lk * D;
+    // grouped-query attention: query head h reads key/value head h / group
+    const __bf16* Kh = K + (int64_t)(h / group) * Lk * D;
+    const __bf16* Vh = V + (int64_t)(h / group) * Lk * D;
     __bf16* Oh = out + (int64_t)h * Lq * D;
 
     const int64_t qw0 = q0 + wave * QW * 16;  // first query of this wave
@@ -345,12 +346,12 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
 
 template <int D, int NW, int QW, int NS, int BKV>
 static hipError_t run_attention(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq, int64_t Lk,
-                                int causal, float scale, void* out, hipStream_t s) {
+                                int causal, float scale, void* out, hipStream_t s, int group) {
     constexpr int BQ = NW * QW * 16;
     const int nqb = (int)((Lq + BQ - 1) / BQ);
     attention_kernel<D, NW, QW, NS, BKV><<<dim3((unsigned)(BH * nqb)), NW * 64, 0, s>>>(
         (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, causal, scale * fa::kLog2e, nqb, 1, Lk,
-        nullptr, (__bf16*)out);
+        nullptr, (__bf16*)out, group);
     return hipGetLastError();
 }
 
@@ -410,12 +411,12 @@ static hipError_t run_attention_decode(const void* Q, const void* K, const void*
     if (nsplit == 1) {  // enough heads to fill the chip: one pass, the division in the kernel's epilogue
         attention_kernel<D, 1, 1, kDecNS, kDecBKV><<<dim3((unsigned)BH), 64, 0, s>>>(
             (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, 0, scale * fa::kLog2e, 1, 1, Lk,
-            nullptr, (__bf16*)out);
+            nullptr, (__bf16*)out, 1);
         return hipGetLastError();
     }
     attention_kernel<D, 1, 1, kDecNS, kDecBKV><<<dim3((unsigned)(BH * nsplit)), 64, 0, s>>>(
         (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, 0, scale * fa::kLog2e, 1, nsplit, kchunk,
-        part, nullptr);
+        part, nullptr, 1);
     const int64_t rows = BH * Lq;
     attention_merge_kernel<D><<<dim3((unsigned)((rows + 3) / 4)), 256, 0, s>>>(part, nsplit, rows, (__bf16*)out);
     return hipGetLastError();
@@ -435,12 +436,13 @@ hipError_t launch_attention_decode(const void* Q, const void* K, const void* V, 
 }
 
 hipError_t launch_attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,
-                                     int64_t Lk, int64_t d, int causal, float scale, void* out, hipStream_t s) {
+                                     int64_t Lk, int64_t d, int causal, float scale, void* out, hipStream_t s,
+                                     int group) {
     // 8 waves x 2 query fragments (256 queries per workgroup), two ring slots of 128 keys
     // (128 KiB of LDS at d = 128): measured fastest against 64-key steps, 3 slots, 1 or 3
-    // fragments, and 4 waves on the causal 32 x 8192 x 8192, d = 128
-    if (d == 64) return run_attention<64, 8, 2, 2, 128>(Q, K, V, BH, Lq, Lk, causal, scale, out, s);
-    return run_attention<128, 8, 2, 2, 128>(Q, K, V, BH, Lq, Lk, causal, scale, out, s);
+    // fragments, and 4 waves on the causal 32 x 8192 x 8192, d = 128.  BH counts query heads.
+    if (d == 64) return run_attention<64, 8, 2, 2, 128>(Q, K, V, BH, Lq, Lk, causal, scale, out, s, group);
+    return run_attention<128, 8, 2, 2, 128>(Q, K, V, BH, Lq, Lk, causal, scale, out, s, group);
 }
 
 }  // namespace dn

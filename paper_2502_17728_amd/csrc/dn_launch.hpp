@@ -64,9 +64,11 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
 hipError_t launch_softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq,
                                       int64_t Lk, int64_t d, int causal, void* out, hipStream_t s);
 
-// out[BH][Lq][d] = softmax(scale * Q K^T) V per head, the scores formed in the kernel.
+// out[BH][Lq][d] = softmax(scale * Q K^T) V per query head, the scores formed in the kernel;
+// query head h reads key/value head h / group (K, V hold BH / group heads).
 hipError_t launch_attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,
-                                     int64_t Lk, int64_t d, int causal, float scale, void* out, hipStream_t s);
+                                     int64_t Lk, int64_t d, int causal, float scale, void* out, hipStream_t s,
+                                     int group = 1);
 
 // Decode attention (Lq <= 16, all Lk keys visible): key ranges split over workgroups
 // (partials in `workspace`, attention_decode_workspace_bytes of them), then one merge;

@@ -25,7 +25,8 @@ SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linea
            "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered", "ln_linear_serial",
            "ln_linear_norm_on_load", "ln_linear_deferred_post", "rms_linear_deferred_post",
            "swiglu_packed_bytes", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
-           "attention_deferred", "attention_decode_workspace_bytes", "attention_decode_deferred", "layernorm",
+           "attention_deferred", "attention_gqa_deferred", "attention_decode_workspace_bytes",
+           "attention_decode_deferred", "layernorm",
            "rmsnorm", "silu_mul", "softmax", "gemm")
 
 
@@ -66,6 +67,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.silu_mul.argtypes = [vp, vp, i64, i32, vp, vp]
     lib.softmax_pv_deferred.argtypes = [vp, vp, i64, i64, i64, i64, i32, i32, vp, vp]
     lib.attention_deferred.argtypes = [vp, vp, vp, i64, i64, i64, i64, i32, f32, i32, vp, vp]
+    lib.attention_gqa_deferred.argtypes = [vp, vp, vp, i64, i64, i64, i64, i64, i32, f32, i32, vp, vp]
     lib.attention_decode_workspace_bytes.argtypes = [i64, i64, i64, i64]
     lib.attention_decode_workspace_bytes.restype = ctypes.c_size_t
     lib.attention_decode_deferred.argtypes = [vp, vp, vp, i64, i64, i64, i64, f32, i32, vp, ctypes.c_size_t, vp, vp]
@@ -76,7 +78,8 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered",
               "ln_linear_serial", "ln_linear_norm_on_load", "ln_linear_deferred_post",
               "rms_linear_deferred_post", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
-              "attention_deferred", "attention_decode_deferred", "layernorm", "rmsnorm", "silu_mul", "softmax",
+              "attention_deferred", "attention_gqa_deferred", "attention_decode_deferred", "layernorm", "rmsnorm",
+              "silu_mul", "softmax",
               "gemm"):
         getattr(lib, f).restype = i32
     return lib
@@ -282,18 +285,28 @@ def softmax_pv_deferred(S: torch.Tensor, V: torch.Tensor, causal: bool = False,
 def attention_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, causal: bool = False,
                        scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
                        stream=None) -> torch.Tensor:
-    """softmax(scale * Q K^T) V per head; Q[BH, Lq, d], K/V[BH, Lk, d]; scale defaults to 1/sqrt(d)."""
-    BH, Lq, d = Q.shape
-    Lk = K.shape[1]
-    if tuple(K.shape) != (BH, Lk, d) or tuple(V.shape) != (BH, Lk, d):
-        raise ValueError("K and V must be [BH, Lk, d] like Q")
+    """softmax(scale * Q K^T) V per query head; scale defaults to 1/sqrt(d).
+
+    Q[BH * g, Lq, d], K/V[BH, Lk, d]: g = 1 is one key/value head per query head; g > 1 is
+    grouped-query attention, query head h reading key/value head h // g.
+    """
+    BHq, Lq, d = Q.shape
+    BH, Lk = K.shape[0], K.shape[1]
+    if K.shape[2] != d or tuple(V.shape) != tuple(K.shape) or BHq % BH:
+        raise ValueError("K and V must be [BH, Lk, d] with the query heads a multiple of BH")
+    g = BHq // BH
     if scale is None:
         scale = 1.0 / float(d) ** 0.5
     if out is None:
         out = torch.empty_like(Q)
-    _check("attention_deferred", _lib.attention_deferred(
-        _dev(Q, "Q"), _dev(K, "K"), _dev(V, "V"), BH, Lq, Lk, d, int(causal), float(scale), _dt(Q),
-        _dev(out, "out"), _stream(stream)))
+    if g == 1:
+        st = _lib.attention_deferred(_dev(Q, "Q"), _dev(K, "K"), _dev(V, "V"), BH, Lq, Lk, d, int(causal),
+                                     float(scale), _dt(Q), _dev(out, "out"), _stream(stream))
+        _check("attention_deferred", st)
+    else:
+        st = _lib.attention_gqa_deferred(_dev(Q, "Q"), _dev(K, "K"), _dev(V, "V"), BH, g, Lq, Lk, d, int(causal),
+                                         float(scale), _dt(Q), _dev(out, "out"), _stream(stream))
+        _check("attention_gqa_deferred", st)
     return out
 
 

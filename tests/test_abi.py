@@ -186,6 +186,17 @@ def test_attention_deferred_validation():
     assert f(P, P2, P3, 1, 64, 64, 64, 0, 0.125, 1, P + 64, None) == INVALID              # out overlaps Q
 
 
+def test_attention_gqa_validation():
+    f = ops._lib.attention_gqa_deferred
+    O = P + (1 << 33)
+    assert f(P, P2, P3, 2, 0, 64, 64, 128, 1, 0.1, 1, O, None) == INVALID        # group >= 1
+    assert f(P, P2, P3, 2, 4, 64, 32, 128, 1, 0.1, 1, O, None) == INVALID        # causal needs Lq == Lk
+    assert f(P, P2, P3, 1 << 40, 1 << 40, 64, 64, 128, 0, 0.1, 1, O, None) == INVALID  # head count overflow
+    assert f(P, P2, P3, 2, 4, 64, 64, 96, 0, 0.1, 1, O, None) == UNSUPPORTED
+    assert f(P, P2, P3, 2, 4, 64, 64, 128, 0, 0.1, 1, O + 8, None) == MISALIGNED
+    assert f(P, P2, P3, 2, 4, 64, 64, 128, 0, 0.1, 1, P + 4096, None) == INVALID  # out overlaps Q (8 heads)
+
+
 def test_attention_decode_validation():
     f, wb = ops._lib.attention_decode_deferred, ops._lib.attention_decode_workspace_bytes
     assert wb(32, 1, 8192, 128) > 0

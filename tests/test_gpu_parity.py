@@ -523,6 +523,23 @@ def test_attention_cross_lengths(ops, Lq, Lk, d):
     _attn_check(ops, dict(Q=a["Q"], K=b["K"], V=b["V"], causal=False, scale=a["scale"]))
 
 
+@pytest.mark.parametrize("BH,g,Lq,Lk,d,causal", [(2, 4, 300, 300, 128, True), (3, 2, 100, 520, 64, False),
+                                                 (1, 8, 260, 260, 64, True)])
+def test_attention_grouped_query(ops, BH, g, Lq, Lk, d, causal):
+    # grouped-query attention: g consecutive query heads read one key/value head
+    q = I.make_qkv_case(BH * g, Lq, d, causal, seed=Lq + g)["Q"]
+    kv = I.make_qkv_case(BH, Lk, d, causal, seed=Lk + 3)
+    scale = 1.0 / d ** 0.5
+    out = ops.attention_deferred(cuda(q), cuda(kv["K"]), cuda(kv["V"]), causal=causal, scale=scale)
+    torch.cuda.synchronize()
+    rows = np.arange(BH * g * Lq)
+    qh, pos = rows // Lq, rows % Lq
+    ref = oracle.attention(q.reshape(-1, d), kv["K"], kv["V"], scale, head=qh // g, qpos=pos if causal else None)
+    err = rowwise_rel_err(out.cpu().reshape(-1, d), ref)
+    print(f"attention GQA Q{tuple(q.shape)} K{tuple(kv['K'].shape)} causal={causal}: err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
+
+
 def test_attention_matches_softmax_pv_on_materialized_scores(ops):
     # the same workload through S = Q K^T / sqrt(d) stored in bf16 and softmax_pv_deferred:
     # the two differ only by the rounding of S to bf16
