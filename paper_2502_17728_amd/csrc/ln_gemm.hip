@@ -740,7 +740,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
 }
 
 // =============================================================================
-// Decode-shaped deferred LN -> Linear: M <= 16 tokens, bf16.
+// Decode-shaped deferred LN -> Linear: M <= 64 tokens, bf16.
 // The work is streaming W' from HBM.  Each workgroup owns NC blocks of 16
 // output columns and its KS waves split K; per 32-k chunk a wave reads the
 // (zero-padded) x fragment once and NC packed W' chunks straight from HBM into
@@ -754,7 +754,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
 // 2j+1 of the group form output block j), out[M][n_out] = SiLU(gate) * up.
 // PLAIN: the plain product out = x . W' + bias (bias: [N] bf16, nullable), no
 // moments -- the decode-shaped GEMM of the unfused comparators.
-template <int KS, int NC, int U, bool SW = false, bool PLAIN = false>
+template <int KS, int NC, int U, bool SW = false, bool PLAIN = false, int MT = 1>
 __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16* __restrict__ x,
                                                              const char* __restrict__ Wp, int64_t kchunks,
                                                              int64_t nblocks, const float* __restrict__ c_col,
@@ -766,12 +766,20 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
                                                              const __bf16* __restrict__ bias) {
     static_assert(!SW || NC % 2 == 0, "gate/up block pairs");
     static_assert(!(SW && PLAIN), "the plain product has no gate");
-    __shared__ f32x4 part[2 + NC][KS][kWave];
+    // MT fragments of 16 token rows (M <= 16 MT); per fragment the slots hold the moments
+    // (sum x, Gram) and then the NC column blocks' partial products
+    constexpr int SLOTS = 2 + NC;
+    __shared__ f32x4 part[MT * SLOTS][KS][kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t nb0 = (int64_t)blockIdx.x * NC;
     const int row = lane & 15;
-    const bool row_ok = row < M;
-    const __bf16* xr = x + (int64_t)(row_ok ? row : 0) * K;
+    bool row_ok[MT];
+    const __bf16* xr[MT];
+#pragma unroll
+    for (int f = 0; f < MT; ++f) {
+        row_ok[f] = 16 * f + row < M;
+        xr[f] = x + (int64_t)(row_ok[f] ? 16 * f + row : 0) * K;
+    }
     const char* wr[NC];
 #pragma unroll
     for (int q = 0; q < NC; ++q) wr[q] = Wp + packed_chunk(min(nb0 + q, nblocks - 1), 0, kchunks, lane);
@@ -782,9 +790,14 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
 
     const u32x4 ones = {0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
     const u32x4 zero = {0, 0, 0, 0};
-    f32x4 acc[NC], sx = {0.f, 0.f, 0.f, 0.f}, sxx = sx;
+    const f32x4 fz = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[MT][NC], sx[MT], sxx[MT];
 #pragma unroll
-    for (int q = 0; q < NC; ++q) acc[q] = sx;
+    for (int f = 0; f < MT; ++f) {
+        sx[f] = sxx[f] = fz;
+#pragma unroll
+        for (int q = 0; q < NC; ++q) acc[f][q] = fz;
+    }
 
     // Software pipeline over groups of U chunks: the loads of group g + 1 are in
     // flight while group g multiplies.  Every load is unconditional (chunk
@@ -792,8 +805,8 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
     // zeros) so the wait counts stay exact; the group count is rounded up to
     // even and a group wholly past the range adds x = 0 times finite W'.
     const int64_t ngroups = c_end > c_begin ? (c_end - c_begin + U - 1) / U : 0;
-    u32x4 a0[U], b0[U][NC], a1[U], b1[U][NC];
-    auto load = [&](u32x4(&a)[U], u32x4(&b)[U][NC], int64_t g) {
+    u32x4 a0[U][MT], b0[U][NC], a1[U][MT], b1[U][NC];
+    auto load = [&](u32x4(&a)[U][MT], u32x4(&b)[U][NC], int64_t g) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t cc = c_begin + g * U + u;
@@ -802,20 +815,25 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
             const int64_t kk = cl * 32 + (lane >> 4) * 8;
 #pragma unroll
             for (int q = 0; q < NC; ++q) b[u][q] = ld16(wr[q] + cl * kWave * 16);  // zero-padded past K
-            const u32x4 xv = ld16(xr + min(kk, K - 8));                              // K % 8 == 0
-            a[u] = (ok && kk < K && row_ok) ? xv : zero;
-        }
-    };
-    auto compute = [&](const u32x4(&a)[U], const u32x4(&b)[U][NC]) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-#pragma unroll
-            for (int q = 0; q < NC; ++q) acc[q] = mfma_chunk<__bf16>(a[u], b[u][q], acc[q]);
-            if constexpr (!PLAIN) {
-                sx = mfma_chunk<__bf16>(a[u], ones, sx);
-                sxx = mfma_chunk<__bf16>(a[u], a[u], sxx);
+            for (int f = 0; f < MT; ++f) {
+                const u32x4 xv = ld16(xr[f] + min(kk, K - 8));  // K % 8 == 0
+                a[u][f] = (ok && kk < K && row_ok[f]) ? xv : zero;
             }
         }
+    };
+    auto compute = [&](const u32x4(&a)[U][MT], const u32x4(&b)[U][NC]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int f = 0; f < MT; ++f) {
+#pragma unroll
+                for (int q = 0; q < NC; ++q) acc[f][q] = mfma_chunk<__bf16>(a[u][f], b[u][q], acc[f][q]);
+                if constexpr (!PLAIN) {
+                    sx[f] = mfma_chunk<__bf16>(a[u][f], ones, sx[f]);
+                    sxx[f] = mfma_chunk<__bf16>(a[u][f], a[u][f], sxx[f]);
+                }
+            }
     };
     if (ngroups > 0) {
         load(a0, b0, 0);
@@ -827,60 +845,68 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
         }
     }
 #pragma unroll
-    for (int q = 0; q < NC; ++q) part[2 + q][wave][lane] = acc[q];
-    part[0][wave][lane] = sx;
-    part[1][wave][lane] = sxx;
+    for (int f = 0; f < MT; ++f) {
+#pragma unroll
+        for (int q = 0; q < NC; ++q) part[f * SLOTS + 2 + q][wave][lane] = acc[f][q];
+        part[f * SLOTS][wave][lane] = sx[f];
+        part[f * SLOTS + 1][wave][lane] = sxx[f];
+    }
     __syncthreads();
-    // Column block j of the workgroup (SW: block pair j, gate then up): reduce over
-    // the KS slices of K, then the epilogue.
+    // Column block j of the workgroup (SW: block pair j, gate then up) and row
+    // fragment f: reduce over the KS slices of K, then the epilogue.
     constexpr int NOUT = SW ? NC / 2 : NC;
     for (int j = wave; j < NOUT && nb0 + (SW ? 2 * j : j) < nblocks; j += KS) {
         const int q0 = SW ? 2 * j : j;
-        f32x4 tot[4];  // block q0, the moments, block q0 + 1 (SW)
-#pragma unroll
-        for (int w = 0; w < KS; ++w) {
-            const f32x4 a0 = part[2 + q0][w][lane], a1 = part[0][w][lane], a2 = part[1][w][lane];
-            tot[0] = w ? tot[0] + a0 : a0;
-            tot[1] = w ? tot[1] + a1 : a1;
-            tot[2] = w ? tot[2] + a2 : a2;
-            if constexpr (SW) tot[3] = w ? tot[3] + part[3 + q0][w][lane] : part[3 + q0][w][lane];
-        }
-        // Gram diagonal (r, r) sits in lane r + 16*(r>>2), element r&3.  This lane's
-        // rows are r = 4*(l>>4) + i, so the source lane is 20*(l>>4) + i.
-        float diag[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) diag[i] = __shfl(tot[2][i], 20 * (lane >> 4) + i);
         const int64_t col = (nb0 + q0) * 16 + (lane & 15);
         const int64_t n = min(col, N - 1), nu = min(col + 16, N - 1);
-        if constexpr (PLAIN) {
-            const float bn = bias ? (float)bias[n] : 0.f;
+#pragma unroll
+        for (int f = 0; f < MT; ++f) {
+            if (16 * f >= M) break;
+            const int sb = f * SLOTS;
+            f32x4 tot[4];  // block q0, the moments, block q0 + 1 (SW)
+#pragma unroll
+            for (int w = 0; w < KS; ++w) {
+                const f32x4 v0 = part[sb + 2 + q0][w][lane], v1 = part[sb][w][lane], v2 = part[sb + 1][w][lane];
+                tot[0] = w ? tot[0] + v0 : v0;
+                tot[1] = w ? tot[1] + v1 : v1;
+                tot[2] = w ? tot[2] + v2 : v2;
+                if constexpr (SW) tot[3] = w ? tot[3] + part[sb + 3 + q0][w][lane] : part[sb + 3 + q0][w][lane];
+            }
+            if constexpr (PLAIN) {
+                const float bn = bias ? (float)bias[n] : 0.f;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int r = 16 * f + 4 * (lane >> 4) + i;
+                    if (r < M && col < N) out[(int64_t)r * N + col] = (__bf16)(tot[0][i] + bn);
+                }
+                continue;
+            }
+            // Gram diagonal (r, r) sits in lane r + 16*(r>>2), element r&3.  This lane's
+            // rows are r = 4*(l>>4) + i of the fragment, so the source lane is 20*(l>>4) + i.
+            float diag[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) diag[i] = __shfl(tot[2][i], 20 * (lane >> 4) + i);
+            const float cn = c_col[n], bn = b_col[n];
+            const float cu = SW ? c_col[nu] : 0.f, bu = SW ? b_col[nu] : 0.f;
+            const int64_t o = SW ? (nb0 / 2 + j) * 16 + (lane & 15) : col;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int r = 4 * (lane >> 4) + i;
-                if (r < M && col < N) out[(int64_t)r * N + col] = (__bf16)(tot[0][i] + bn);
+                const int r = 16 * f + 4 * (lane >> 4) + i;
+                float mean = rms ? 0.f : tot[1][i] / (float)K;
+                const float var = __builtin_fmaxf(diag[i] / (float)K - mean * mean, 0.f);
+                float rstd = 1.0f / __builtin_sqrtf(var + eps);
+                if (row_stats) {  // serial ablation (the moment products above are then unused)
+                    mean = row_stats[2 * min(r, M - 1)];
+                    rstd = row_stats[2 * min(r, M - 1) + 1];
+                }
+                if (stats_out && blockIdx.x == 0 && j == 0 && (lane & 15) == 0 && r < M) {
+                    stats_out[2 * r] = mean;  // the first column block's lanes export them, once per row
+                    stats_out[2 * r + 1] = rstd;
+                }
+                float v = __builtin_fmaf(rstd, __builtin_fmaf(-mean, cn, tot[0][i]), bn);
+                if constexpr (SW) v = silu(v) * __builtin_fmaf(rstd, __builtin_fmaf(-mean, cu, tot[3][i]), bu);
+                if (r < M && o < n_out) out[(int64_t)r * n_out + o] = (__bf16)v;
             }
-            continue;
-        }
-        const float cn = c_col[n], bn = b_col[n];
-        const float cu = SW ? c_col[nu] : 0.f, bu = SW ? b_col[nu] : 0.f;
-        const int64_t o = SW ? (nb0 / 2 + j) * 16 + (lane & 15) : col;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = 4 * (lane >> 4) + i;
-            float mean = rms ? 0.f : tot[1][i] / (float)K;
-            const float var = __builtin_fmaxf(diag[i] / (float)K - mean * mean, 0.f);
-            float rstd = 1.0f / __builtin_sqrtf(var + eps);
-            if (row_stats) {  // serial ablation (the moment products above are then unused)
-                mean = row_stats[2 * min(r, M - 1)];
-                rstd = row_stats[2 * min(r, M - 1) + 1];
-            }
-            if (stats_out && blockIdx.x == 0 && j == 0 && (lane & 15) == 0 && r < M) {
-                stats_out[2 * r] = mean;  // the first column block's lanes export them, once per row
-                stats_out[2 * r + 1] = rstd;
-            }
-            float v = __builtin_fmaf(rstd, __builtin_fmaf(-mean, cn, tot[0][i]), bn);
-            if constexpr (SW) v = silu(v) * __builtin_fmaf(rstd, __builtin_fmaf(-mean, cu, tot[3][i]), bu);
-            if (r < M && o < n_out) out[(int64_t)r * n_out + o] = (__bf16)v;
         }
     }
 }
@@ -1091,18 +1117,31 @@ static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_
 // for the partial sums).  Measured on the 8192 x 28672 up-projection (1792
 // blocks, nc = 7): 78.5-78.8 us for 1-16 tokens, against 81-91 us for the
 // 4- and 8-wave layouts with 1-4 blocks per workgroup.
-template <bool PLAIN, class F>
-static void decode_dispatch(int64_t nblocks, F&& launch) {
-    const int64_t nc = std::min<int64_t>(7, std::max<int64_t>(1, (nblocks + 255) / 256));
+template <bool PLAIN, int MT, int KS, int U, class F>
+static void decode_dispatch_nc(int64_t nc, F&& launch) {
     switch (nc) {
-        case 1: launch(ln_decode_bf16_kernel<16, 1, 1, false, PLAIN>, 16, 1); break;
-        case 2: launch(ln_decode_bf16_kernel<16, 2, 1, false, PLAIN>, 16, 2); break;
-        case 3: launch(ln_decode_bf16_kernel<16, 3, 1, false, PLAIN>, 16, 3); break;
-        case 4: launch(ln_decode_bf16_kernel<16, 4, 1, false, PLAIN>, 16, 4); break;
-        case 5: launch(ln_decode_bf16_kernel<16, 5, 1, false, PLAIN>, 16, 5); break;
-        case 6: launch(ln_decode_bf16_kernel<16, 6, 1, false, PLAIN>, 16, 6); break;
-        default: launch(ln_decode_bf16_kernel<16, 7, 1, false, PLAIN>, 16, 7); break;
+        case 1: launch(ln_decode_bf16_kernel<KS, 1, U, false, PLAIN, MT>, KS, 1); break;
+        case 2: launch(ln_decode_bf16_kernel<KS, 2, U, false, PLAIN, MT>, KS, 2); break;
+        case 3: launch(ln_decode_bf16_kernel<KS, 3, U, false, PLAIN, MT>, KS, 3); break;
+        case 4: launch(ln_decode_bf16_kernel<KS, 4, U, false, PLAIN, MT>, KS, 4); break;
+        case 5: launch(ln_decode_bf16_kernel<KS, 5, U, false, PLAIN, MT>, KS, 5); break;
+        case 6: launch(ln_decode_bf16_kernel<KS, 6, U, false, PLAIN, MT>, KS, 6); break;
+        default: launch(ln_decode_bf16_kernel<KS, 7, U, false, PLAIN, MT>, KS, 7); break;
     }
+}
+template <bool PLAIN, class F>
+static void decode_dispatch(int64_t M, int64_t nblocks, F&& launch) {
+    const int64_t nc = std::min<int64_t>(7, std::max<int64_t>(1, (nblocks + 255) / 256));
+    // 17-64 tokens: 2-4 row fragments per wave; 4 waves split K (the partial sums of
+    // 4 fragments x 9 slots x 4 waves fill 144 KiB of LDS at nc = 7)
+    if (M <= 16)
+        decode_dispatch_nc<PLAIN, 1, 16, 1>(nc, launch);
+    else if (M <= 32)
+        decode_dispatch_nc<PLAIN, 2, 4, 2>(nc, launch);
+    else if (M <= 48)
+        decode_dispatch_nc<PLAIN, 3, 4, 2>(nc, launch);
+    else
+        decode_dispatch_nc<PLAIN, 4, 4, 2>(nc, launch);
 }
 
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
@@ -1113,14 +1152,14 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
     a.rms = rms;
     a.row_stats = row_stats;
     a.stats_out = stats_out;
-    if (dtype == 1 && M <= 16) {
+    if (dtype == 1 && M <= 64) {
         auto launch = [&](auto kern, int ks, int cols) {
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks,
                                                             a.nblocks, a.c_col, a.b_col, (int)M, K, N, eps, rms,
                                                             N, a.row_stats, a.stats_out, (__bf16*)out, nullptr);
         };
-        decode_dispatch<false>(a.nblocks, launch);
+        decode_dispatch<false>(M, a.nblocks, launch);
         return hipGetLastError();
     }
     if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
@@ -1146,7 +1185,7 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
     a.eps = eps;
     a.rms = rms;
     a.n_out = N;
-    if (dtype == 1 && M <= 16) {
+    if (dtype == 1 && M <= 64) {
         auto launch = [&](auto kern, int ks, int cols) {
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks, a.nblocks,
@@ -1155,7 +1194,14 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
         };
         // one gate/up block pair per workgroup, 4 K-slices, 2-chunk groups: measured
         // flat at 69 % of HBM for 1-16 tokens on the 8192 x 2 x 28672 weights
-        launch(ln_decode_bf16_kernel<4, 2, 2, true>, 4, 2);
+        if (M <= 16)
+            launch(ln_decode_bf16_kernel<4, 2, 2, true>, 4, 2);
+        else if (M <= 32)
+            launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 2>, 4, 2);
+        else if (M <= 48)
+            launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 3>, 4, 2);
+        else
+            launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 4>, 4, 2);
         return hipGetLastError();
     }
     if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kSwiGlu>(a, 1, s);
@@ -1182,7 +1228,7 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
     a.bias = bias;
     a.a_causal = a_causal;
     if (b_layout == 2) {
-        if (dtype == 1 && M <= 16) {
+        if (dtype == 1 && M <= 64) {
             // decode shapes: the streaming kernel of the deferred path without its moments,
             // in the same layouts (so the unfused comparison is like for like)
             auto launch = [&](auto kern, int ks, int cols) {
@@ -1192,7 +1238,7 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
                                                                 N, nullptr, nullptr, (__bf16*)C,
                                                                 (const __bf16*)bias);
             };
-            decode_dispatch<true>(a.nblocks, launch);
+            decode_dispatch<true>(M, a.nblocks, launch);
             return hipGetLastError();
         }
         if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);

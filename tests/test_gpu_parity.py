@@ -59,10 +59,10 @@ def test_ln_linear_bf16_ragged(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M + K))
 
 
-# token counts on both sides of each decode-layout switch (4 | 5..8 | 9..16);
-# K = 8 leaves three of four K-slices empty, N = 24 / 520 leave a partial
-# group of column blocks
-@pytest.mark.parametrize("M", [1, 3, 4, 5, 8, 9, 16])
+# token counts on both sides of each decode-layout switch (16 | 17..32 | 33..48 |
+# 49..64 | 65 = the tiled kernels), partial row fragments; K = 8 leaves most
+# K-slices empty, N = 24 / 520 leave a partial group of column blocks
+@pytest.mark.parametrize("M", [1, 3, 4, 5, 8, 9, 16, 17, 32, 33, 48, 49, 63, 64, 65])
 @pytest.mark.parametrize("K,N", [(1024, 520), (8200, 64), (8, 24)])
 def test_ln_linear_bf16_decode_shapes(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M * 7 + 1, outliers=4))
@@ -112,7 +112,8 @@ def test_gemm_sampled(ops, M, K, N, layout):
     assert rowwise_rel_err(C.cpu()[torch.as_tensor(rows)], ref) <= TOL[torch.bfloat16]
 
 
-@pytest.mark.parametrize("M,K,N", [(1, 1024, 520), (5, 8200, 264), (16, 512, 72), (3, 8, 8)])
+@pytest.mark.parametrize("M,K,N", [(1, 1024, 520), (5, 8200, 264), (16, 512, 72), (3, 8, 8), (17, 1024, 520),
+                                   (40, 2048, 264), (64, 512, 4104)])
 def test_gemm_packed_decode(ops, M, K, N):
     # decode shapes with packed weights: the streaming kernel without moments (the unfused
     # comparators' GEMM at M <= 16), bias added once; ragged N and K
@@ -199,7 +200,7 @@ def test_centered_weight_loses_accuracy_on_offset_rows(ops):
 
 
 @pytest.mark.parametrize("M,K,N,dtype", [(37, 104, 72, "f32"), (257, 1024, 264, "bf16"), (3, 1024, 520, "bf16"),
-                                         (12, 8200, 64, "bf16"), (4000, 544, 4104, "bf16")])
+                                         (12, 8200, 64, "bf16"), (45, 1024, 264, "bf16"), (4000, 544, 4104, "bf16")])
 def test_ln_linear_serial_stats(ops, M, K, N, dtype):
     # statistics from a pre-pass kernel, then the same product and deferred epilogue
     case = I.make_ln_case(M, K, N, dtype, seed=M + 4, outliers=2)
@@ -254,7 +255,8 @@ def test_ln_linear_norm_on_load_rejects_small_shapes(ops):
 
 
 @pytest.mark.parametrize("M,K,N,dtype,norm", [(37, 104, 72, "f32", "layernorm"), (257, 1024, 264, "bf16", "layernorm"),
-                                              (5, 1024, 520, "bf16", "layernorm"), (4104, 320, 4096, "bf16", "layernorm"),
+                                              (5, 1024, 520, "bf16", "layernorm"), (50, 1024, 520, "bf16", "layernorm"),
+                                              (4104, 320, 4096, "bf16", "layernorm"),
                                               (300, 512, 200, "bf16", "rms"), (3, 8200, 64, "bf16", "rms")])
 def test_linear_deferred_post(ops, M, K, N, dtype, norm):
     # post-LN placement: the deferred product and the normalized rows (the residual branch) from
@@ -308,7 +310,7 @@ def test_rms_linear_bf16_ragged(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M + K + 1, norm="rms"))
 
 
-@pytest.mark.parametrize("M", [1, 5, 16])
+@pytest.mark.parametrize("M", [1, 5, 16, 20, 40, 64])
 @pytest.mark.parametrize("K,N", [(1024, 520), (8, 24)])
 def test_rms_linear_bf16_decode_shapes(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M * 5 + 2, outliers=4, norm="rms"))
@@ -371,10 +373,10 @@ def test_rms_swiglu_bf16_ragged(ops, M, K, N):
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M + K, outliers=2))
 
 
-@pytest.mark.parametrize("M", [1, 8, 9, 16])
+@pytest.mark.parametrize("M", [1, 8, 9, 16, 17, 48, 64])
 @pytest.mark.parametrize("K,N", [(1024, 520), (8, 24)])
 def test_rms_swiglu_bf16_decode_shapes(ops, M, K, N):
-    # 5-8 tokens: gate/up pairs per workgroup; 9-16: two pairs; N = 520 / 24 leave a partial pair group
+    # one gate/up pair per workgroup, 1-4 row fragments; N = 520 / 24 leave a partial pair group
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M * 3 + 1, outliers=4))
 
 
