@@ -740,7 +740,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
 }
 
 // =============================================================================
-// Decode-shaped deferred LN -> Linear: M <= 64 tokens, bf16.
+// Decode-shaped deferred LN -> Linear: M <= 128 tokens, bf16.
 // The work is streaming W' from HBM.  Each workgroup owns NC blocks of 16
 // output columns and its KS waves split K; per 32-k chunk a wave reads the
 // (zero-padded) x fragment once and NC packed W' chunks straight from HBM into
@@ -766,10 +766,11 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
                                                              const __bf16* __restrict__ bias) {
     static_assert(!SW || NC % 2 == 0, "gate/up block pairs");
     static_assert(!(SW && PLAIN), "the plain product has no gate");
-    // MT fragments of 16 token rows (M <= 16 MT); per fragment the slots hold the moments
-    // (sum x, Gram) and then the NC column blocks' partial products
+    // MT fragments of 16 token rows (M <= 16 MT), reduced one fragment at a time; the
+    // slots hold the fragment's moments (sum x, Gram) and then the NC column blocks'
+    // partial products
     constexpr int SLOTS = 2 + NC;
-    __shared__ f32x4 part[MT * SLOTS][KS][kWave];
+    __shared__ f32x4 part[SLOTS][KS][kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t nb0 = (int64_t)blockIdx.x * NC;
     const int row = lane & 15;
@@ -844,33 +845,30 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
             compute(a1, b1);
         }
     }
+    // Row fragment f and column block j of the workgroup (SW: block pair j, gate
+    // then up): reduce over the KS slices of K, then the epilogue.
+    constexpr int NOUT = SW ? NC / 2 : NC;
 #pragma unroll
     for (int f = 0; f < MT; ++f) {
+        if (16 * f >= M) break;  // uniform over the workgroup
+        if (f) __syncthreads();  // the previous fragment's partial sums have been read
 #pragma unroll
-        for (int q = 0; q < NC; ++q) part[f * SLOTS + 2 + q][wave][lane] = acc[f][q];
-        part[f * SLOTS][wave][lane] = sx[f];
-        part[f * SLOTS + 1][wave][lane] = sxx[f];
-    }
-    __syncthreads();
-    // Column block j of the workgroup (SW: block pair j, gate then up) and row
-    // fragment f: reduce over the KS slices of K, then the epilogue.
-    constexpr int NOUT = SW ? NC / 2 : NC;
-    for (int j = wave; j < NOUT && nb0 + (SW ? 2 * j : j) < nblocks; j += KS) {
-        const int q0 = SW ? 2 * j : j;
-        const int64_t col = (nb0 + q0) * 16 + (lane & 15);
-        const int64_t n = min(col, N - 1), nu = min(col + 16, N - 1);
-#pragma unroll
-        for (int f = 0; f < MT; ++f) {
-            if (16 * f >= M) break;
-            const int sb = f * SLOTS;
+        for (int q = 0; q < NC; ++q) part[2 + q][wave][lane] = acc[f][q];
+        part[0][wave][lane] = sx[f];
+        part[1][wave][lane] = sxx[f];
+        __syncthreads();
+        for (int j = wave; j < NOUT && nb0 + (SW ? 2 * j : j) < nblocks; j += KS) {
+            const int q0 = SW ? 2 * j : j;
+            const int64_t col = (nb0 + q0) * 16 + (lane & 15);
+            const int64_t n = min(col, N - 1), nu = min(col + 16, N - 1);
             f32x4 tot[4];  // block q0, the moments, block q0 + 1 (SW)
 #pragma unroll
             for (int w = 0; w < KS; ++w) {
-                const f32x4 v0 = part[sb + 2 + q0][w][lane], v1 = part[sb][w][lane], v2 = part[sb + 1][w][lane];
+                const f32x4 v0 = part[2 + q0][w][lane], v1 = part[0][w][lane], v2 = part[1][w][lane];
                 tot[0] = w ? tot[0] + v0 : v0;
                 tot[1] = w ? tot[1] + v1 : v1;
                 tot[2] = w ? tot[2] + v2 : v2;
-                if constexpr (SW) tot[3] = w ? tot[3] + part[sb + 3 + q0][w][lane] : part[sb + 3 + q0][w][lane];
+                if constexpr (SW) tot[3] = w ? tot[3] + part[3 + q0][w][lane] : part[3 + q0][w][lane];
             }
             if constexpr (PLAIN) {
                 const float bn = bias ? (float)bias[n] : 0.f;
@@ -1117,31 +1115,39 @@ static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_
 // for the partial sums).  Measured on the 8192 x 28672 up-projection (1792
 // blocks, nc = 7): 78.5-78.8 us for 1-16 tokens, against 81-91 us for the
 // 4- and 8-wave layouts with 1-4 blocks per workgroup.
-template <bool PLAIN, int MT, int KS, int U, class F>
-static void decode_dispatch_nc(int64_t nc, F&& launch) {
-    switch (nc) {
-        case 1: launch(ln_decode_bf16_kernel<KS, 1, U, false, PLAIN, MT>, KS, 1); break;
-        case 2: launch(ln_decode_bf16_kernel<KS, 2, U, false, PLAIN, MT>, KS, 2); break;
-        case 3: launch(ln_decode_bf16_kernel<KS, 3, U, false, PLAIN, MT>, KS, 3); break;
-        case 4: launch(ln_decode_bf16_kernel<KS, 4, U, false, PLAIN, MT>, KS, 4); break;
-        case 5: launch(ln_decode_bf16_kernel<KS, 5, U, false, PLAIN, MT>, KS, 5); break;
-        case 6: launch(ln_decode_bf16_kernel<KS, 6, U, false, PLAIN, MT>, KS, 6); break;
-        default: launch(ln_decode_bf16_kernel<KS, 7, U, false, PLAIN, MT>, KS, 7); break;
-    }
+constexpr int64_t kDecodeMaxRows = 128;
+// Past 64 tokens the streaming kernel re-reads x once per workgroup and stops
+// beating the 128 x 128 tiles once those fill most of the chip: measured at
+// 65-128 tokens, 1.7-2x faster for the 4096 -> 12288 projection (96 tiles),
+// 1.15-1.4x slower for 8192 -> 28672 (224 tiles); the crossover sits near 160.
+static bool decode_rows(int64_t M, int64_t ncols) {
+    if (M <= 64) return true;
+    return M <= kDecodeMaxRows && ((M + 127) / 128) * ((ncols + 127) / 128) < 160;
+}
+template <bool PLAIN, int MT, int KS, int U, int NC, class F>
+static void decode_dispatch_nc(int64_t nc, F&& launch) {  // min(nc, NC) column blocks per workgroup
+    if constexpr (NC > 1)
+        if (nc < NC) return decode_dispatch_nc<PLAIN, MT, KS, U, NC - 1>(nc, launch);
+    launch(ln_decode_bf16_kernel<KS, NC, U, false, PLAIN, MT>, KS, NC);
 }
 template <bool PLAIN, class F>
 static void decode_dispatch(int64_t M, int64_t nblocks, F&& launch) {
     const int64_t nc = std::min<int64_t>(7, std::max<int64_t>(1, (nblocks + 255) / 256));
-    // 17-64 tokens: 2-4 row fragments per wave; 4 waves split K (the partial sums of
-    // 4 fragments x 9 slots x 4 waves fill 144 KiB of LDS at nc = 7)
+    // 17-128 tokens: 2-8 row fragments per wave and 4 (8 at 6 fragments) waves
+    // splitting K; past 4 fragments at most 3 column blocks per workgroup (the
+    // accumulators of 8 fragments x 3 blocks take 96 registers per lane)
     if (M <= 16)
-        decode_dispatch_nc<PLAIN, 1, 16, 1>(nc, launch);
+        decode_dispatch_nc<PLAIN, 1, 16, 1, 7>(nc, launch);
     else if (M <= 32)
-        decode_dispatch_nc<PLAIN, 2, 4, 2>(nc, launch);
+        decode_dispatch_nc<PLAIN, 2, 4, 2, 7>(nc, launch);
     else if (M <= 48)
-        decode_dispatch_nc<PLAIN, 3, 4, 2>(nc, launch);
+        decode_dispatch_nc<PLAIN, 3, 4, 2, 7>(nc, launch);
+    else if (M <= 64)
+        decode_dispatch_nc<PLAIN, 4, 4, 2, 7>(nc, launch);
+    else if (M <= 96)
+        decode_dispatch_nc<PLAIN, 6, 8, 1, 3>(nc, launch);
     else
-        decode_dispatch_nc<PLAIN, 4, 4, 2>(nc, launch);
+        decode_dispatch_nc<PLAIN, 8, 4, 2, 3>(nc, launch);
 }
 
 hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N,
@@ -1152,7 +1158,7 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
     a.rms = rms;
     a.row_stats = row_stats;
     a.stats_out = stats_out;
-    if (dtype == 1 && M <= 64) {
+    if (dtype == 1 && decode_rows(M, N)) {
         auto launch = [&](auto kern, int ks, int cols) {
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks,
@@ -1185,7 +1191,7 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
     a.eps = eps;
     a.rms = rms;
     a.n_out = N;
-    if (dtype == 1 && M <= 64) {
+    if (dtype == 1 && decode_rows(M, np)) {
         auto launch = [&](auto kern, int ks, int cols) {
             const int64_t wgs = (a.nblocks + cols - 1) / cols;
             kern<<<dim3((unsigned)wgs), ks * kWave, 0, s>>>((const __bf16*)x, (const char*)a.B, a.kchunks, a.nblocks,
@@ -1200,8 +1206,12 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
             launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 2>, 4, 2);
         else if (M <= 48)
             launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 3>, 4, 2);
-        else
+        else if (M <= 64)
             launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 4>, 4, 2);
+        else if (M <= 96)
+            launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 6>, 4, 2);
+        else
+            launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 8>, 4, 2);
         return hipGetLastError();
     }
     if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kSwiGlu>(a, 1, s);
@@ -1228,7 +1238,7 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
     a.bias = bias;
     a.a_causal = a_causal;
     if (b_layout == 2) {
-        if (dtype == 1 && M <= 64) {
+        if (dtype == 1 && decode_rows(M, N)) {
             // decode shapes: the streaming kernel of the deferred path without its moments,
             // in the same layouts (so the unfused comparison is like for like)
             auto launch = [&](auto kern, int ks, int cols) {

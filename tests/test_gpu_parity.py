@@ -60,12 +60,19 @@ def test_ln_linear_bf16_ragged(ops, M, K, N):
 
 
 # token counts on both sides of each decode-layout switch (16 | 17..32 | 33..48 |
-# 49..64 | 65 = the tiled kernels), partial row fragments; K = 8 leaves most
-# K-slices empty, N = 24 / 520 leave a partial group of column blocks
-@pytest.mark.parametrize("M", [1, 3, 4, 5, 8, 9, 16, 17, 32, 33, 48, 49, 63, 64, 65])
+# 49..64 | 65..96 | 97..128 | 129 = the tiled kernels), partial row fragments; K = 8
+# leaves most K-slices empty, N = 24 / 520 leave a partial group of column blocks
+@pytest.mark.parametrize("M", [1, 3, 4, 5, 8, 9, 16, 17, 32, 33, 48, 49, 63, 64, 65, 81, 96, 97, 127, 128, 129])
 @pytest.mark.parametrize("K,N", [(1024, 520), (8200, 64), (8, 24)])
 def test_ln_linear_bf16_decode_shapes(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M * 7 + 1, outliers=4))
+
+
+@pytest.mark.parametrize("M,N", [(100, 20352), (100, 20608), (128, 20352)])
+def test_ln_linear_bf16_batched_decode_switch(ops, M, N):
+    # 65-128 tokens take the streaming kernel below 160 tiles of 128 x 128 (159 here) and
+    # the tiled kernel from 160 tiles (161)
+    _ln_check(ops, I.make_ln_case(M, 256, N, "bf16", seed=N % 97, outliers=2))
 
 
 def test_ln_linear_bf16_outliers(ops):
@@ -113,10 +120,10 @@ def test_gemm_sampled(ops, M, K, N, layout):
 
 
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 520), (5, 8200, 264), (16, 512, 72), (3, 8, 8), (17, 1024, 520),
-                                   (40, 2048, 264), (64, 512, 4104)])
+                                   (40, 2048, 264), (64, 512, 4104), (90, 1024, 520), (128, 512, 4104)])
 def test_gemm_packed_decode(ops, M, K, N):
     # decode shapes with packed weights: the streaming kernel without moments (the unfused
-    # comparators' GEMM at M <= 16), bias added once; ragged N and K
+    # comparators' GEMM at M <= 128), bias added once; ragged N and K
     g = torch.Generator().manual_seed(M + K)
     A = torch.randn(M, K, generator=g).to(torch.bfloat16)
     B = (torch.randn(K, N, generator=g) / K ** 0.5).to(torch.bfloat16)
@@ -200,7 +207,8 @@ def test_centered_weight_loses_accuracy_on_offset_rows(ops):
 
 
 @pytest.mark.parametrize("M,K,N,dtype", [(37, 104, 72, "f32"), (257, 1024, 264, "bf16"), (3, 1024, 520, "bf16"),
-                                         (12, 8200, 64, "bf16"), (45, 1024, 264, "bf16"), (4000, 544, 4104, "bf16")])
+                                         (12, 8200, 64, "bf16"), (45, 1024, 264, "bf16"), (100, 1024, 264, "bf16"),
+                                         (4000, 544, 4104, "bf16")])
 def test_ln_linear_serial_stats(ops, M, K, N, dtype):
     # statistics from a pre-pass kernel, then the same product and deferred epilogue
     case = I.make_ln_case(M, K, N, dtype, seed=M + 4, outliers=2)
@@ -310,7 +318,7 @@ def test_rms_linear_bf16_ragged(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M + K + 1, norm="rms"))
 
 
-@pytest.mark.parametrize("M", [1, 5, 16, 20, 40, 64])
+@pytest.mark.parametrize("M", [1, 5, 16, 20, 40, 64, 100, 128])
 @pytest.mark.parametrize("K,N", [(1024, 520), (8, 24)])
 def test_rms_linear_bf16_decode_shapes(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M * 5 + 2, outliers=4, norm="rms"))
@@ -373,10 +381,10 @@ def test_rms_swiglu_bf16_ragged(ops, M, K, N):
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M + K, outliers=2))
 
 
-@pytest.mark.parametrize("M", [1, 8, 9, 16, 17, 48, 64])
+@pytest.mark.parametrize("M", [1, 8, 9, 16, 17, 48, 64, 65, 96, 97, 128])
 @pytest.mark.parametrize("K,N", [(1024, 520), (8, 24)])
 def test_rms_swiglu_bf16_decode_shapes(ops, M, K, N):
-    # one gate/up pair per workgroup, 1-4 row fragments; N = 520 / 24 leave a partial pair group
+    # one gate/up pair per workgroup, 1-8 row fragments; N = 520 / 24 leave a partial pair group
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M * 3 + 1, outliers=4))
 
 
