@@ -181,8 +181,8 @@ DN_API dn_status ln_linear_serial(const void* x, const ln_linear_weights* w, int
  * from ln_linear_prepare, so this is y F of Eq. (4) with y formed in
  * registers).  The normalization sits on the product's input path instead of
  * after it, which isolates what deferral buys over plain fusion.  bf16 only,
- * and only for the large-tile shapes (K % 64 == 0, at least 256 tiles of
- * 256 x 256, N < 2^22); other shapes give DN_ERR_UNSUPPORTED.  Otherwise as
+ * and only for the shapes that run the 256 x 256 kernel (M > 128,
+ * K % 64 == 0, K and N < 2^22); other shapes give DN_ERR_UNSUPPORTED.  Otherwise as
  * ln_linear_serial.
  */
 DN_API dn_status ln_linear_norm_on_load(const void* x, const ln_linear_weights* w, int64_t M, float eps,

@@ -1083,12 +1083,17 @@ static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-// The 256x256 kernel once its tiles fill the chip (and K is a multiple of its stage).
+// The 256x256 kernel past 128 rows (and K a multiple of its stage).  Below one
+// tile per CU it still wins: a 128 x 128 tile takes about as long as a 256 x 256
+// one on a chip this far from full, so the 128 x 128 kernel needs a second round
+// of tiles where the 256 x 256 kernel needs none.  Measured on 4096 -> 12288:
+// 768 and 1024 rows 89 / 97 us against 178 / 185 us; 8192 -> 28672 at 384 and
+// 512 rows 222 / 226 against 376 / 381 us, at 129-256 rows within 5 %.
 static bool use_big_tiles(int64_t M, int64_t N, int64_t K) {
     if (N >= (int64_t(1) << 22)) return false;  // 256 output rows < 2^31 bytes (32-bit store offsets)
     // K < 2^22 keeps the 32-bit copy offsets of a 256-row panel (256 K bf16) and of a
     // 16-chunk-column W' panel (16 x K/32 KiB) below 4 GiB.
-    return K % 64 == 0 && K < (int64_t(1) << 22) && ((M + 255) / 256) * ((N + 255) / 256) >= 256;
+    return K % 64 == 0 && K < (int64_t(1) << 22) && M > 128;
 }
 
 static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_t K, int64_t N, int dtype,

@@ -53,7 +53,8 @@ def test_ln_linear_f32_ragged(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "f32", seed=M))
 
 
-@pytest.mark.parametrize("M,K,N", [(17, 64, 136), (200, 520, 392), (257, 1024, 264), (300, 72, 8),
+@pytest.mark.parametrize("M,K,N", [(17, 64, 136), (200, 520, 392), (200, 512, 392), (129, 256, 8),
+                                   (257, 1024, 264), (300, 72, 8),
                                    (128, 768, 3072), (1, 8, 8)])
 def test_ln_linear_bf16_ragged(ops, M, K, N):
     _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M + K))
@@ -103,8 +104,8 @@ def test_ln_linear_bf16_large_tiles_sampled(ops, M, K, N):
 @pytest.mark.parametrize("M,K,N,layout", [(4104, 320, 4096, 2), (4104, 264, 4096, 2), (4104, 264, 4096, 1),
                                            (300, 136, 264, 2)])
 def test_gemm_sampled(ops, M, K, N, layout):
-    # layout 2 (packed weights, gamma = 1) at >= 256 tiles and K % 64 == 0 runs the 256x256
-    # pipelined loop; K = 264 and the small case run the 128x128 loop
+    # layout 2 (packed weights, gamma = 1) past 128 rows with K % 64 == 0 runs the 256x256
+    # pipelined loop; K = 264 and K = 136 run the 128x128 loop
     g = torch.Generator().manual_seed(5)
     A = torch.randn(M, K, generator=g).to(torch.bfloat16)
     B = torch.randn(K, N, generator=g).to(torch.bfloat16)
