@@ -21,7 +21,9 @@ on the same inputs; speedups compare each path timed on its own, back to back.
 workload on this host's cores and extrapolates by work.
 
 Other workloads (--workload): ln_qkv, causal_softmax_pv, ffn_prefill,
-ffn_decode_t{1,4,16} (LayerNorm -> FFN up-projection, 8192 x 28672), rms_qkv,
+ffn_decode_t{1,4,16} (LayerNorm -> FFN up-projection, 8192 x 28672),
+qkv_t{32,128,1024} (the LN -> QKV projection over 32 / 128 tokens of batched
+decode and a 1024-token prefill chunk), rms_qkv,
 rms_ffn_decode_t1 (RMSNorm, Eq. (6)), swiglu_prefill, swiglu_decode_t1
 (RMSNorm -> gated MLP input), causal_attention (scores formed in the kernel),
 decode_attention, decode_attention_gqa (split keys + merge), small.  Per kernel
@@ -109,7 +111,8 @@ def parse():
                     help="keep running warmup steps until this much wall time has passed")
     ap.add_argument("--workload", default="layer",
                     choices=["layer", "small", "ln_qkv", "causal_softmax_pv", "ffn_prefill",
-                             "ffn_decode_t1", "ffn_decode_t4", "ffn_decode_t16", "rms_qkv",
+                             "ffn_decode_t1", "ffn_decode_t4", "ffn_decode_t16", "qkv_t32", "qkv_t128",
+                             "qkv_t1024", "rms_qkv",
                              "rms_ffn_decode_t1", "swiglu_prefill", "swiglu_decode_t1", "causal_attention",
                              "decode_attention", "decode_attention_gqa"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -442,7 +445,10 @@ def build_sites(ops, I, name):
         w = I.swiglu_decode(1)
         return [SwiGLUSite(ops, I, w)], w.name
     t = int(name.rsplit("t", 1)[1])
-    w = I.rms_ffn_decode(t) if name.startswith("rms_") else I.ln_ffn_decode(t)
+    if name.startswith("qkv_"):
+        w = I.ln_qkv_tokens(t)
+    else:
+        w = I.rms_ffn_decode(t) if name.startswith("rms_") else I.ln_ffn_decode(t)
     return [LNSite(ops, I, w)], w.name
 
 
@@ -579,7 +585,10 @@ def main():
 
     d = sites[dom]
     dname = list(kernels)[dom]
-    hbm_bound = isinstance(d, (SMSite, DecodeAttnSite)) or (isinstance(d, (LNSite, SwiGLUSite)) and d.w.M <= 16)
+    # the roof the dominant kernel's arithmetic intensity (algorithmic FLOP per algorithmic
+    # byte) meets first: HBM below the ridge point (peak FLOP/s over peak bytes/s), else MFMA
+    hbm_bound = isinstance(d, (SMSite, DecodeAttnSite)) or \
+        d.flops() / d.bytes() < d.peak_tflops() * 1e12 / (PEAK_HBM_GBS * 1e9)
     if hbm_bound:
         ach = d.bytes() / (per[dom] * 1e-3) / 1e9
         roof = {"kernel": dname, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,

@@ -91,6 +91,11 @@ def ln_ffn_decode(t: int) -> LNWorkload:
     return LNWorkload(f"ln_ffn_up_bf16_decode_t{t}_8192x28672", 5, t, 8192, 28672, "bf16")
 
 
+def ln_qkv_tokens(t: int) -> LNWorkload:
+    """The QKV projection of LN_QKV over t tokens: batched decode (t <= 128) or a prefill chunk."""
+    return LNWorkload(f"ln_qkv_bf16_t{t}_4096x12288", 3, t, 4096, 12288, "bf16", outliers=8)
+
+
 # Attention from Q, K, V directly (the scores formed in the kernel): the causal
 # workload's own tensors, 32 heads x 8192 tokens, d = 128.
 ATTN_CAUSAL = SMWorkload("causal_attention_bf16_32x8192x8192_d128", 4, 32, 8192, 128, causal=True, from_qk=True)
@@ -157,6 +162,7 @@ def swiglu_decode(t: int) -> LNWorkload:
 
 WORKLOADS = {w.name: w for w in (LN_F32_SMALL, SM_BF16_SMALL, LN_QKV, SM_CAUSAL, LN_FFN_PREFILL,
                                  ln_ffn_decode(1), ln_ffn_decode(4), ln_ffn_decode(16),
+                                 ln_qkv_tokens(32), ln_qkv_tokens(128), ln_qkv_tokens(1024),
                                  RMS_QKV, rms_ffn_decode(1), SWIGLU_PREFILL, swiglu_decode(1), ATTN_CAUSAL,
                                  ATTN_DECODE, ATTN_DECODE_GQA)}
 
