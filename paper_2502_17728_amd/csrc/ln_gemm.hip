@@ -429,9 +429,10 @@ __device__ __forceinline__ u32x4 normalize_chunk(const u32x4& a, float r, float 
 
 __device__ __forceinline__ int a_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-template <Epi EPI, int WM, int WN>
+template <Epi EPI, int WM, int WN, int BM = 256, int BN = 256>
 __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int group) {
-    constexpr int BM = 256, BN = 256, NW = WM * WN;
+    constexpr int NW = WM * WN;
+    static_assert(WN == 2, "the two wave columns split each row fragment's moments");
     constexpr int BK = 64;                        // bf16 elements per stage (128 B per row)
     constexpr int WTM = BM / WM, WTN = BN / WN;   // 64 x 128 per wave
     constexpr int FM = WTM / 16, FN = WTN / 16;   // 4 x 8 output fragments
@@ -1051,9 +1052,9 @@ static hipError_t run_main(const MainArgs& a, int64_t batch, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <Epi EPI>
+template <Epi EPI, int BT = 256>
 static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
-    const int64_t tm = (a.M + 255) / 256, tn = (a.N + 255) / 256;
+    const int64_t tm = (a.M + BT - 1) / BT, tn = (a.N + BT - 1) / BT;
     // deferred LN: each workgroup takes `group` column tiles of one row block and
     // reduces the row moments once, on its first tile.  With one workgroup per CU
     // the run takes about ceil(workgroups / 256) * group tile times; take the
@@ -1079,14 +1080,18 @@ static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
 #define DN_PIPE_WM 4
 #define DN_PIPE_WN 2
 #endif
-    pipe_kernel<EPI, DN_PIPE_WM, DN_PIPE_WN><<<dim3((unsigned)wgs), DN_PIPE_WM * DN_PIPE_WN * kWave, 0, s>>>(a, (int)group);
+    if constexpr (BT == 128)  // 4 waves of 64 x 64, 64 KiB of LDS: two workgroups per CU
+        pipe_kernel<EPI, 2, 2, 128, 128><<<dim3((unsigned)wgs), 4 * kWave, 0, s>>>(a, (int)group);
+    else
+        pipe_kernel<EPI, DN_PIPE_WM, DN_PIPE_WN><<<dim3((unsigned)wgs), DN_PIPE_WM * DN_PIPE_WN * kWave, 0, s>>>(
+            a, (int)group);
     return hipGetLastError();
 }
 
-// The 256x256 kernel past 128 rows (and K a multiple of its stage).  Below one
-// tile per CU it still wins: a 128 x 128 tile takes about as long as a 256 x 256
-// one on a chip this far from full, so the 128 x 128 kernel needs a second round
-// of tiles where the 256 x 256 kernel needs none.  Measured on 4096 -> 12288:
+// The 256x256 kernel past 128 rows (and K a multiple of its stage), where the
+// 128 x 128 tiles do not fit in one round.  Below one 256 x 256 tile per CU it
+// still beats the two-stage 128 x 128 loop, which then needs a second round of
+// tiles where the 256 x 256 kernel needs none.  Measured on 4096 -> 12288:
 // 768 and 1024 rows 89 / 97 us against 178 / 185 us; 8192 -> 28672 at 384 and
 // 512 rows 222 / 226 against 376 / 381 us, at 129-256 rows within 5 %.
 static bool use_big_tiles(int64_t M, int64_t N, int64_t K) {
@@ -1094,6 +1099,16 @@ static bool use_big_tiles(int64_t M, int64_t N, int64_t K) {
     // K < 2^22 keeps the 32-bit copy offsets of a 256-row panel (256 K bf16) and of a
     // 16-chunk-column W' panel (16 x K/32 KiB) below 4 GiB.
     return K % 64 == 0 && K < (int64_t(1) << 22) && M > 128;
+}
+// The pipelined kernel on 128 x 128 tiles (4 waves, two workgroups per CU) while
+// those tiles number at most one per CU: then a tile takes far less than a
+// 256 x 256 one and the chip is as full.  Measured on 4096 -> 12288 at 129 / 256
+// rows (192 tiles) 56 / 58 us against 86 us on 256 x 256 tiles, on 8192 -> 28672
+// at 65 / 100 rows (224 tiles) 132 / 133 us against 174 / 184 us on the 128 x 128
+// two-stage loop; at 288 tiles and more it lost (97-448 us against 89-230 us).
+static bool use_mid_tiles(int64_t M, int64_t N, int64_t K) {
+    return K % 64 == 0 && K < (int64_t(1) << 22) && N < (int64_t(1) << 22) &&
+           ((M + 127) / 128) * ((N + 127) / 128) <= 256;
 }
 
 static MainArgs packed_args(const void* A, const void* packed, int64_t M, int64_t K, int64_t N, int dtype,
@@ -1174,6 +1189,7 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
         return hipGetLastError();
     }
     if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
+    if (use_mid_tiles(M, N, K)) return run_pipe<Epi::kLnDeferred, 128>(a, s);
     if (use_big_tiles(M, N, K)) return run_pipe<Epi::kLnDeferred>(a, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
 }
@@ -1220,6 +1236,7 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
         return hipGetLastError();
     }
     if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kSwiGlu>(a, 1, s);
+    if (use_mid_tiles(M, np, K)) return run_pipe<Epi::kSwiGlu, 128>(a, s);
     if (use_big_tiles(M, np, K)) return run_pipe<Epi::kSwiGlu>(a, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kSwiGlu>(a, 1, s);
 }
@@ -1257,6 +1274,7 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
             return hipGetLastError();
         }
         if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);
+        if (use_mid_tiles(M, N, K)) return run_pipe<Epi::kGemm, 128>(a, s);
         if (use_big_tiles(M, N, K)) return run_pipe<Epi::kGemm>(a, s);
         return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);
     }
