@@ -69,13 +69,13 @@ TRAFFIC = {
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
         "fetch_kib": 1151051, "fetch_scale": 1.99993, "write_kib": 66101, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("cc569ab1ac23d5c050a788c1a58e8e73ccb888cab4ae2b7f4076319f19d596d6",
+        "sha256": ("cce5fe5af035ecc1a112f8f5f3617de14c00829f5902c5339a1305844446d3c6",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 296698, "fetch_scale": 1.99993, "write_kib": 102403, "write_scale": 1.0},
+        "fetch_kib": 296596, "fetch_scale": 1.99993, "write_kib": 102403, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("cc569ab1ac23d5c050a788c1a58e8e73ccb888cab4ae2b7f4076319f19d596d6",
+        "sha256": ("cce5fe5af035ecc1a112f8f5f3617de14c00829f5902c5339a1305844446d3c6",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 229646, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
+        "fetch_kib": 229677, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
         "sha256": ("76dc4fc2b2825ebd51688a01e9472cb45cd21d7dbf8e43ec98ab907f8cf91adf",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
