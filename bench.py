@@ -69,11 +69,11 @@ TRAFFIC = {
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
         "fetch_kib": 1151051, "fetch_scale": 1.99993, "write_kib": 66101, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("cce5fe5af035ecc1a112f8f5f3617de14c00829f5902c5339a1305844446d3c6",
+        "sha256": ("1a9a8b22c5e0f347a5995b69976b79266e0a9bc9adbac277086936100446b995",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
         "fetch_kib": 296596, "fetch_scale": 1.99993, "write_kib": 102403, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("cce5fe5af035ecc1a112f8f5f3617de14c00829f5902c5339a1305844446d3c6",
+        "sha256": ("1a9a8b22c5e0f347a5995b69976b79266e0a9bc9adbac277086936100446b995",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
         "fetch_kib": 229677, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {

@@ -462,9 +462,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
     // the epilogues of all the group's tiles.  Workgroup order: XCD-contiguous,
     // then blocks of GM row blocks x all column groups (operand panels shared
     // under one L2).
-#ifndef DN_GROUP_FORCE
     if constexpr (!LN) group = 1;  // the plain product has no per-row work to share
-#endif
     const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
     const int ngroups = (tiles_n + group - 1) / group;
     const int t = xcd_contiguous(blockIdx.x, gridDim.x);
@@ -1072,19 +1070,11 @@ static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
             }
         }
     }
-#ifdef DN_GROUP_FORCE
-    group = DN_GROUP_FORCE;
-#endif
     const int64_t wgs = tm * ((tn + group - 1) / group);
-#ifndef DN_PIPE_WM
-#define DN_PIPE_WM 4
-#define DN_PIPE_WN 2
-#endif
     if constexpr (BT == 128)  // 4 waves of 64 x 64, 64 KiB of LDS: two workgroups per CU
         pipe_kernel<EPI, 2, 2, 128, 128><<<dim3((unsigned)wgs), 4 * kWave, 0, s>>>(a, (int)group);
     else
-        pipe_kernel<EPI, DN_PIPE_WM, DN_PIPE_WN><<<dim3((unsigned)wgs), DN_PIPE_WM * DN_PIPE_WN * kWave, 0, s>>>(
-            a, (int)group);
+        pipe_kernel<EPI, 4, 2><<<dim3((unsigned)wgs), 8 * kWave, 0, s>>>(a, (int)group);
     return hipGetLastError();
 }
 
