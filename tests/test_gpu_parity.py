@@ -102,10 +102,11 @@ def test_ln_linear_bf16_large_tiles_sampled(ops, M, K, N):
 
 
 @pytest.mark.parametrize("M,K,N,layout", [(4104, 320, 4096, 2), (4104, 264, 4096, 2), (4104, 264, 4096, 1),
-                                           (300, 136, 264, 2)])
+                                           (300, 136, 264, 2), (257, 512, 1032, 2)])
 def test_gemm_sampled(ops, M, K, N, layout):
-    # layout 2 (packed weights, gamma = 1) past 128 rows with K % 64 == 0 runs the 256x256
-    # pipelined loop; K = 264 and K = 136 run the 128x128 loop
+    # layout 2 (packed weights, gamma = 1) with K % 64 == 0 runs the pipelined loop, on
+    # 256 x 256 tiles at 4104 rows and on 128 x 128 tiles at 257 x 1032 (27 tiles);
+    # K = 264 and K = 136 run the two-stage 128 x 128 loop
     g = torch.Generator().manual_seed(5)
     A = torch.randn(M, K, generator=g).to(torch.bfloat16)
     B = torch.randn(K, N, generator=g).to(torch.bfloat16)
@@ -158,6 +159,15 @@ def test_ln_linear_qkv_workload_sampled(ops):
 @pytest.mark.parametrize("t", [1, 4, 8, 16])
 def test_ln_linear_ffn_decode_workload(ops, t):
     _ln_check(ops, I.make_ln(I.ln_ffn_decode(t)))
+
+
+@pytest.mark.parametrize("t", [32, 128, 1024])
+def test_ln_linear_qkv_tokens_workload_sampled(ops, t):
+    # the QKV projection at the bench's batched-decode and prefill-chunk sizes, in the
+    # launch configurations it times: 2 and 8 row fragments of the streaming kernel, and
+    # 4 x 48 tiles of 256 x 256 (one tile per workgroup, each reducing its rows' moments)
+    w = I.ln_qkv_tokens(t)
+    _ln_check(ops, I.make_ln(w), rows=I.sample_rows(w.M, min(w.M, 24), seed=t))
 
 
 def test_ln_linear_deterministic(ops):
