@@ -181,8 +181,9 @@ DN_API dn_status ln_linear_serial(const void* x, const ln_linear_weights* w, int
  * from ln_linear_prepare, so this is y F of Eq. (4) with y formed in
  * registers).  The normalization sits on the product's input path instead of
  * after it, which isolates what deferral buys over plain fusion.  bf16 only,
- * and only for the shapes that run the 256 x 256 kernel (M > 128,
- * K % 64 == 0, K and N < 2^22); other shapes give DN_ERR_UNSUPPORTED.  Otherwise as
+ * and only where the 256 x 256 kernel applies (M > 128, K % 64 == 0,
+ * K and N < 2^22; it runs there even when ln_linear_deferred would take
+ * 128 x 128 tiles); other shapes give DN_ERR_UNSUPPORTED.  Otherwise as
  * ln_linear_serial.
  */
 DN_API dn_status ln_linear_norm_on_load(const void* x, const ln_linear_weights* w, int64_t M, float eps,
