@@ -1195,6 +1195,13 @@ hipError_t launch_ln_linear_on_load(const void* x, const void* packed, int64_t M
     return run_pipe<Epi::kLnOnLoad>(a, s);
 }
 
+template <int NC, class F>
+static void swiglu_dispatch_nc(int64_t nc, F&& launch) {  // min(nc, NC) column blocks (NC / 2 pairs)
+    if constexpr (NC > 2)
+        if (nc < NC) return swiglu_dispatch_nc<NC - 2>(nc, launch);
+    launch(ln_decode_bf16_kernel<4, NC, 2, true>, 4, NC);
+}
+
 hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, int64_t K, int64_t N, int dtype,
                                   float eps, int rms, void* out, hipStream_t s) {
     const int64_t np = 2 * ((N + 15) / 16) * 16;  // packed (gate + up) columns
@@ -1209,10 +1216,13 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
                                                            a.c_col, a.b_col, (int)M, K, np, eps, rms, N,
                                                            nullptr, nullptr, (__bf16*)out, nullptr);
         };
-        // one gate/up block pair per workgroup, 4 K-slices, 2-chunk groups: measured
-        // flat at 69 % of HBM for 1-16 tokens on the 8192 x 2 x 28672 weights
+        // up to 16 tokens: up to 7 gate/up block pairs per workgroup (about one
+        // workgroup per CU), 4 K-slices, 2-chunk groups -- on the 8192 x 2 x 28672
+        // weights 154.5 us (6.1 TB/s) for 1 token against 166.3 us with one pair per
+        // workgroup and 154.9 us with 8 K-slices; past 16 tokens one pair per workgroup
         if (M <= 16)
-            launch(ln_decode_bf16_kernel<4, 2, 2, true>, 4, 2);
+            swiglu_dispatch_nc<14>(2 * std::min<int64_t>(7, std::max<int64_t>(1, (a.nblocks / 2 + 255) / 256)),
+                                   launch);
         else if (M <= 32)
             launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 2>, 4, 2);
         else if (M <= 48)

@@ -387,7 +387,10 @@ def test_rms_swiglu_f32_ragged(ops, M, K, N):
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "f32", seed=M))
 
 
-@pytest.mark.parametrize("M,K,N", [(17, 64, 136), (257, 1024, 264), (128, 768, 1032), (1, 8, 8)])
+# (1, 64, 12304), (16, 128, 28688), (3, 64, 4112): 4, 7 and 2 gate/up pairs per decode
+# workgroup, each with a last workgroup holding a single pair
+@pytest.mark.parametrize("M,K,N", [(17, 64, 136), (257, 1024, 264), (128, 768, 1032), (1, 8, 8),
+                                   (1, 64, 12304), (16, 128, 28688), (3, 64, 4112)])
 def test_rms_swiglu_bf16_ragged(ops, M, K, N):
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M + K, outliers=2))
 
