@@ -69,13 +69,13 @@ TRAFFIC = {
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
         "fetch_kib": 1151051, "fetch_scale": 1.99993, "write_kib": 66101, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("a62aeed983ce02d7857050d58f316045f2f991152178c911d28b780d239c7252",
+        "sha256": ("62a6e76fd0309292980b2b1fab4a93d9d66d3c6a5363476a119877b86a52a822",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 296655, "fetch_scale": 1.99993, "write_kib": 102403, "write_scale": 1.0},
+        "fetch_kib": 296706, "fetch_scale": 1.99993, "write_kib": 102403, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("a62aeed983ce02d7857050d58f316045f2f991152178c911d28b780d239c7252",
+        "sha256": ("62a6e76fd0309292980b2b1fab4a93d9d66d3c6a5363476a119877b86a52a822",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 229680, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
+        "fetch_kib": 229678, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
         "sha256": ("76dc4fc2b2825ebd51688a01e9472cb45cd21d7dbf8e43ec98ab907f8cf91adf",
                    "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),

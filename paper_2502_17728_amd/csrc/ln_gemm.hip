@@ -1219,16 +1219,18 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
         // up to 16 tokens: up to 7 gate/up block pairs per workgroup (about one
         // workgroup per CU), 4 K-slices, 2-chunk groups -- on the 8192 x 2 x 28672
         // weights 154.5 us (6.1 TB/s) for 1 token against 166.3 us with one pair per
-        // workgroup and 154.9 us with 8 K-slices; past 16 tokens one pair per workgroup
+        // workgroup and 154.9 us with 8 K-slices; 33-64 tokens two pairs per workgroup
+        // (48 / 64 tokens: 220 / 276 us against 262 / 309 us with one; three pairs
+        // 258 / 307 us); 17-32 and 65-128 tokens one pair
         if (M <= 16)
             swiglu_dispatch_nc<14>(2 * std::min<int64_t>(7, std::max<int64_t>(1, (a.nblocks / 2 + 255) / 256)),
                                    launch);
         else if (M <= 32)
             launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 2>, 4, 2);
         else if (M <= 48)
-            launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 3>, 4, 2);
+            launch(ln_decode_bf16_kernel<4, 4, 2, true, false, 3>, 4, 4);
         else if (M <= 64)
-            launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 4>, 4, 2);
+            launch(ln_decode_bf16_kernel<4, 4, 2, true, false, 4>, 4, 4);
         else if (M <= 96)
             launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 6>, 4, 2);
         else
