@@ -227,3 +227,25 @@ def attention(Q_rows, K, V, scale, head=None, qpos=None, nthreads=None):
     _check(_load().oracle_attention(_ptr(Q), _ptr(K), _ptr(V), _ptr(h), _ptr(q), R, Lk, d, float(scale),
                                     _ptr(out), _threads(nthreads)), "attention")
     return out
+
+
+def norm_linear_matmul(x, gamma, beta, W, bias, eps, rms=False, nthreads=None):
+    """LayerNorm (Eq. (1)-(2)) or RMSNorm (Eq. (6)) of x[M, K] by the C oracle, then the Eq. (4)
+    product y . W + bias as one fp64 library matmul (numpy's BLAS), in place of the C row loop that
+    streams all of W once per row.  Same definition, same fp64 operands; used to check every row of
+    the large workloads.  Pinned against ln_linear / rms_linear in the oracle's tests."""
+    y = rmsnorm(x, gamma, eps, beta=beta, nthreads=nthreads) if rms else \
+        layernorm(x, gamma, beta, eps, nthreads=nthreads)
+    out = y @ to_f64(W)
+    if bias is not None:
+        out += to_f64(bias).reshape(1, -1)
+    return out
+
+
+def rms_swiglu_matmul(x, gamma, Wg, Wu, eps, nthreads=None):
+    """SiLU(RMSNorm(x) . Wg) * (RMSNorm(x) . Wu) with both products as fp64 library matmuls;
+    SiLU(z) = z / (1 + e^-z).  Pinned against rms_swiglu in the oracle's tests."""
+    y = rmsnorm(x, gamma, eps, nthreads=nthreads)
+    g = y @ to_f64(Wg)
+    u = y @ to_f64(Wu)
+    return g / (1.0 + np.exp(-g)) * u

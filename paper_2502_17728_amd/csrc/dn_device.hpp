@@ -191,6 +191,20 @@ __device__ __forceinline__ float xor32_pair_op(float v, bool is_max) {
 __device__ __forceinline__ float sum_lane_groups(float v) { return xor32_pair_op(xor16_pair_op(v, false), false); }
 __device__ __forceinline__ float max_lane_groups(float v) { return xor32_pair_op(xor16_pair_op(v, true), true); }
 
+// ----------------------------------------------------------------- row statistics
+// rstd = 1/sqrt(var + eps) from one-pass moments, var = E[x^2] - mean^2 (Eq. (1)-(2);
+// RMSNorm, Eq. (6): mean = 0).  Rounding can take the difference slightly below
+// zero, so it is clamped at 0 -- but only when it is a number: a row holding NaN
+// or +-inf has NaN moments (inf - inf), and its statistics stay NaN so that every
+// output of the row is NaN, as the plain definition gives.  A zero variance with
+// eps = 0 makes the definition (x - mean) / 0 = 0/0 for every element: NaN as well.
+__device__ __forceinline__ float rstd_from_moments(float mean_sq, float mean, float eps) {
+    const float d = mean_sq - mean * mean;
+    const float var = d > 0.f ? d : (d == d ? 0.f : d);
+    const float r = 1.0f / __builtin_sqrtf(var + eps);
+    return r == __builtin_inff() ? __builtin_nanf("") : r;
+}
+
 // ----------------------------------------------------------------- 8x8 bf16 transpose
 // in[r] holds 8 bf16 (columns 0..7) of row r; out[c] gets column c (rows 0..7).
 __device__ __forceinline__ void transpose8x8_bf16(const u32x4 in[8], u32x4 out[8]) {

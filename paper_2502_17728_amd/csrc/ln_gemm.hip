@@ -332,9 +332,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 b += red[(1 * WN + w) * BM + r];
             }
             const float mean = p.rms ? 0.f : a / (float)K;
-            const float var = __builtin_fmaxf(b / (float)K - mean * mean, 0.f);
             row_mean[r] = mean;
-            row_rstd[r] = 1.0f / __builtin_sqrtf(var + p.eps);
+            row_rstd[r] = rstd_from_moments(b / (float)K, mean, p.eps);
             if (p.stats_out && pn == 0 && m0 + r < M) {  // one tile per row block exports them
                 p.stats_out[2 * (m0 + r)] = mean;
                 p.stats_out[2 * (m0 + r) + 1] = row_rstd[r];
@@ -632,9 +631,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
             __syncthreads();
             for (int r = tid; r < BM; r += NW * kWave) {
                 const float mean = p.rms ? 0.f : row_s1[r] / (float)K;
-                const float var = __builtin_fmaxf(row_s2[r] / (float)K - mean * mean, 0.f);
+                row_s2[r] = rstd_from_moments(row_s2[r] / (float)K, mean, p.eps);
                 row_s1[r] = mean;
-                row_s2[r] = 1.0f / __builtin_sqrtf(var + p.eps);
                 if (p.stats_out && gn == 0 && m0 + r < M) {  // the row block's first group exports them
                     p.stats_out[2 * (m0 + r)] = mean;
                     p.stats_out[2 * (m0 + r) + 1] = row_s2[r];
@@ -890,8 +888,7 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
             for (int i = 0; i < 4; ++i) {
                 const int r = 16 * f + 4 * (lane >> 4) + i;
                 float mean = rms ? 0.f : tot[1][i] / (float)K;
-                const float var = __builtin_fmaxf(diag[i] / (float)K - mean * mean, 0.f);
-                float rstd = 1.0f / __builtin_sqrtf(var + eps);
+                float rstd = rstd_from_moments(diag[i] / (float)K, mean, eps);
                 if (row_stats) {  // serial ablation (the moment products above are then unused)
                     mean = row_stats[2 * min(r, M - 1)];
                     rstd = row_stats[2 * min(r, M - 1) + 1];

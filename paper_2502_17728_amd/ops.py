@@ -110,6 +110,30 @@ def _dev(t: Optional[torch.Tensor], name: str):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _expect(t: Optional[torch.Tensor], name: str, shape=None, dtype=None, device=None, numel=None):
+    """Check a tensor before its pointer reaches the C ABI, which sees only raw pointers and
+    sizes: a wrong shape there becomes an out-of-bounds access on the GPU.  Raises ValueError
+    on any mismatch; shape entries of None match any size."""
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if shape is not None:
+        ok = t.dim() == len(shape) and all(s is None or int(a) == int(s) for a, s in zip(t.shape, shape))
+        if not ok:
+            want = "[" + ", ".join("*" if s is None else str(int(s)) for s in shape) + "]"
+            raise ValueError(f"{name} has shape {list(t.shape)}, expected {want}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device} (all tensors of a call share one device)")
+
+
+_TORCH_DT = {DN_F32: torch.float32, DN_BF16: torch.bfloat16}
+
+
 def _stream(stream) -> ctypes.c_void_p:
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -119,6 +143,19 @@ def _stream(stream) -> ctypes.c_void_p:
 def _check(fn: str, status: int):
     if status != 0:
         raise DNError(fn, status)
+
+
+def _check_rows(x: torch.Tensor, w, out: Optional[torch.Tensor], stats: Optional[torch.Tensor] = None) -> int:
+    """x[M, w.K] in the weights' dtype; out (if given) [M, w.N] like x; stats (if given) 2 M fp32."""
+    if not isinstance(w, PreparedLinear):
+        raise TypeError("w must come from ln_linear_prepare / swiglu_prepare")
+    if x.dim() != 2:
+        raise ValueError(f"x has shape {list(x.shape)}, expected [M, {w.K}]")
+    M = x.shape[0]
+    _expect(x, "x", (M, w.K), _TORCH_DT.get(w.desc.dtype), w.packed.device)
+    _expect(out, "out", (M, w.N), x.dtype, x.device)
+    _expect(stats, "stats", None, torch.float32, x.device, numel=2 * M)
+    return M
 
 
 @dataclasses.dataclass
@@ -143,8 +180,13 @@ def ln_linear_packed_bytes(K: int, N: int, dtype: int) -> int:
 def ln_linear_prepare(W: torch.Tensor, gamma: torch.Tensor, beta: Optional[torch.Tensor] = None,
                       bias: Optional[torch.Tensor] = None, stream=None, centered: bool = False) -> PreparedLinear:
     """centered=True calls ln_linear_prepare_centered (the literal Eq. (5) weight)."""
+    if W.dim() != 2:
+        raise ValueError(f"W has shape {list(W.shape)}, expected [K, N]")
     K, N = W.shape
     dt = _dt(W)
+    _expect(gamma, "gamma", (K,), W.dtype, W.device)
+    _expect(beta, "beta", (K,), W.dtype, W.device)
+    _expect(bias, "bias", (N,), W.dtype, W.device)
     nbytes = ln_linear_packed_bytes(K, N, dt)
     if nbytes == 0:
         raise DNError("ln_linear_packed_bytes", 1)
@@ -159,11 +201,9 @@ def ln_linear_prepare(W: torch.Tensor, gamma: torch.Tensor, beta: Optional[torch
 
 def ln_linear_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
                        out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    M = x.shape[0]
+    M = _check_rows(x, w, out)
     if out is None:
         out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
-    if _dt(x) != w.desc.dtype:
-        raise TypeError("x dtype differs from the prepared weights")
     _check("ln_linear_deferred", _lib.ln_linear_deferred(
         _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(out, "out"), _stream(stream)))
     return out
@@ -171,13 +211,11 @@ def ln_linear_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
 
 def ln_linear_serial(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5, stats: Optional[torch.Tensor] = None,
                      out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    M = x.shape[0]
+    M = _check_rows(x, w, out, stats)
     if out is None:
         out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
     if stats is None:
         stats = torch.empty(2 * M, dtype=torch.float32, device=x.device)
-    if _dt(x) != w.desc.dtype:
-        raise TypeError("x dtype differs from the prepared weights")
     _check("ln_linear_serial", _lib.ln_linear_serial(
         _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(stats, "stats"), _dev(out, "out"), _stream(stream)))
     return out
@@ -187,13 +225,11 @@ def ln_linear_norm_on_load(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5
                            stats: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
                            stream=None) -> torch.Tensor:
     """Ablation: statistics pre-pass, then x normalized on load into the product (no deferral)."""
-    M = x.shape[0]
+    M = _check_rows(x, w, out, stats)
     if out is None:
         out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
     if stats is None:
         stats = torch.empty(2 * M, dtype=torch.float32, device=x.device)
-    if _dt(x) != w.desc.dtype:
-        raise TypeError("x dtype differs from the prepared weights")
     _check("ln_linear_norm_on_load", _lib.ln_linear_norm_on_load(
         _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(stats, "stats"), _dev(out, "out"), _stream(stream)))
     return out
@@ -204,15 +240,17 @@ def linear_deferred_post(x: torch.Tensor, w: PreparedLinear, gamma: torch.Tensor
                          y: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
                          stream=None):
     """Post-LN placement: (out, y, stats) -- the deferred product and the normalized rows."""
-    M, K = x.shape
+    M = _check_rows(x, w, out, stats)
+    K = w.K
+    _expect(gamma, "gamma", (K,), x.dtype, x.device)
+    _expect(beta, "beta", (K,), x.dtype, x.device)
+    _expect(y, "y", (M, K), x.dtype, x.device)
     if out is None:
         out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
     if y is None:
         y = torch.empty_like(x)
     if stats is None:
         stats = torch.empty(2 * M, dtype=torch.float32, device=x.device)
-    if _dt(x) != w.desc.dtype or gamma.dtype != x.dtype or (beta is not None and beta.dtype != x.dtype):
-        raise TypeError("x, gamma, beta and the prepared weights must share one dtype")
     if rms:
         if beta is not None:
             raise ValueError("RMSNorm has no shift")
@@ -229,11 +267,9 @@ def linear_deferred_post(x: torch.Tensor, w: PreparedLinear, gamma: torch.Tensor
 
 def rms_linear_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
                         out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    M = x.shape[0]
+    M = _check_rows(x, w, out)
     if out is None:
         out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
-    if _dt(x) != w.desc.dtype:
-        raise TypeError("x dtype differs from the prepared weights")
     _check("rms_linear_deferred", _lib.rms_linear_deferred(
         _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(out, "out"), _stream(stream)))
     return out
@@ -244,9 +280,11 @@ def swiglu_packed_bytes(K: int, N: int, dtype: int) -> int:
 
 
 def swiglu_prepare(W_gate: torch.Tensor, W_up: torch.Tensor, gamma: torch.Tensor, stream=None) -> PreparedLinear:
+    if W_gate.dim() != 2:
+        raise ValueError(f"W_gate has shape {list(W_gate.shape)}, expected [K, N]")
     K, N = W_gate.shape
-    if tuple(W_up.shape) != (K, N):
-        raise ValueError("W_gate and W_up must have the same [K, N] shape")
+    _expect(W_up, "W_up", (K, N), W_gate.dtype, W_gate.device)
+    _expect(gamma, "gamma", (K,), W_gate.dtype, W_gate.device)
     dt = _dt(W_gate)
     nbytes = swiglu_packed_bytes(K, N, dt)
     if nbytes == 0:
@@ -261,11 +299,9 @@ def swiglu_prepare(W_gate: torch.Tensor, W_up: torch.Tensor, gamma: torch.Tensor
 
 def rms_swiglu_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
                         out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    M = x.shape[0]
+    M = _check_rows(x, w, out)
     if out is None:
         out = torch.empty((M, w.N), dtype=x.dtype, device=x.device)
-    if _dt(x) != w.desc.dtype:
-        raise TypeError("x dtype differs from the prepared weights")
     _check("rms_swiglu_deferred", _lib.rms_swiglu_deferred(
         _dev(x, "x"), ctypes.byref(w.desc), M, eps, _dev(out, "out"), _stream(stream)))
     return out
@@ -273,13 +309,31 @@ def rms_swiglu_deferred(x: torch.Tensor, w: PreparedLinear, eps: float = 1e-5,
 
 def softmax_pv_deferred(S: torch.Tensor, V: torch.Tensor, causal: bool = False,
                         out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    if S.dim() != 3 or V.dim() != 3:
+        raise ValueError(f"S must be [BH, Lq, Lk] and V [BH, Lk, d]; got {list(S.shape)} and {list(V.shape)}")
     BH, Lq, Lk = S.shape
     d = V.shape[-1]
+    _expect(V, "V", (BH, Lk, d), S.dtype, S.device)
+    _expect(out, "out", (BH, Lq, d), S.dtype, S.device)
     if out is None:
         out = torch.empty((BH, Lq, d), dtype=S.dtype, device=S.device)
     _check("softmax_pv_deferred", _lib.softmax_pv_deferred(
         _dev(S, "S"), _dev(V, "V"), BH, Lq, Lk, d, int(causal), _dt(S), _dev(out, "out"), _stream(stream)))
     return out
+
+
+def _check_qkv(Q, K, V, out):
+    """Q[BHq, Lq, d], K and V [BH, Lk, d] with BHq a multiple of BH, one dtype and device; out like Q."""
+    if Q.dim() != 3 or K.dim() != 3:
+        raise ValueError(f"Q must be [BHq, Lq, d] and K, V [BH, Lk, d]; got {list(Q.shape)} and {list(K.shape)}")
+    BHq, Lq, d = Q.shape
+    BH, Lk = K.shape[0], K.shape[1]
+    _expect(K, "K", (BH, Lk, d), Q.dtype, Q.device)
+    _expect(V, "V", (BH, Lk, d), Q.dtype, Q.device)
+    if BH < 1 or BHq % BH:
+        raise ValueError(f"the query heads ({BHq}) must be a multiple of the key/value heads ({BH})")
+    _expect(out, "out", tuple(Q.shape), Q.dtype, Q.device)
+    return BHq, Lq, d, BH, Lk
 
 
 def attention_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, causal: bool = False,
@@ -290,10 +344,7 @@ def attention_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, causal
     Q[BH * g, Lq, d], K/V[BH, Lk, d]: g = 1 is one key/value head per query head; g > 1 is
     grouped-query attention, query head h reading key/value head h // g.
     """
-    BHq, Lq, d = Q.shape
-    BH, Lk = K.shape[0], K.shape[1]
-    if K.shape[2] != d or tuple(V.shape) != tuple(K.shape) or BHq % BH:
-        raise ValueError("K and V must be [BH, Lk, d] with the query heads a multiple of BH")
+    BHq, Lq, d, BH, Lk = _check_qkv(Q, K, V, out)
     g = BHq // BH
     if scale is None:
         scale = 1.0 / float(d) ** 0.5
@@ -323,10 +374,8 @@ def attention_decode_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
     heads h * g .. h * g + g - 1 share key/value head h, and the g heads' rows go through
     the kernel together as g * Lq (<= 16) queries of that head.
     """
-    BHq, Lq, d = Q.shape
-    BH, Lk = K.shape[0], K.shape[1]
-    if K.shape[2] != d or tuple(V.shape) != tuple(K.shape) or BHq % BH:
-        raise ValueError("K and V must be [BH, Lk, d] with the query heads a multiple of BH")
+    BHq, Lq, d, BH, Lk = _check_qkv(Q, K, V, out)
+    _expect(workspace, "workspace", None, torch.uint8, Q.device)
     g = BHq // BH
     if out is None:
         out = torch.empty_like(Q)
@@ -343,9 +392,19 @@ def attention_decode_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
     return out
 
 
+def _check_norm(x, gamma, beta, out):
+    if x.dim() != 2:
+        raise ValueError(f"x has shape {list(x.shape)}, expected [M, K]")
+    M, K = x.shape
+    _expect(gamma, "gamma", (K,), x.dtype, x.device)
+    _expect(beta, "beta", (K,), x.dtype, x.device)
+    _expect(out, "out", (M, K), x.dtype, x.device)
+    return M, K
+
+
 def layernorm(x: torch.Tensor, gamma: torch.Tensor, beta: Optional[torch.Tensor] = None, eps: float = 1e-5,
               out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    M, K = x.shape
+    M, K = _check_norm(x, gamma, beta, out)
     if out is None:
         out = torch.empty_like(x)
     _check("layernorm", _lib.layernorm(_dev(x, "x"), _dev(gamma, "gamma"), _dev(beta, "beta"), M, K, eps,
@@ -355,7 +414,7 @@ def layernorm(x: torch.Tensor, gamma: torch.Tensor, beta: Optional[torch.Tensor]
 
 def rmsnorm(x: torch.Tensor, gamma: torch.Tensor, eps: float = 1e-5, out: Optional[torch.Tensor] = None,
             stream=None) -> torch.Tensor:
-    M, K = x.shape
+    M, K = _check_norm(x, gamma, None, out)
     if out is None:
         out = torch.empty_like(x)
     _check("rmsnorm", _lib.rmsnorm(_dev(x, "x"), _dev(gamma, "gamma"), M, K, eps, _dt(x), _dev(out, "out"),
@@ -364,8 +423,8 @@ def rmsnorm(x: torch.Tensor, gamma: torch.Tensor, eps: float = 1e-5, out: Option
 
 
 def silu_mul(g: torch.Tensor, u: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    if g.shape != u.shape or g.dtype != u.dtype:
-        raise ValueError("g and u must match in shape and dtype")
+    _expect(u, "u", tuple(g.shape), g.dtype, g.device)
+    _expect(out, "out", None, g.dtype, g.device, numel=g.numel())
     if out is None:
         out = torch.empty_like(g)
     _check("silu_mul", _lib.silu_mul(_dev(g, "g"), _dev(u, "u"), g.numel(), _dt(g), _dev(out, "out"),
@@ -374,7 +433,10 @@ def silu_mul(g: torch.Tensor, u: torch.Tensor, out: Optional[torch.Tensor] = Non
 
 
 def softmax(S: torch.Tensor, causal: int = 0, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    if S.dim() != 3:
+        raise ValueError(f"S has shape {list(S.shape)}, expected [BH, Lq, Lk]")
     BH, Lq, Lk = S.shape
+    _expect(out, "out", tuple(S.shape), S.dtype, S.device)
     if out is None:
         out = torch.empty_like(S)
     _check("softmax", _lib.softmax(_dev(S, "S"), BH, Lq, Lk, int(causal), _dt(S), _dev(out, "out"),
@@ -386,15 +448,30 @@ def gemm(A: torch.Tensor, B, bias: Optional[torch.Tensor] = None, b_layout: int 
          a_causal: bool = False, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """C = A . B (+ bias).  B is a tensor ([K, N] for b_layout 0, [N, K] for 1, optionally
     batched) or a PreparedLinear (b_layout 2: the packed weights of ln_linear_prepare)."""
+    if A.dim() not in (2, 3):
+        raise ValueError(f"A has shape {list(A.shape)}, expected [M, K] or [batch, M, K]")
     squeeze = A.dim() == 2
     A3 = A.unsqueeze(0) if squeeze else A
     batch, M, K = A3.shape
     if isinstance(B, PreparedLinear):
-        b_layout, N, bptr = 2, B.N, _dev(B.packed, "B")
+        if B.K != K or _TORCH_DT.get(B.desc.dtype) != A.dtype:
+            raise ValueError(f"the prepared weights are [{B.K}, {B.N}] of dtype {_TORCH_DT.get(B.desc.dtype)}; "
+                             f"A is [*, {K}] of dtype {A.dtype}")
+        if batch != 1:
+            raise ValueError("prepared (packed) weights take an unbatched A")
+        _expect(B.packed, "B", None, None, A.device)
+        b_layout, N = 2, B.N
+        bptr = None
     else:
+        if b_layout not in (0, 1) or B.dim() not in (2, 3):
+            raise ValueError("B must be [K, N] (b_layout 0) or [N, K] (b_layout 1), optionally batched")
         B3 = B.unsqueeze(0) if B.dim() == 2 else B
         N = B3.shape[2] if b_layout == 0 else B3.shape[1]
-        bptr = _dev(B3, "B")
+        _expect(B3, "B", (batch, K, N) if b_layout == 0 else (batch, N, K), A.dtype, A.device)
+        bptr = None
+    _expect(bias, "bias", (N,), A.dtype, A.device)
+    _expect(out, "out", (batch, M, N), A.dtype, A.device)
+    bptr = _dev(B.packed, "B") if isinstance(B, PreparedLinear) else _dev(B3, "B")
     if out is None:
         out = torch.empty((batch, M, N), dtype=A.dtype, device=A.device)
     _check("gemm", _lib.gemm(_dev(A3, "A"), bptr, _dev(bias, "bias"), batch, M, K, N, int(b_layout),

@@ -247,3 +247,121 @@ def test_binding_rejects_host_tensors():
     with pytest.raises(ValueError):
         ops.layernorm(torch.zeros(4, 64, dtype=torch.bfloat16), torch.ones(64, dtype=torch.bfloat16),
                       out=torch.zeros(4, 64, dtype=torch.bfloat16))
+
+
+# ------------------------------------------------------------------ the binding's shape checks
+# The C ABI sees raw pointers and sizes, so a mis-shaped tensor would reach the GPU as an
+# out-of-bounds access.  The binding checks every tensor against the sizes it passes before
+# taking any pointer; these calls use host tensors and fail on the shape (or dtype), never
+# reaching the device check or the library.
+def _bf(*shape):
+    import torch
+    return torch.zeros(*shape, dtype=torch.bfloat16)
+
+
+def _prepared(K, N, dtype=1):
+    import torch
+    return ops.PreparedLinear(torch.zeros(64, dtype=torch.uint8), ops.LnLinearWeights(K, N, dtype, 2, None))
+
+
+@pytest.mark.parametrize("fn", ["ln_linear_deferred", "rms_linear_deferred", "rms_swiglu_deferred",
+                                "ln_linear_serial", "ln_linear_norm_on_load"])
+def test_binding_checks_ln_shapes(fn):
+    import torch
+    f = getattr(ops, fn)
+    w = _prepared(64, 32)
+    with pytest.raises(ValueError, match="x has shape"):
+        f(_bf(4, 72), w)                                   # K differs from the weights'
+    with pytest.raises(ValueError, match="x has shape"):
+        f(_bf(4, 8, 8), w)                                 # not 2-D
+    with pytest.raises(ValueError, match="x has dtype"):
+        f(torch.zeros(4, 64), w)                           # fp32 x, bf16 weights
+    with pytest.raises(ValueError, match="out has shape"):
+        f(_bf(4, 64), w, out=_bf(4, 16))
+    with pytest.raises(ValueError, match="out has shape"):
+        f(_bf(4, 64), w, out=_bf(5, 32))
+    with pytest.raises(ValueError, match="out has dtype"):
+        f(_bf(4, 64), w, out=torch.zeros(4, 32))
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        f(_bf(4, 64), w, out=_bf(4, 32))                   # shapes right: only the device is wrong
+    if fn in ("ln_linear_serial", "ln_linear_norm_on_load"):
+        with pytest.raises(ValueError, match="stats has"):
+            f(_bf(4, 64), w, stats=torch.zeros(6))
+        with pytest.raises(ValueError, match="stats has dtype"):
+            f(_bf(4, 64), w, stats=torch.zeros(8, dtype=torch.float64))
+
+
+def test_binding_checks_post_and_prepare_shapes():
+    import torch
+    w = _prepared(64, 32)
+    g = _bf(64)
+    with pytest.raises(ValueError, match="gamma has shape"):
+        ops.linear_deferred_post(_bf(4, 64), w, _bf(63))
+    with pytest.raises(ValueError, match="beta has shape"):
+        ops.linear_deferred_post(_bf(4, 64), w, g, _bf(32))
+    with pytest.raises(ValueError, match="y has shape"):
+        ops.linear_deferred_post(_bf(4, 64), w, g, y=_bf(4, 32))
+    with pytest.raises(ValueError, match="stats has"):
+        ops.linear_deferred_post(_bf(4, 64), w, g, stats=torch.zeros(4))
+    with pytest.raises(ValueError, match="gamma has shape"):
+        ops.ln_linear_prepare(_bf(64, 32), _bf(32))
+    with pytest.raises(ValueError, match="bias has shape"):
+        ops.ln_linear_prepare(_bf(64, 32), _bf(64), None, _bf(64))
+    with pytest.raises(ValueError, match="gamma has dtype"):
+        ops.ln_linear_prepare(_bf(64, 32), torch.ones(64))
+    with pytest.raises(ValueError, match="W_up has shape"):
+        ops.swiglu_prepare(_bf(64, 32), _bf(64, 24), _bf(64))
+    with pytest.raises(ValueError, match="gamma has shape"):
+        ops.swiglu_prepare(_bf(64, 32), _bf(64, 32), _bf(32))
+
+
+def test_binding_checks_softmax_and_attention_shapes():
+    import torch
+    with pytest.raises(ValueError, match="V has shape"):
+        ops.softmax_pv_deferred(_bf(2, 64, 128), _bf(2, 64, 64))       # V rows != Lk
+    with pytest.raises(ValueError, match="V has shape"):
+        ops.softmax_pv_deferred(_bf(2, 64, 64), _bf(1, 64, 64))        # heads differ
+    with pytest.raises(ValueError, match="V has dtype"):
+        ops.softmax_pv_deferred(_bf(2, 64, 64), torch.zeros(2, 64, 64))
+    with pytest.raises(ValueError, match="out has shape"):
+        ops.softmax_pv_deferred(_bf(2, 64, 64), _bf(2, 64, 128), out=_bf(2, 64, 64))
+    with pytest.raises(ValueError, match="out has shape"):
+        ops.softmax(_bf(2, 64, 64), out=_bf(2, 64, 32))
+    for call in (ops.attention_deferred, ops.attention_decode_deferred):
+        with pytest.raises(ValueError, match="K has shape"):
+            call(_bf(4, 1, 128), _bf(4, 100, 64), _bf(4, 100, 64))     # head dims differ
+        with pytest.raises(ValueError, match="V has shape"):
+            call(_bf(4, 1, 128), _bf(4, 100, 128), _bf(4, 90, 128))
+        with pytest.raises(ValueError, match="multiple of the key/value heads"):
+            call(_bf(6, 1, 128), _bf(4, 100, 128), _bf(4, 100, 128))
+        with pytest.raises(ValueError, match="out has shape"):
+            call(_bf(4, 1, 128), _bf(4, 100, 128), _bf(4, 100, 128), out=_bf(4, 2, 128))
+    with pytest.raises(ValueError, match="workspace has dtype"):
+        ops.attention_decode_deferred(_bf(4, 1, 128), _bf(4, 100, 128), _bf(4, 100, 128),
+                                      workspace=torch.zeros(16))
+
+
+def test_binding_checks_norm_and_gemm_shapes():
+    import torch
+    with pytest.raises(ValueError, match="gamma has shape"):
+        ops.layernorm(_bf(4, 64), _bf(32))
+    with pytest.raises(ValueError, match="beta has shape"):
+        ops.layernorm(_bf(4, 64), _bf(64), _bf(32))
+    with pytest.raises(ValueError, match="out has shape"):
+        ops.rmsnorm(_bf(4, 64), _bf(64), out=_bf(4, 32))
+    with pytest.raises(ValueError, match="u has shape"):
+        ops.silu_mul(_bf(4, 64), _bf(4, 32))
+    with pytest.raises(ValueError, match="B has shape"):
+        ops.gemm(_bf(4, 64), _bf(32, 16))                  # [K, N] with K != A's K
+    with pytest.raises(ValueError, match="B has shape"):
+        ops.gemm(_bf(2, 4, 64), _bf(3, 64, 16))            # batch differs
+    with pytest.raises(ValueError, match="B has shape"):
+        ops.gemm(_bf(4, 64), _bf(16, 32), b_layout=1)      # [N, K] with K != 64
+    with pytest.raises(ValueError, match="bias has shape"):
+        ops.gemm(_bf(4, 64), _bf(64, 16), bias=_bf(32))
+    with pytest.raises(ValueError, match="out has shape"):
+        ops.gemm(_bf(4, 64), _bf(64, 16), out=_bf(1, 4, 8))
+    with pytest.raises(ValueError, match="prepared"):
+        ops.gemm(_bf(4, 72), _prepared(64, 16))
+    with pytest.raises(ValueError, match="B has dtype"):
+        ops.gemm(_bf(4, 64), torch.zeros(64, 16))

@@ -1,9 +1,11 @@
 """GPU parity: the HIP path, called through the C ABI, against the fp64 oracle.
 
 Small cases span several tiles and ragged tails; the named workloads run at
-full size in the bench's launch configuration and are checked on sampled
-rows the oracle computes one by one.
+full size in the bench's launch configuration and every output row is
+compared with the oracle.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -41,6 +43,36 @@ def _ln_check(ops, case, rows=None, tol=None):
     print(f"{name} {tuple(case['x'].shape)}x{tuple(case['W'].shape)} {case['x'].dtype}: err={err:.3e}")
     assert err <= (tol or TOL[case["x"].dtype]), err
     return out, w
+
+
+# Full-row checks of the large workloads: the oracle's normalization in C, the product as one
+# fp64 library matmul (oracle.norm_linear_matmul), compared chunk by chunk over every row.
+ORACLE_THREADS = min(16, len(os.sched_getaffinity(0)))
+
+
+def _all_rows_err(got, ref_rows, M, chunk):
+    err = 0.0
+    for r0 in range(0, M, chunk):
+        r1 = min(M, r0 + chunk)
+        err = max(err, rowwise_rel_err(got[r0:r1], ref_rows(r0, r1)))
+    return err
+
+
+def _ln_check_all_rows(ops, case, name, chunk=1024):
+    rms = case.get("norm") == "rms"
+    x, W = cuda(case["x"]), cuda(case["W"])
+    w = ops.ln_linear_prepare(W, cuda(case["gamma"]), cuda(case["beta"]), cuda(case["bias"]))
+    del W
+    out = (ops.rms_linear_deferred if rms else ops.ln_linear_deferred)(x, w, case["eps"])
+    got = out.cpu()
+    del out, w, x
+    W64 = oracle.to_f64(case["W"])
+    M = case["x"].shape[0]
+    err = _all_rows_err(got, lambda r0, r1: oracle.norm_linear_matmul(
+        case["x"][r0:r1], case["gamma"], case["beta"], W64, case["bias"], case["eps"], rms=rms,
+        nthreads=ORACLE_THREADS), M, chunk)
+    print(f"{name}: all {M} rows, err={err:.3e}", flush=True)
+    assert err <= TOL[case["x"].dtype], err
 
 
 # ---------------------------------------------------------------------------- LN -> Linear
@@ -94,16 +126,16 @@ def test_ln_linear_constant_rows_give_b(ops):
 
 
 @pytest.mark.parametrize("M,K,N", [(4000, 544, 4104), (4000, 520, 4104), (4096, 4096, 4096)])
-def test_ln_linear_bf16_large_tiles_sampled(ops, M, K, N):
+def test_ln_linear_bf16_large_tiles(ops, M, K, N):
     # >= 256 output tiles of 256x256: the pipelined main loop with ragged M and N (K % 32 == 0);
     # K = 520 takes the 128x128 loop with its K tail
     case = I.make_ln_case(M, K, N, "bf16", seed=M % 97, outliers=3)
-    _ln_check(ops, case, rows=I.sample_rows(M, 40, seed=1) + 0)
+    _ln_check(ops, case)
 
 
 @pytest.mark.parametrize("M,K,N,layout", [(4104, 320, 4096, 2), (4104, 264, 4096, 2), (4104, 264, 4096, 1),
                                            (300, 136, 264, 2), (257, 512, 1032, 2)])
-def test_gemm_sampled(ops, M, K, N, layout):
+def test_gemm_large(ops, M, K, N, layout):
     # layout 2 (packed weights, gamma = 1) with K % 64 == 0 runs the pipelined loop, on
     # 256 x 256 tiles at 4104 rows and on 128 x 128 tiles at 257 x 1032 (27 tiles);
     # K = 264 and K = 136 run the two-stage 128 x 128 loop
@@ -116,9 +148,8 @@ def test_gemm_sampled(ops, M, K, N, layout):
     else:
         Bd = cuda(B.t().contiguous())
     C = ops.gemm(cuda(A), Bd, cuda(bias), b_layout=layout)
-    rows = I.sample_rows(M, 32, seed=2)
-    ref = oracle.linear(A[torch.as_tensor(rows)], B, bias)
-    assert rowwise_rel_err(C.cpu()[torch.as_tensor(rows)], ref) <= TOL[torch.bfloat16]
+    ref = oracle.to_f64(A) @ oracle.to_f64(B) + oracle.to_f64(bias)
+    assert rowwise_rel_err(C.cpu(), ref) <= TOL[torch.bfloat16]
 
 
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 520), (5, 8200, 264), (16, 512, 72), (3, 8, 8), (17, 1024, 520),
@@ -143,17 +174,14 @@ def test_gemm_packed_f32(ops):
     assert rowwise_rel_err(C.cpu(), oracle.linear(A, B)) <= TOL[torch.float32]
 
 
-def test_ln_linear_ffn_prefill_workload_sampled(ops):
-    # the 8192 x 8192 x 28672 up-projection at full size (the 256x256 kernel, 14 waves of tiles)
-    w = I.LN_FFN_PREFILL
-    case = I.make_ln(w)
-    _ln_check(ops, case, rows=I.sample_rows(w.M, 16, seed=5))
+def test_ln_linear_ffn_prefill_workload_all_rows(ops):
+    # the 8192 x 8192 x 28672 up-projection at full size in the bench's launch configuration
+    # (the 256x256 kernel, 14 column tiles per workgroup), every row against the oracle
+    _ln_check_all_rows(ops, I.make_ln(I.LN_FFN_PREFILL), "ln_linear_deferred ffn prefill 8192x8192x28672")
 
 
-def test_ln_linear_qkv_workload_sampled(ops):
-    w = I.LN_QKV
-    case = I.make_ln(w)
-    _ln_check(ops, case, rows=I.sample_rows(w.M, 24, seed=3))
+def test_ln_linear_qkv_workload_all_rows(ops):
+    _ln_check_all_rows(ops, I.make_ln(I.LN_QKV), "ln_linear_deferred qkv 4096x4096x12288")
 
 
 @pytest.mark.parametrize("t", [1, 4, 8, 16])
@@ -162,12 +190,11 @@ def test_ln_linear_ffn_decode_workload(ops, t):
 
 
 @pytest.mark.parametrize("t", [32, 128, 1024])
-def test_ln_linear_qkv_tokens_workload_sampled(ops, t):
+def test_ln_linear_qkv_tokens_workload_all_rows(ops, t):
     # the QKV projection at the bench's batched-decode and prefill-chunk sizes, in the
     # launch configurations it times: 2 and 8 row fragments of the streaming kernel, and
     # 4 x 48 tiles of 256 x 256 (one tile per workgroup, each reducing its rows' moments)
-    w = I.ln_qkv_tokens(t)
-    _ln_check(ops, I.make_ln(w), rows=I.sample_rows(w.M, min(w.M, 24), seed=t))
+    _ln_check_all_rows(ops, I.make_ln(I.ln_qkv_tokens(t)), f"ln_linear_deferred qkv {t} tokens")
 
 
 def test_ln_linear_deterministic(ops):
@@ -189,6 +216,48 @@ def test_ln_linear_guard_band(ops):
     assert (buf[:512] == 7.0).all() and (buf[-512:] == 7.0).all()
 
 
+# Non-finite inputs propagate as in the plain definition (Eq. (1)-(2), Eq. (6)): a row holding
+# NaN, +inf or -inf gives an all-NaN output row and leaves every other row untouched; with
+# eps = 0 a constant row (LayerNorm: zero variance) or an all-zero row (RMSNorm) gives 0/0 = NaN.
+# The shapes take every kernel: fp32 tiles, the 128 x 128 two-stage loop (K % 64 != 0), the
+# pipelined 128 x 128 and 256 x 256 kernels, and the decode kernel with 1 and 3 row fragments.
+NONFINITE_SHAPES = [(37, 104, 72, "f32"), (200, 520, 392, "bf16"), (300, 256, 4104, "bf16"),
+                    (520, 256, 8200, "bf16"), (5, 1024, 520, "bf16"), (40, 1024, 520, "bf16")]
+
+
+@pytest.mark.parametrize("M,K,N,dtype", NONFINITE_SHAPES)
+@pytest.mark.parametrize("norm", ["layernorm", "rms"])
+def test_ln_linear_nonfinite_rows(ops, M, K, N, dtype, norm):
+    case = I.make_ln_case(M, K, N, dtype, seed=M + N, outliers=2, norm=norm)
+    x = case["x"].clone()
+    x[1, K // 3] = float("nan")
+    x[2, K - 1] = float("inf")
+    x[M - 1, 0] = float("-inf")
+    case["x"] = x
+    out, _ = _ln_check(ops, case)
+    o = out.cpu().float()
+    assert torch.isnan(o[[1, 2, M - 1]]).all() and torch.isfinite(o[3:M - 1]).all()
+
+
+@pytest.mark.parametrize("M,K,N,dtype", NONFINITE_SHAPES)
+@pytest.mark.parametrize("norm", ["layernorm", "rms"])
+def test_ln_linear_eps0_degenerate_rows(ops, M, K, N, dtype, norm):
+    case = I.make_ln_case(M, K, N, dtype, seed=M + K, norm=norm)
+    case["eps"] = 0.0
+    x = case["x"].clone()
+    # values whose sums and squares are exact in fp32, so the one-pass variance is exactly 0
+    if norm == "rms":
+        x[0] = 0
+        x[M - 1] = 0
+    else:
+        x[0] = 0.75
+        x[M - 1] = -1.5
+    case["x"] = x
+    out, _ = _ln_check(ops, case)
+    o = out.cpu().float()
+    assert torch.isnan(o[[0, M - 1]]).all() and torch.isfinite(o[1:M - 1]).all()
+
+
 # ---------------------------------------------------------------------------- ablations
 @pytest.mark.parametrize("M,K,N,dtype", [(37, 104, 72, "f32"), (257, 1024, 264, "bf16"), (5, 1024, 520, "bf16"),
                                          (4000, 544, 4104, "bf16")])
@@ -197,11 +266,8 @@ def test_ln_linear_centered_weight(ops, M, K, N, dtype):
     case = I.make_ln_case(M, K, N, dtype, seed=M + 3, outliers=2)
     w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]), centered=True)
     out = ops.ln_linear_deferred(cuda(case["x"]), w, case["eps"])
-    rows = None if M < 1000 else I.sample_rows(M, 24, seed=8)
-    xs = case["x"] if rows is None else case["x"][torch.as_tensor(rows)]
-    ref = oracle.ln_linear(xs, case["gamma"], case["beta"], case["W"], None, case["eps"])
-    got = out.cpu() if rows is None else out.cpu()[torch.as_tensor(rows)]
-    assert rowwise_rel_err(got, ref) <= TOL[case["x"].dtype]
+    ref = oracle.ln_linear(case["x"], case["gamma"], case["beta"], case["W"], None, case["eps"])
+    assert rowwise_rel_err(out.cpu(), ref) <= TOL[case["x"].dtype]
 
 
 def test_centered_weight_loses_accuracy_on_offset_rows(ops):
@@ -226,11 +292,8 @@ def test_ln_linear_serial_stats(ops, M, K, N, dtype):
     w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
     stats = torch.empty(2 * M, dtype=torch.float32, device="cuda")
     out = ops.ln_linear_serial(cuda(case["x"]), w, case["eps"], stats=stats)
-    rows = None if M < 1000 else I.sample_rows(M, 24, seed=9)
-    xs = case["x"] if rows is None else case["x"][torch.as_tensor(rows)]
-    ref = oracle.ln_linear(xs, case["gamma"], case["beta"], case["W"], None, case["eps"])
-    got = out.cpu() if rows is None else out.cpu()[torch.as_tensor(rows)]
-    assert rowwise_rel_err(got, ref) <= TOL[case["x"].dtype]
+    ref = oracle.ln_linear(case["x"], case["gamma"], case["beta"], case["W"], None, case["eps"])
+    assert rowwise_rel_err(out.cpu(), ref) <= TOL[case["x"].dtype]
     st = stats.cpu().double().numpy().reshape(M, 2)
     xd = oracle.to_f64(case["x"])
     np.testing.assert_allclose(st[:, 0], xd.mean(1), rtol=1e-4, atol=1e-5)
@@ -246,23 +309,22 @@ def test_ln_linear_norm_on_load(ops, M, K, N, offset):
     w = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
     stats = torch.empty(2 * M, dtype=torch.float32, device="cuda")
     out = ops.ln_linear_norm_on_load(cuda(case["x"]), w, case["eps"], stats=stats)
-    rows = I.sample_rows(M, 32, seed=10)
-    ref = oracle.ln_linear(case["x"][torch.as_tensor(rows)], case["gamma"], case["beta"], case["W"], None,
-                           case["eps"])
-    err = rowwise_rel_err(out.cpu()[torch.as_tensor(rows)], ref)
+    ref = oracle.norm_linear_matmul(case["x"], case["gamma"], case["beta"], case["W"], None, case["eps"])
+    err = rowwise_rel_err(out.cpu(), ref)
     print(f"ln_linear_norm_on_load {M}x{K}x{N} offset {offset}: err={err:.3e}")
     assert err <= TOL[torch.bfloat16], err
 
 
-def test_ln_linear_norm_on_load_qkv_workload_sampled(ops):
+def test_ln_linear_norm_on_load_qkv_workload_all_rows(ops):
     w = I.LN_QKV
     case = I.make_ln(w)
     prep = ops.ln_linear_prepare(cuda(case["W"]), cuda(case["gamma"]), cuda(case["beta"]))
-    out = ops.ln_linear_norm_on_load(cuda(case["x"]), prep, case["eps"])
-    rows = I.sample_rows(w.M, 24, seed=13)
-    ref = oracle.ln_linear(case["x"][torch.as_tensor(rows)], case["gamma"], case["beta"], case["W"], None,
-                           case["eps"])
-    assert rowwise_rel_err(out.cpu()[torch.as_tensor(rows)], ref) <= TOL[torch.bfloat16]
+    got = ops.ln_linear_norm_on_load(cuda(case["x"]), prep, case["eps"]).cpu()
+    W64 = oracle.to_f64(case["W"])
+    err = _all_rows_err(got, lambda r0, r1: oracle.norm_linear_matmul(
+        case["x"][r0:r1], case["gamma"], case["beta"], W64, None, case["eps"], nthreads=ORACLE_THREADS), w.M, 1024)
+    print(f"ln_linear_norm_on_load qkv: all {w.M} rows, err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
 
 
 def test_ln_linear_norm_on_load_rejects_small_shapes(ops):
@@ -287,9 +349,7 @@ def test_linear_deferred_post(ops, M, K, N, dtype, norm):
     w = ops.ln_linear_prepare(cuda(case["W"]), g, b, cuda(case["bias"]))
     out, y, st = ops.linear_deferred_post(cuda(case["x"]), w, g, None if rms else b, case["eps"], rms=rms)
     torch.cuda.synchronize()
-    rows = None if M < 1000 else I.sample_rows(M, 24, seed=8)
-    pick = (lambda t: t) if rows is None else (lambda t: t[torch.as_tensor(rows)])
-    xs = pick(case["x"])
+    xs = case["x"]
     if rms:
         ref = oracle.rms_linear(xs, case["gamma"], case["W"], case["bias"], case["eps"])
         yref = oracle.rmsnorm(xs, case["gamma"], case["eps"])
@@ -297,10 +357,10 @@ def test_linear_deferred_post(ops, M, K, N, dtype, norm):
         ref = oracle.ln_linear(xs, case["gamma"], case["beta"], case["W"], case["bias"], case["eps"])
         yref = oracle.layernorm(xs, case["gamma"], case["beta"], case["eps"])
     tol = TOL[case["x"].dtype]
-    e_out, e_y = rowwise_rel_err(pick(out.cpu()), ref), rowwise_rel_err(pick(y.cpu()), yref)
+    e_out, e_y = rowwise_rel_err(out.cpu(), ref), rowwise_rel_err(y.cpu(), yref)
     print(f"linear_deferred_post {M}x{K}x{N} {dtype} {norm}: out err={e_out:.3e}, y err={e_y:.3e}")
     assert e_out <= tol and e_y <= (tol if dtype == "f32" else tol / 4)
-    sd = pick(st.cpu().double().reshape(M, 2)).numpy()
+    sd = st.cpu().double().reshape(M, 2).numpy()
     xd = oracle.to_f64(xs)
     mean = np.zeros(len(xd)) if rms else xd.mean(1)
     var = (xd * xd).mean(1) if rms else xd.var(1)
@@ -336,14 +396,13 @@ def test_rms_linear_bf16_decode_shapes(ops, M, K, N):
 
 
 @pytest.mark.parametrize("M,K,N", [(4000, 544, 4104), (4000, 520, 4104)])
-def test_rms_linear_bf16_large_tiles_sampled(ops, M, K, N):
+def test_rms_linear_bf16_large_tiles(ops, M, K, N):
     case = I.make_ln_case(M, K, N, "bf16", seed=M % 89, outliers=3, norm="rms")
-    _ln_check(ops, case, rows=I.sample_rows(M, 40, seed=4))
+    _ln_check(ops, case)
 
 
-def test_rms_linear_qkv_workload_sampled(ops):
-    w = I.RMS_QKV
-    _ln_check(ops, I.make_ln(w), rows=I.sample_rows(w.M, 24, seed=5))
+def test_rms_linear_qkv_workload_all_rows(ops):
+    _ln_check_all_rows(ops, I.make_ln(I.RMS_QKV), "rms_linear_deferred qkv 4096x4096x6144")
 
 
 def test_rms_linear_ffn_decode_workload(ops):
@@ -395,24 +454,32 @@ def test_rms_swiglu_bf16_ragged(ops, M, K, N):
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M + K, outliers=2))
 
 
-@pytest.mark.parametrize("M", [1, 8, 9, 16, 17, 48, 64, 65, 96, 97, 128])
+@pytest.mark.parametrize("M", [1, 8, 9, 16, 17, 33, 48, 49, 63, 64, 65, 96, 97, 128])
 @pytest.mark.parametrize("K,N", [(1024, 520), (8, 24)])
 def test_rms_swiglu_bf16_decode_shapes(ops, M, K, N):
-    # one gate/up pair per workgroup, 1-8 row fragments; N = 520 / 24 leave a partial pair group
+    # 1-7 gate/up pairs per workgroup, 1-8 row fragments (33, 49 and 63 rows leave the last
+    # fragment partial under the two-pair layout); N = 520 / 24 leave a partial pair group
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M * 3 + 1, outliers=4))
 
 
 @pytest.mark.parametrize("M,K,N", [(4000, 544, 2056), (4000, 520, 2056)])
-def test_rms_swiglu_bf16_large_tiles_sampled(ops, M, K, N):
+def test_rms_swiglu_bf16_large_tiles(ops, M, K, N):
     # 2 x 2056 packed columns: 16 x 17 tiles of 256 x 256 (pipelined loop, ragged M and N); K = 520
     # takes the 128 x 128 loop
-    _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M % 83, outliers=3),
-                  rows=I.sample_rows(M, 32, seed=6))
+    _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M % 83, outliers=3))
 
 
-def test_rms_swiglu_prefill_workload_sampled(ops):
+def test_rms_swiglu_prefill_workload_all_rows(ops):
     w = I.SWIGLU_PREFILL
-    _swiglu_check(ops, I.make_swiglu(w), rows=I.sample_rows(w.M, 12, seed=7))
+    case = I.make_swiglu(w)
+    pw = ops.swiglu_prepare(cuda(case["Wg"]), cuda(case["Wu"]), cuda(case["gamma"]))
+    got = ops.rms_swiglu_deferred(cuda(case["x"]), pw, case["eps"]).cpu()
+    del pw
+    Wg, Wu = oracle.to_f64(case["Wg"]), oracle.to_f64(case["Wu"])
+    err = _all_rows_err(got, lambda r0, r1: oracle.rms_swiglu_matmul(
+        case["x"][r0:r1], case["gamma"], Wg, Wu, case["eps"], nthreads=ORACLE_THREADS), w.M, 1024)
+    print(f"rms_swiglu_deferred prefill 4096x4096x2x14336: all {w.M} rows, err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
 
 
 def test_rms_swiglu_decode_workload(ops):
@@ -472,11 +539,35 @@ def test_softmax_pv_ragged(ops, BH, L, d, causal):
     _sm_check(ops, I.make_sm_case(BH, L, d, causal, seed=L, from_qk=causal))
 
 
-def test_softmax_pv_causal_workload_sampled(ops):
+def test_softmax_pv_causal_workload_all_rows(ops):
+    # the causal 32 x 8192 x 8192, d = 128 workload in the bench's launch configuration; every
+    # row of every head against the oracle, one head at a time
     w = I.SM_CAUSAL
     case = I.make_sm(w)
-    rows = I.sample_rows(w.BH * w.L, 48, seed=5)
-    _sm_check(ops, case, rows=rows)
+    out = ops.softmax_pv_deferred(cuda(case["S"]), cuda(case["V"]), causal=True)
+    got = out.cpu()
+    del out
+    err, qpos = 0.0, np.arange(w.L)
+    for h in range(w.BH):
+        ref = oracle.softmax_pv(case["S"][h], case["V"][h], qpos=qpos, nthreads=ORACLE_THREADS)
+        err = max(err, rowwise_rel_err(got[h], ref))
+    print(f"softmax_pv_deferred causal 32x8192x8192 d128: all {w.BH * w.L} rows, err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
+
+
+@pytest.mark.parametrize("BH,Lq,Lk,d", [(2, 100, 300, 64), (3, 300, 72, 128), (1, 7, 1000, 128),
+                                        (2, 257, 520, 64)])
+def test_softmax_pv_cross_lengths(ops, BH, Lq, Lk, d):
+    # non-causal with Lq != Lk: every query row takes all Lk keys (Eq. (7) per row)
+    case = I.make_sm_case(BH, max(Lq, Lk), d, False, seed=Lq + Lk)
+    S = case["S"][:, :Lq, :Lk].contiguous()
+    V = case["V"][:, :Lk].contiguous()
+    out = ops.softmax_pv_deferred(cuda(S), cuda(V))
+    torch.cuda.synchronize()
+    ref = oracle.softmax_pv(S.reshape(BH * Lq, Lk), V, head=np.repeat(np.arange(BH), Lq))
+    err = rowwise_rel_err(out.cpu().reshape(BH * Lq, d), ref)
+    print(f"softmax_pv_deferred S{tuple(S.shape)} V{tuple(V.shape)}: err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
 
 
 def test_softmax_pv_causal_row0_exact(ops):
@@ -574,11 +665,22 @@ def test_attention_matches_softmax_pv_on_materialized_scores(ops):
     assert rowwise_rel_err(a.cpu().reshape(-1, 128), oracle.to_f64(b.cpu()).reshape(-1, 128)) <= TOL[torch.bfloat16]
 
 
-def test_attention_causal_workload_sampled(ops):
+def test_attention_causal_workload_all_rows(ops):
+    # causal 32 x 8192 x 8192, d = 128 with the scores formed in the kernel; every row of
+    # every head against the oracle, one head at a time
     w = I.ATTN_CAUSAL
     case = I.make_qkv(w)
-    rows = I.sample_rows(w.BH * w.L, 48, seed=11)
-    _attn_check(ops, case, rows=rows)
+    out = ops.attention_deferred(cuda(case["Q"]), cuda(case["K"]), cuda(case["V"]), causal=True,
+                                 scale=case["scale"])
+    got = out.cpu()
+    del out
+    err, qpos = 0.0, np.arange(w.L)
+    for h in range(w.BH):
+        ref = oracle.attention(case["Q"][h], case["K"][h], case["V"][h], case["scale"], qpos=qpos,
+                               nthreads=ORACLE_THREADS)
+        err = max(err, rowwise_rel_err(got[h], ref))
+    print(f"attention_deferred causal 32x8192x8192 d128: all {w.BH * w.L} rows, err={err:.3e}")
+    assert err <= TOL[torch.bfloat16], err
 
 
 # ---------------------------------------------------------------------------- decode attention (split keys + merge)
@@ -659,9 +761,8 @@ def test_attention_decode_grouped_query(ops, BH, g, Lq, Lk, d):
     _decode_gqa_check(ops, I.make_decode_case(BH, Lq, Lk, d, seed=BH + g, group=g))
 
 
-def test_attention_decode_gqa_workload_sampled(ops):
-    w = I.ATTN_DECODE_GQA
-    _decode_gqa_check(ops, I.make_decode(w), heads=[0, 5, 100, 200, w.BH - 1])
+def test_attention_decode_gqa_workload_all_heads(ops):
+    _decode_gqa_check(ops, I.make_decode(I.ATTN_DECODE_GQA))
 
 
 def test_attention_deterministic(ops):
@@ -674,13 +775,9 @@ def test_attention_deterministic(ops):
     assert torch.equal(ops.attention_decode_deferred(q, k, v), ops.attention_decode_deferred(q, k, v))
 
 
-def test_attention_decode_workload_sampled(ops):
-    # the benchmarked decode workload at full size, in its own launch configuration; the
-    # oracle computes a sample of heads (the GPU runs every head)
-    w = I.ATTN_DECODE
-    heads = [0, 1, 77, 128, 200, w.BH - 1]
-    case = I.make_decode(w)
-    _decode_check(ops, case, heads=heads)
+def test_attention_decode_workload_all_heads(ops):
+    # the benchmarked decode workload at full size, in its own launch configuration, every head
+    _decode_check(ops, I.make_decode(I.ATTN_DECODE))
 
 
 # ---------------------------------------------------------------------------- unfused comparators

@@ -208,6 +208,25 @@ def test_rms_swiglu_matches_torch(M, K, N, eps):
     np.testing.assert_allclose(oracle.rms_swiglu(x, gamma, Wg, Wu, eps), want.numpy(), rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("M,K,N,eps", [(5, 7, 3, 1e-5), (13, 64, 17, 0.1), (2, 1, 4, 0.0)])
+def test_matmul_step_entries_match_plain_rows(M, K, N, eps):
+    # the library-matmul entries used for full-row checks of the large workloads equal the plain
+    # row loops (ln_linear, rms_linear, rms_swiglu, themselves pinned above) to rounding; a
+    # transposed W, a dropped bias or a swapped gate/up fails here
+    rng = np.random.default_rng(M + 7 * K + 11 * N)
+    x = rng.normal(size=(M, K)) * 3 + 0.5
+    gamma, beta = rng.uniform(0.5, 1.5, K), rng.normal(size=K) * 0.1
+    W, Wu, bias = rng.normal(size=(K, N)), rng.normal(size=(K, N)), rng.normal(size=N)
+    np.testing.assert_allclose(oracle.norm_linear_matmul(x, gamma, beta, W, bias, eps),
+                               oracle.ln_linear(x, gamma, beta, W, bias, eps), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.norm_linear_matmul(x, gamma, None, W, None, eps, rms=True),
+                               oracle.rms_linear(x, gamma, W, None, eps), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.norm_linear_matmul(x, gamma, beta, W, bias, eps, rms=True),
+                               oracle.rms_linear(x, gamma, W, bias, eps, beta=beta), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.rms_swiglu_matmul(x, gamma, W, Wu, eps),
+                               oracle.rms_swiglu(x, gamma, W, Wu, eps), rtol=1e-12, atol=1e-12)
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_softmax_pv_matches_torch_softmax(causal):
     rng = np.random.default_rng(11)
