@@ -300,6 +300,23 @@ DN_API dn_status attention_decode_deferred(const void* Q, const void* K, const v
                                     void* workspace, size_t workspace_bytes, void* out,
                                     hipStream_t stream);
 
+/*
+ * For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): attention_decode_deferred
+ * with no workspace argument.  The key-range partials go to a 12 MiB device
+ * array that the library holds on each GPU it runs on until the process ends;
+ * no call allocates or frees memory.  Every request attention_decode_deferred
+ * accepts fits it (the partials stay below 10.6 MiB at d = 64 and 8.3 MiB at
+ * d = 128); a request that would not gives DN_ERR_UNSUPPORTED.  The array
+ * keeps the last call's partials, which every call overwrites before it reads
+ * them; calls that overlap on one GPU (concurrent streams) share it and race.
+ * Arguments, layout, grouped-query use and status codes as
+ * attention_decode_deferred; the output is bitwise the same.
+ */
+DN_API dn_status attention_decode_deferred_noalloc(const void* Q, const void* K, const void* V, int64_t BH,
+                                            int64_t Lq, int64_t Lk, int64_t d, float scale, int dtype,
+                                            void* out, hipStream_t stream);
+
 /* ======================================================================= */
 /* Unfused comparators: the conventional sub-graph of Fig. 1(a)             */
 /* ======================================================================= */

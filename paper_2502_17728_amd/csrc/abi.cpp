@@ -323,6 +323,23 @@ DN_API dn_status attention_decode_deferred(const void* Q, const void* K, const v
     return from_hip(dn::launch_attention_decode(Q, K, V, BH, Lq, Lk, d, scale, workspace, out, stream));
 }
 
+DN_API dn_status attention_decode_deferred_noalloc(const void* Q, const void* K, const void* V, int64_t BH,
+                                                   int64_t Lq, int64_t Lk, int64_t d, float scale, int dtype,
+                                                   void* out, hipStream_t stream) {
+    if (!Q || !K || !V || !out || BH < 1 || Lq < 1 || Lk < 1 || d < 1 || !valid_dtype(dtype))
+        return DN_ERR_INVALID_ARG;
+    if (!isfinite(scale) || !(scale > 0.f)) return DN_ERR_INVALID_ARG;
+    size_t qb, kb;
+    if (!bytes_of(BH, Lq, d * 2, &qb) || !bytes_of(BH, Lk, d * 2, &kb)) return DN_ERR_INVALID_ARG;
+    if (dtype != DN_BF16 || (d != 64 && d != 128) || Lq > 16) return DN_ERR_UNSUPPORTED;
+    if (Lk * d * 2 >= (int64_t(1) << 31)) return DN_ERR_UNSUPPORTED;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16)) return DN_ERR_MISALIGNED;
+    if (overlaps(out, qb, Q, qb) || overlaps(out, qb, K, kb) || overlaps(out, qb, V, kb)) return DN_ERR_INVALID_ARG;
+    if (BH * 16 > kMaxGridX) return DN_ERR_UNSUPPORTED;
+    if (dn::attention_decode_partials_bytes(BH, Lq, Lk, d) > dn::kDecodeScratchBytes) return DN_ERR_UNSUPPORTED;
+    return from_hip(dn::launch_attention_decode_noalloc(Q, K, V, BH, Lq, Lk, d, scale, out, stream));
+}
+
 static dn_status row_norm(const void* x, const void* gamma, const void* beta, int64_t M, int64_t K, float eps,
                           int rms, int dtype, void* y, hipStream_t stream) {
     if (!x || !gamma || !y || M < 1 || K < 1 || !valid_dtype(dtype)) return DN_ERR_INVALID_ARG;

@@ -38,6 +38,7 @@
 // combines them with weights 2^(m_g - m) -- the deferred division of Eq. (8)
 // postponed once more, past the reduction over key ranges.
 #include <algorithm>
+#include <mutex>
 
 #include "dn_device.hpp"
 #include "dn_launch.hpp"
@@ -433,6 +434,53 @@ hipError_t launch_attention_decode(const void* Q, const void* K, const void* V, 
                                    int64_t d, float scale, void* workspace, void* out, hipStream_t s) {
     if (d == 64) return run_attention_decode<64>(Q, K, V, BH, Lq, Lk, scale, (float*)workspace, out, s);
     return run_attention_decode<128>(Q, K, V, BH, Lq, Lk, scale, (float*)workspace, out, s);
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free decode: the per-split partials go to a file-scope device array
+// instead of a caller workspace.  Every valid call fits it: with nsplit > 1 the
+// heads number fewer than the resident workgroups W (1280 at d = 64, 512 at
+// d = 128), so BH * nsplit < 2 W and the partials take less than
+// 2 W * 16 * (d + 4) * 4 bytes -- 10.6 MiB at d = 64, 8.3 MiB at d = 128.
+// In host code `scratch` names a host-side stand-in; its device address (one
+// copy per GPU) is looked up once per device with hipGetSymbolAddress and only
+// that address is passed to kernels.
+static __device__ __align__(256) float scratch[kDecodeScratchBytes / sizeof(float)];
+
+static hipError_t decode_scratch_address(void** out) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));  // on the current device
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return hipSuccess;
+}
+
+size_t attention_decode_partials_bytes(int64_t BH, int64_t Lq, int64_t Lk, int64_t d) {
+    int nsplit;
+    int64_t kchunk;
+    attention_decode_split(BH, Lk, d, &nsplit, &kchunk);
+    return nsplit == 1 ? 0 : (size_t)BH * (size_t)Lq * (size_t)nsplit * (size_t)(d + 4) * sizeof(float);
+}
+
+hipError_t launch_attention_decode_noalloc(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,
+                                           int64_t Lk, int64_t d, float scale, void* out, hipStream_t s) {
+    void* part = nullptr;
+    if (attention_decode_partials_bytes(BH, Lq, Lk, d) > 0) {
+        const hipError_t e = decode_scratch_address(&part);
+        if (e != hipSuccess) return e;
+    }
+    return launch_attention_decode(Q, K, V, BH, Lq, Lk, d, scale, part, out, s);
 }
 
 hipError_t launch_attention_deferred(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,

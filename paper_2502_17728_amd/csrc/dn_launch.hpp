@@ -77,6 +77,14 @@ size_t attention_decode_workspace_bytes(int64_t BH, int64_t Lq, int64_t Lk, int6
 hipError_t launch_attention_decode(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq, int64_t Lk,
                                    int64_t d, float scale, void* workspace, void* out, hipStream_t s);
 
+// The same with the partials in a library-owned device array of kDecodeScratchBytes per GPU
+// (no workspace argument, no allocation).  attention_decode_partials_bytes: the bytes of
+// partials a call uses there (0 when the heads alone fill the chip and one pass suffices).
+constexpr size_t kDecodeScratchBytes = size_t(12) << 20;
+size_t attention_decode_partials_bytes(int64_t BH, int64_t Lq, int64_t Lk, int64_t d);
+hipError_t launch_attention_decode_noalloc(const void* Q, const void* K, const void* V, int64_t BH, int64_t Lq,
+                                           int64_t Lk, int64_t d, float scale, void* out, hipStream_t s);
+
 hipError_t launch_layernorm(const void* x, const void* gamma, const void* beta, int64_t M,
                             int64_t K, float eps, int rms, int dtype, void* y, hipStream_t s);
 

@@ -26,7 +26,7 @@ SYMBOLS = ("dn_status_string", "dn_version", "ln_linear_packed_bytes", "ln_linea
            "ln_linear_norm_on_load", "ln_linear_deferred_post", "rms_linear_deferred_post",
            "swiglu_packed_bytes", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
            "attention_deferred", "attention_gqa_deferred", "attention_decode_workspace_bytes",
-           "attention_decode_deferred", "layernorm",
+           "attention_decode_deferred", "attention_decode_deferred_noalloc", "layernorm",
            "rmsnorm", "silu_mul", "softmax", "gemm")
 
 
@@ -71,6 +71,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.attention_decode_workspace_bytes.argtypes = [i64, i64, i64, i64]
     lib.attention_decode_workspace_bytes.restype = ctypes.c_size_t
     lib.attention_decode_deferred.argtypes = [vp, vp, vp, i64, i64, i64, i64, f32, i32, vp, ctypes.c_size_t, vp, vp]
+    lib.attention_decode_deferred_noalloc.argtypes = [vp, vp, vp, i64, i64, i64, i64, f32, i32, vp, vp]
     lib.layernorm.argtypes = [vp, vp, vp, i64, i64, f32, i32, vp, vp]
     lib.rmsnorm.argtypes = [vp, vp, i64, i64, f32, i32, vp, vp]
     lib.softmax.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp]
@@ -78,7 +79,8 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     for f in ("ln_linear_prepare", "ln_linear_deferred", "rms_linear_deferred", "ln_linear_prepare_centered",
               "ln_linear_serial", "ln_linear_norm_on_load", "ln_linear_deferred_post",
               "rms_linear_deferred_post", "swiglu_prepare", "rms_swiglu_deferred", "softmax_pv_deferred",
-              "attention_deferred", "attention_gqa_deferred", "attention_decode_deferred", "layernorm", "rmsnorm",
+              "attention_deferred", "attention_gqa_deferred", "attention_decode_deferred",
+              "attention_decode_deferred_noalloc", "layernorm", "rmsnorm",
               "silu_mul", "softmax",
               "gemm"):
         getattr(lib, f).restype = i32
@@ -389,6 +391,27 @@ def attention_decode_deferred(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
     _check("attention_decode_deferred", _lib.attention_decode_deferred(
         _dev(Q, "Q"), _dev(K, "K"), _dev(V, "V"), BH, Lq, Lk, d, float(scale), _dt(Q), _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _dev(out_k, "out"), _stream(stream)))
+    return out
+
+
+def attention_decode_deferred_noalloc(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
+                                      scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                                      stream=None) -> torch.Tensor:
+    """attention_decode_deferred without a workspace: the partials live in the library's own
+    device array (the C call allocates nothing; pass `out` to keep this wrapper from allocating
+    the output).  Calls overlapping on one GPU share that array."""
+    BHq, Lq, d, BH, Lk = _check_qkv(Q, K, V, out)
+    g = BHq // BH
+    if out is None:
+        out = torch.empty_like(Q)
+    if not (Q.is_contiguous() and out.is_contiguous()):
+        raise ValueError("Q and out must be contiguous")
+    Qg, out_k = Q.view(BH, g * Lq, d), out.view(BH, g * Lq, d)
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    _check("attention_decode_deferred_noalloc", _lib.attention_decode_deferred_noalloc(
+        _dev(Qg, "Q"), _dev(K, "K"), _dev(V, "V"), BH, g * Lq, Lk, d, float(scale), _dt(Q), _dev(out_k, "out"),
+        _stream(stream)))
     return out
 
 

@@ -211,6 +211,20 @@ def test_attention_decode_validation():
     assert f(P, P2, P3, 2, 4, 1000, 64, 0.125, 1, P2, n, P + (1 << 32), None) == INVALID     # workspace over K
 
 
+def test_attention_decode_noalloc_validation():
+    f = ops._lib.attention_decode_deferred_noalloc
+    O = P + (1 << 32)
+    assert f(None, P2, P3, 2, 4, 1000, 64, 0.125, 1, O, None) == INVALID
+    assert f(P, P2, P3, 2, 4, 1000, 64, 0.125, 1, None, None) == INVALID
+    assert f(P, P2, P3, 0, 4, 1000, 64, 0.125, 1, O, None) == INVALID
+    assert f(P, P2, P3, 2, 4, 1000, 64, float("nan"), 1, O, None) == INVALID
+    assert f(P, P2, P3, 2, 17, 1000, 64, 0.125, 1, O, None) == UNSUPPORTED   # Lq > 16
+    assert f(P, P2, P3, 2, 4, 1000, 96, 0.125, 1, O, None) == UNSUPPORTED    # d
+    assert f(P, P2, P3, 2, 4, 1000, 64, 0.125, 0, O, None) == UNSUPPORTED    # fp32
+    assert f(P, P2, P3, 2, 4, 1000, 64, 0.125, 1, O + 8, None) == MISALIGNED
+    assert f(P, P2, P3, 2, 4, 1000, 64, 0.125, 1, P2, None) == INVALID       # out over K
+
+
 def test_unfused_validation():
     ln, sm, gm = ops._lib.layernorm, ops._lib.softmax, ops._lib.gemm
     assert ln(None, P2, None, 4, 64, 1e-5, 1, P3, None) == INVALID
