@@ -12,7 +12,12 @@
  * ---------------------------------------
  * - Tensor pointers are DEVICE pointers (hipMalloc'd or equivalent), row-major
  *   and contiguous, 16-byte aligned.  The caller owns all memory; the library
- *   allocates nothing and keeps no state between calls.
+ *   allocates nothing.  Two library-owned device arrays exist on each GPU the
+ *   library runs on, held until the process ends: the 1 MiB mailbox in which
+ *   the workgroups of one LayerNorm/RMSNorm product exchange their shares of
+ *   the row moments (every entry stamped with its call's number, so no call
+ *   ever uses another's; see ln_linear_deferred), and the partials array of
+ *   attention_decode_deferred_noalloc.  No other state outlives a call.
  * - Every call validates its arguments on the host BEFORE any HIP call; an
  *   invalid call returns a status and enqueues nothing.  A valid call only
  *   enqueues kernels on `stream` (NULL = the default stream) and returns; it
@@ -99,6 +104,17 @@ DN_API dn_status ln_linear_prepare(const void* W, const void* gamma, const void*
  * centering (I - E/n) applied as  x(I - E/n)W' = xW' - mean 1 W').
  * mean and the biased variance follow Eq. (1); rstd = 1/sqrt(var + eps) as
  * in Eq. (2).  eps must be finite and >= 0.  x and out have w->dtype.
+ * On the large-tile kernels (more than 128 rows, K % 64 == 0) the
+ * workgroups that share a 256-row block split the reduction of its moments
+ * and exchange the sums through the library's mailbox; a workgroup that does
+ * not find a peer's sums within 200 us (a peer not resident on a busy GPU)
+ * reduces all its rows itself, so the result never depends on scheduling.
+ * (DN_MOMENT_WAIT_TICKS in the environment overrides the wait, in 10 ns
+ * ticks; 0 makes every workgroup reduce its rows itself.)  A row holding
+ * NaN or +-inf gives an all-NaN output row; with eps = 0 a row whose fp32
+ * one-pass variance is exactly 0 (a constant row whose squares sum exactly)
+ * gives NaN, as (x - mean) / 0 does.  |x| >= 2^64 (fp32 overflow of x^2) is
+ * outside the supported range.
  */
 DN_API dn_status ln_linear_deferred(const void* x, const ln_linear_weights* w, int64_t M,
                              float eps, void* out, hipStream_t stream);

@@ -188,6 +188,12 @@ __device__ __forceinline__ float xor32_pair_op(float v, bool is_max) {
     const float a = __uint_as_float(p[0]), b = __uint_as_float(p[1]);
     return is_max ? vmax2(a, b) : a + b;
 }
+// Sum over all 64 lanes (every lane gets the total).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
 __device__ __forceinline__ float sum_lane_groups(float v) { return xor32_pair_op(xor16_pair_op(v, false), false); }
 __device__ __forceinline__ float max_lane_groups(float v) { return xor32_pair_op(xor16_pair_op(v, true), true); }
 

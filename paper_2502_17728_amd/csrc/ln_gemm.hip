@@ -23,6 +23,9 @@
 // chunk is 1 KiB, contiguous, already in MFMA operand order: a wave copies it
 // with one fully coalesced instruction, and a lane's 16 bytes are its operand.
 #include <algorithm>
+#include <atomic>
+#include <cstdlib>
+#include <mutex>
 #include <type_traits>
 
 #include "dn_device.hpp"
@@ -56,6 +59,12 @@ struct MainArgs {
     float* stats_out;        // LN: (mean, rstd) per row as reduced by the kernel, written once per row, or null
     const void* bias;     // GEMM: bias[N] in the element type, or null
     int a_causal;         // GEMM: A lower-triangular, skip k > row
+    // LN, shared row moments (pipelined kernel): the workgroups that share a row block each
+    // reduce a share of its rows and exchange them through mom_slots (2 words per row,
+    // stamped with mom_call); null = every workgroup reduces all its rows itself
+    unsigned long long* mom_slots;
+    uint32_t mom_call;
+    uint32_t mom_wait_ticks;  // bound of the wait for the peers' shares, s_memrealtime ticks (100 MHz)
 };
 
 // SiLU(z) = z / (1 + e^-z) with e^-z = 2^(-z log2 e) on the hardware exponential;
@@ -449,6 +458,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
 
     __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
     __shared__ float row_s1[LN ? BM : 1], row_s2[LN ? BM : 1];
+    __shared__ float mom_part[LN ? 2 * WN * BM : 1];  // shared moments: (sum x, sum x^2) per wave column
+    __shared__ int mom_missing;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -458,9 +469,13 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
     // A workgroup owns one 256-row block and `group` consecutive 256-column
     // tiles of it.  The row moments depend only on the rows, so they are
     // reduced once, alongside the first tile's main loop, and kept in LDS for
-    // the epilogues of all the group's tiles.  Workgroup order: XCD-contiguous,
-    // then blocks of GM row blocks x all column groups (operand panels shared
-    // under one L2).
+    // the epilogues of all the group's tiles.  When the row block's column
+    // groups are co-resident they split that reduction between them (each
+    // takes a share of the block's 16-row fragments) and exchange the results
+    // through a device mailbox -- the normalization's collective carried out
+    // by the workgroups that share the rows, 1/ngroups of the work each.
+    // Workgroup order: XCD-contiguous, then blocks of GM row blocks x all
+    // column groups (operand panels shared under one L2).
     if constexpr (!LN) group = 1;  // the plain product has no per-row work to share
     const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
     const int ngroups = (tiles_n + group - 1) / group;
@@ -471,6 +486,19 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
     const int pm = first + (t % span) % gsz;
     const int gn = (t % span) / gsz;
     const int64_t m0 = (int64_t)pm * BM;
+
+    // Shared moments: the ngroups workgroups of a row block split its 16-row fragments
+    // (fragment f goes to column group f mod ngroups); each reduces the moments of its
+    // fragments alongside its first tile's main loop -- the two wave columns of the
+    // fragment's wave row taking alternate k-halves -- and publishes them.  With
+    // ngroups >= FM (the host's condition) a wave row holds at most one of them, own_fm.
+    const bool share = LN && !NOL && p.mom_slots != nullptr && p.row_stats == nullptr;
+    int own_fm = -1;
+    if (share) {
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+            if ((wm * FM + fm) % ngroups == gn) own_fm = fm;
+    }
 
     const __bf16* A = reinterpret_cast<const __bf16*>(p.A);
     const char* Bp = reinterpret_cast<const char*>(p.B);
@@ -576,7 +604,13 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
                 if (i < NRD) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
             }
         };
-        auto run = [&](auto own) {
+        // Shared moments: the wave's owned fragment for k-half h == wn, re-read from the
+        // stage in LDS (one fragment read per stage) next to the first half's MFMAs.
+        float ms1 = 0.f, ms2 = 0.f;
+        const int mr = wm * WTM + max(own_fm, 0) * 16 + (lane & 15);
+        const int mrow = mr * 128 + (((wn * 4 + (lane >> 4)) ^ a_swz(mr)) << 4);
+        auto run = [&](auto own, auto slice) {
+            constexpr bool SLICE = decltype(slice)::value;
             issue(0);
             if (nst > 1) {
                 issue(1);
@@ -585,11 +619,15 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
                 wait_vmcnt<0>();
             }
             block_barrier();
-            u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+            u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN], ms;
             read(0, 0, fa0, fb0);
             for (int s = 0; s < nst; ++s) {
                 read(s, 1, fa1, fb1);
+                // the owned fragment's k-half wn of stage s, read (like every read of stage s)
+                // before the barrier after which stage s + 2 overwrites the buffer
+                if (SLICE) ms = lds_ld16(lds_ptr(smem + (s & 1) * STAGE + mrow));
                 compute(own, fa0, fb0);
+                if (SLICE) chunk_moments<__bf16>(ms, ms1, ms2);
                 wait_vmcnt<0>();  // this wave's copies of stage s+1 have landed
                 wait_lgkm0();     // this wave's reads of stage s are complete
                 block_barrier();
@@ -598,14 +636,19 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
                 compute(own, fa1, fb1);
             }
         };
-        const bool moments = LN && tt == 0 && !p.row_stats;
-        if (moments) {
-            if (wn == 1)
-                run(std::integral_constant<int, 1>{});
+        const bool moments = LN && !NOL && tt == 0 && !p.row_stats;
+        if (moments && share) {
+            if (own_fm >= 0)
+                run(std::integral_constant<int, -1>{}, std::true_type{});
             else
-                run(std::integral_constant<int, 0>{});
+                run(std::integral_constant<int, -1>{}, std::false_type{});
+        } else if (moments) {
+            if (wn == 1)
+                run(std::integral_constant<int, 1>{}, std::false_type{});
+            else
+                run(std::integral_constant<int, 0>{}, std::false_type{});
         } else {
-            run(std::integral_constant<int, -1>{});
+            run(std::integral_constant<int, -1>{}, std::false_type{});
         }
         wait_lgkm0();
 
@@ -617,7 +660,83 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
             }
             __syncthreads();
         }
-        if (moments) {
+        if (moments && share) {
+            // this workgroup's fragments: the two k-halves' partial sums meet in LDS, the
+            // totals are published stamped with the call number ...
+            if (own_fm >= 0) {
+                const float a = sum_lane_groups(ms1);
+                const float b = sum_lane_groups(ms2);
+                if (lane < 16) {
+                    const int r = wm * WTM + own_fm * 16 + lane;
+                    mom_part[(2 * wn) * BM + r] = a;
+                    mom_part[(2 * wn + 1) * BM + r] = b;
+                }
+            }
+            if (tid == 0) mom_missing = 0;
+            __syncthreads();
+            const unsigned long long stamp = (unsigned long long)p.mom_call << 32;
+            for (int r = tid; r < BM; r += NW * kWave) {
+                if ((r / 16) % ngroups == gn && m0 + r < M) {
+                    float a = 0.f, b = 0.f;
+#pragma unroll
+                    for (int w = 0; w < WN; ++w) {
+                        a += mom_part[(2 * w) * BM + r];
+                        b += mom_part[(2 * w + 1) * BM + r];
+                    }
+                    __hip_atomic_store(p.mom_slots + 2 * (m0 + r), stamp | __float_as_uint(a), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(p.mom_slots + 2 * (m0 + r) + 1, stamp | __float_as_uint(b), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            // ... and the whole row block's are read back, each word checked against the stamp.
+            // The wait is bounded (s_memrealtime, 100 MHz): a peer that has not published by
+            // then (not resident, say) makes this workgroup reduce every row itself below.
+            // A bound of 0 skips the exchange (every row reduced locally).
+            for (int r = tid; r < BM; r += NW * kWave) {
+                float a = 0.f, b = 0.f;
+                if (p.mom_wait_ticks == 0) {
+                    mom_missing = 1;
+                } else if (m0 + r < M) {
+                    const unsigned long long* sl = p.mom_slots + 2 * (m0 + r);
+                    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+                    bool ok = false;
+                    while (true) {
+                        const unsigned long long w1 = __hip_atomic_load(sl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        const unsigned long long w2 =
+                            __hip_atomic_load(sl + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if ((w1 >> 32) == p.mom_call && (w2 >> 32) == p.mom_call) {
+                            a = __uint_as_float((uint32_t)w1);
+                            b = __uint_as_float((uint32_t)w2);
+                            ok = true;
+                            break;
+                        }
+                        if (__builtin_amdgcn_s_memrealtime() - t0 > p.mom_wait_ticks) break;
+                        __builtin_amdgcn_s_sleep(8);
+                    }
+                    if (!ok) mom_missing = 1;
+                }
+                row_s1[r] = a;
+                row_s2[r] = b;
+            }
+            __syncthreads();
+            if (mom_missing) {  // fallback: every row of the block from x itself, one wave per row
+                for (int r = wave; r < BM; r += NW) {
+                    float a = 0.f, b = 0.f;
+                    if (m0 + r < M) {
+                        const __bf16* xr = A + (m0 + r) * K;
+                        for (int64_t k = lane * 8; k < K; k += 8 * kWave) chunk_moments<__bf16>(ld16(xr + k), a, b);
+                        a = wave_sum(a);
+                        b = wave_sum(b);
+                    }
+                    if (lane == 0) {
+                        row_s1[r] = a;
+                        row_s2[r] = b;
+                    }
+                }
+                __syncthreads();
+            }
+        } else if (moments) {
 #pragma unroll
             for (int i = 0; i < FMW; ++i) {
                 const float a = sum_lane_groups(s1[i]);
@@ -629,6 +748,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
                 }
             }
             __syncthreads();
+        }
+        if (moments) {
             for (int r = tid; r < BM; r += NW * kWave) {
                 const float mean = p.rms ? 0.f : row_s1[r] / (float)K;
                 row_s2[r] = rstd_from_moments(row_s2[r] / (float)K, mean, p.eps);
@@ -1047,8 +1168,50 @@ static hipError_t run_main(const MainArgs& a, int64_t batch, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Mailbox of the shared row moments: 2 words per row, each (call number << 32) | fp32
+// bits of sum x or sum x^2.  One array per GPU, held until the process ends; in host
+// code `mom_mailbox` names a host-side stand-in, so kernels get the device address
+// looked up once per device with hipGetSymbolAddress.  A reader accepts only words
+// stamped with its own call number, so calls that overlap on one GPU (concurrent
+// streams) stay correct: at worst a workgroup misses its peers' words and reduces its
+// rows itself.
+constexpr int64_t kMomentRows = 65536;
+static __device__ __align__(256) unsigned long long mom_mailbox[2 * kMomentRows];
+
+static unsigned long long* moment_mailbox() {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static unsigned long long* addr[kMaxDevices] = {};
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(mom_mailbox)) != hipSuccess) return nullptr;
+        addr[dev] = (unsigned long long*)ptr;
+    }
+    return addr[dev];
+}
+
+// Call numbers 1, 2, ... (0 never: the mailbox starts zeroed).
+static uint32_t next_moment_call() {
+    static std::atomic<uint32_t> counter{0};
+    uint32_t c = ++counter;
+    while (c == 0) c = ++counter;
+    return c;
+}
+
+// How long a workgroup waits for its peers' moments before reducing its rows itself,
+// in s_memrealtime ticks (100 MHz): 200 us, far above the spread of the peers' first
+// tiles.  DN_MOMENT_WAIT_TICKS overrides it (0 forces the local reduction; tests use it).
+static uint32_t moment_wait_ticks() {
+    const char* e = getenv("DN_MOMENT_WAIT_TICKS");
+    return e ? (uint32_t)strtoul(e, nullptr, 10) : 20000u;
+}
+
 template <Epi EPI, int BT = 256>
-static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
+static hipError_t run_pipe(const MainArgs& args, hipStream_t s) {
+    MainArgs a = args;
     const int64_t tm = (a.M + BT - 1) / BT, tn = (a.N + BT - 1) / BT;
     // deferred LN: each workgroup takes `group` column tiles of one row block and
     // reduces the row moments once, on its first tile.  With one workgroup per CU
@@ -1067,7 +1230,17 @@ static hipError_t run_pipe(const MainArgs& a, hipStream_t s) {
             }
         }
     }
-    const int64_t wgs = tm * ((tn + group - 1) / group);
+    const int64_t ngroups = (tn + group - 1) / group, wgs = tm * ngroups;
+    // Shared moments where the workgroups of a row block are co-resident (one round of
+    // workgroups: 256 at one per CU, 512 for the 128 x 128 tiles at two per CU) and number
+    // at least 4 (then each wave row of a workgroup owns at most one 16-row fragment).
+    a.mom_slots = nullptr;
+    if ((EPI == Epi::kLnDeferred || EPI == Epi::kSwiGlu) && !a.row_stats && ngroups >= 4 &&
+        wgs <= (BT == 128 ? 512 : 256) && a.M <= kMomentRows) {
+        a.mom_slots = moment_mailbox();
+        a.mom_call = next_moment_call();
+        a.mom_wait_ticks = moment_wait_ticks();
+    }
     if constexpr (BT == 128)  // 4 waves of 64 x 64, 64 KiB of LDS: two workgroups per CU
         pipe_kernel<EPI, 2, 2, 128, 128><<<dim3((unsigned)wgs), 4 * kWave, 0, s>>>(a, (int)group);
     else

@@ -216,6 +216,40 @@ def test_ln_linear_guard_band(ops):
     assert (buf[:512] == 7.0).all() and (buf[-512:] == 7.0).all()
 
 
+# Shared row moments: on the pipelined kernels the workgroups of a row block each reduce a share
+# of its rows' moments and exchange them through a device mailbox, every word stamped with its
+# call's number.  A bound of 0 on the wait for the peers' shares makes every workgroup reduce all
+# its rows itself -- the path taken when a peer is not resident.
+@pytest.mark.parametrize("M,K,N", [(4096, 1024, 4096), (300, 256, 4104), (4000, 544, 4104), (520, 256, 8200)])
+@pytest.mark.parametrize("norm", ["layernorm", "rms"])
+def test_ln_linear_moments_reduced_locally(ops, M, K, N, norm, monkeypatch):
+    monkeypatch.setenv("DN_MOMENT_WAIT_TICKS", "0")
+    _ln_check(ops, I.make_ln_case(M, K, N, "bf16", seed=M + 5, outliers=3, norm=norm))
+
+
+def test_swiglu_moments_reduced_locally(ops, monkeypatch):
+    monkeypatch.setenv("DN_MOMENT_WAIT_TICKS", "0")
+    _swiglu_check(ops, I.make_swiglu_case(1100, 512, 2056, "bf16", seed=6, outliers=2))
+
+
+def test_ln_linear_shared_moments_follow_each_call(ops):
+    # calls of one shape on different rows, back to back: each call's workgroups take only
+    # their own call's moments (a stale share would shift whole rows), and a repeated call
+    # gives the same bits
+    a = I.make_ln_case(4096, 512, 4104, "bf16", seed=40, outliers=2)
+    b = I.make_ln_case(4096, 512, 4104, "bf16", seed=41, outliers=2, mean_offset=1.0)
+    w = ops.ln_linear_prepare(cuda(a["W"]), cuda(a["gamma"]), cuda(a["beta"]))
+    xa, xb = cuda(a["x"]), cuda(b["x"])
+    oa = ops.ln_linear_deferred(xa, w, a["eps"])
+    ob = ops.ln_linear_deferred(xb, w, a["eps"])
+    oa2 = ops.ln_linear_deferred(xa, w, a["eps"])
+    torch.cuda.synchronize()
+    for x, out in ((a["x"], oa), (b["x"], ob)):
+        ref = oracle.ln_linear(x, a["gamma"], a["beta"], a["W"], None, a["eps"])
+        assert rowwise_rel_err(out.cpu(), ref) <= TOL[torch.bfloat16]
+    assert torch.equal(oa, oa2)
+
+
 # Non-finite inputs propagate as in the plain definition (Eq. (1)-(2), Eq. (6)): a row holding
 # NaN, +inf or -inf gives an all-NaN output row and leaves every other row untouched; with
 # eps = 0 a constant row (LayerNorm: zero variance) or an all-zero row (RMSNorm) gives 0/0 = NaN.
