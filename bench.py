@@ -50,6 +50,7 @@ METRIC = "TFLOP/s fused LN→GEMM & softmax→PV, % MFMA peak, speedup vs unfuse
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 flop/clk (dense bf16 MFMA)
 PEAK_F32_TFLOPS = 157.3     # fp32 MFMA / vector
 PEAK_HBM_GBS = 8000.0       # HBM3E
+ROUNDS = 7                  # rounds of the alternating isolated timings
 
 # HBM traffic per launch, from two rocprofv3 --pmc runs of this script (FETCH_SIZE, then WRITE_SIZE,
 # KiB per dispatch, averaged over the timed launches), each scaled by what the same counter reads for
@@ -117,6 +118,11 @@ def parse():
                              "decode_attention", "decode_attention_gqa"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--path", default="fused", choices=["fused", "unfused"],
+                    help="what the timed steps run: the deferred kernels (default) or the unfused "
+                         "comparators (for profiling them on their own)")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the other named workloads (timed on their own after the layer step)")
     ap.add_argument("--cpu-threads", type=int, default=None)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time of the oracle sample behind cpu_baseline")
@@ -141,30 +147,42 @@ def sm_bytes(w) -> float:
 class LNSite:
     """LayerNorm -> Linear (Eq. (5)), or RMSNorm -> Linear (Eq. (6)) when the workload says so."""
 
-    def __init__(self, ops, I, w):
+    def __init__(self, ops, I, w, case=None, copies=1):
+        """case: the workload's tensors when already generated; copies: how many separately
+        prepared copies of the static weights the calls rotate through (HBM-bound shapes take
+        enough of them that the weights cannot stay in the 256 MB last-level cache)."""
         self.w = w
         self.rms = w.norm == "rms"
         self.kernel = "rms_linear_deferred" if self.rms else "ln_linear_deferred"
-        self.case = I.make_ln(w)
+        self.case = I.make_ln(w) if case is None else case
         c = self.case
         cuda = lambda t: None if t is None else t.cuda()
         self.x = c["x"].cuda()
-        self.W = c["W"].cuda()
-        self.prep = ops.ln_linear_prepare(self.W, c["gamma"].cuda(), cuda(c["beta"]), cuda(c["bias"]))
-        self.out = torch.empty((w.M, w.N), dtype=self.x.dtype, device="cuda")
-        # unfused comparator: the same static weights packed once the same way (gamma = 1 folds
-        # nothing), so both paths run the same weight layout and MFMA main loop
-        self.Wpk = ops.ln_linear_prepare(self.W, torch.ones(w.K, dtype=self.W.dtype, device="cuda"))
+        W = c["W"].cuda()
         self.g, self.b = c["gamma"].cuda(), cuda(c["beta"])
         self.bias = cuda(c["bias"])
+        self.preps = [ops.ln_linear_prepare(W, self.g, self.b, self.bias) for _ in range(copies)]
+        self.prep = self.preps[0]
+        self.out = torch.empty((w.M, w.N), dtype=self.x.dtype, device="cuda")
+        # unfused comparator: the same static weights packed the same way (gamma = 1 folds
+        # nothing), so both paths run the same weight layout and MFMA main loop
+        one = torch.ones(w.K, dtype=W.dtype, device="cuda")
+        self.Wpks = [ops.ln_linear_prepare(W, one) for _ in range(copies)]
+        del W
+        self.copies, self.it = copies, 0
         self.y = torch.empty_like(self.x)
         self.stats = torch.empty(2 * w.M, dtype=torch.float32, device="cuda")
         self.ops = ops
         torch.cuda.synchronize()
 
+    def _next(self):
+        """Index of the weight copy for this call (round robin)."""
+        self.it = (self.it + 1) % self.copies
+        return self.it
+
     def serial(self):
         # ablation: the row statistics in a pre-pass kernel, then the same deferred epilogue
-        self.ops.ln_linear_serial(self.x, self.prep, self.w.eps, stats=self.stats, out=self.out)
+        self.ops.ln_linear_serial(self.x, self.preps[self._next()], self.w.eps, stats=self.stats, out=self.out)
 
     def on_load_supported(self):
         return (not self.rms and self.w.dtype == "bf16" and self.w.K % 64 == 0
@@ -172,23 +190,29 @@ class LNSite:
 
     def post(self):
         # post-LN placement: the deferred product plus the normalized rows (the residual branch)
-        self.ops.linear_deferred_post(self.x, self.prep, self.g, None if self.rms else self.b, self.w.eps,
+        self.ops.linear_deferred_post(self.x, self.preps[self._next()], self.g, None if self.rms else self.b,
+                                      self.w.eps,
                                       rms=self.rms, stats=self.stats, y=self.y, out=self.out)
 
     def norm_on_load(self):
         # ablation without deferral: pre-pass statistics, x normalized on load into the product
-        self.ops.ln_linear_norm_on_load(self.x, self.prep, self.w.eps, stats=self.stats, out=self.out)
+        self.ops.ln_linear_norm_on_load(self.x, self.preps[self._next()], self.w.eps, stats=self.stats,
+                                        out=self.out)
 
     def fused(self):
         f = self.ops.rms_linear_deferred if self.rms else self.ops.ln_linear_deferred
-        f(self.x, self.prep, self.w.eps, out=self.out)
+        f(self.x, self.preps[self._next()], self.w.eps, out=self.out)
+
+    def gemm_only(self):
+        # the product alone on the same packed weights: no statistics, no normalization
+        self.ops.gemm(self.x, self.Wpks[self._next()], self.bias, out=self.out.view(1, self.w.M, self.w.N))
 
     def unfused(self):
         if self.rms:
             self.ops.rmsnorm(self.x, self.g, self.w.eps, out=self.y)
         else:
             self.ops.layernorm(self.x, self.g, self.b, self.w.eps, out=self.y)
-        self.ops.gemm(self.y, self.Wpk, self.bias, out=self.out.view(1, self.w.M, self.w.N))
+        self.ops.gemm(self.y, self.Wpks[self._next()], self.bias, out=self.out.view(1, self.w.M, self.w.N))
 
     def flops(self):
         return self.w.flops()
@@ -449,7 +473,7 @@ def build_sites(ops, I, name):
         w = I.ln_qkv_tokens(t)
     else:
         w = I.rms_ffn_decode(t) if name.startswith("rms_") else I.ln_ffn_decode(t)
-    return [LNSite(ops, I, w)], w.name
+    return [LNSite(ops, I, w, copies=weight_copies(w))], w.name
 
 
 # ------------------------------------------------------------------------------ timing
@@ -495,6 +519,160 @@ def time_steps(fns, steps, warmup, warm_seconds=0.0):
     return per, total
 
 
+def weight_copies(w) -> int:
+    """Prepared weight copies for an HBM-bound LN shape: enough that the calls rotate through
+    about 1 GB of weights, four times the 256 MB last-level cache (1 for MFMA-bound shapes)."""
+    es = 4 if w.dtype == "f32" else 2
+    peak = PEAK_F32_TFLOPS if w.dtype == "f32" else PEAK_BF16_TFLOPS
+    if 2.0 * w.M * w.K * w.N / (es * (w.M * w.K + w.K * w.N + w.M * w.N)) >= peak / PEAK_HBM_GBS * 1e3:
+        return 1
+    return int(min(16, max(1, -(-1.0e9 // (es * w.K * w.N)))))
+
+
+def roof_of(s, ms):
+    """Bound ("hbm" below the ridge point of the site's arithmetic intensity, else "mfma"), the
+    achieved rate at `ms` per launch and its fraction of that roof's peak."""
+    hbm = isinstance(s, (SMSite, DecodeAttnSite)) or \
+        s.flops() / s.bytes() < s.peak_tflops() * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if hbm:
+        a = s.bytes() / (ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": round(a, 1), "unit": "GB/s", "peak": PEAK_HBM_GBS,
+                "frac": round(a / PEAK_HBM_GBS, 4)}
+    a = s.flops() / (ms * 1e-3) / 1e12
+    return {"bound": "mfma", "achieved": round(a, 2), "unit": "TFLOP/s", "peak": s.peak_tflops(),
+            "frac": round(a / s.peak_tflops(), 4)}
+
+
+def workload_entries(ops, I, steps):
+    """The other named workloads, each timed on its own (isolated median over ROUNDS rounds) with its
+    unfused comparator: LayerNorm -> Linear fp32 128 x 768 x 3072, Softmax -> P.V 12 x 512 x 512
+    (d 64), the LayerNorm -> FFN up-projection 8192 -> 28672 over 8192 tokens (prefill) and over
+    1, 4 and 16 tokens (decode, rotating through weight copies so every call streams W' from HBM).
+    The decode tokens are the first t rows of the prefill batch (the same stream)."""
+    out = {}
+
+    def one(site, extra=None):
+        k = isolated(site, steps)
+        e = {"isolated_ms": k["isolated_ms"], "isolated_spread_ms": k["isolated_spread_ms"],
+             "tflops": round(site.flops() / (k["isolated_ms"] * 1e-3) / 1e12, 2),
+             "gbs": round(site.bytes() / (k["isolated_ms"] * 1e-3) / 1e9, 1),
+             "alg_gflop": round(site.flops() / 1e9, 3), "alg_mbytes": round(site.bytes() / 1e6, 2)}
+        e["roofline"] = roof_of(site, k["isolated_ms"])
+        e.update({a: b for a, b in k.items() if a not in e})
+        if extra:
+            e.update(extra)
+        out[site.w.name] = e
+        torch.cuda.synchronize()
+
+    one(LNSite(ops, I, I.LN_F32_SMALL))
+    one(SMSite(ops, I, I.SM_BF16_SMALL))
+    case = I.make_ln(I.LN_FFN_PREFILL)
+    site = LNSite(ops, I, I.LN_FFN_PREFILL, case=case)
+    one(site)
+    del site
+    torch.cuda.empty_cache()
+    for t in (1, 4, 16):
+        w = I.ln_ffn_decode(t)
+        c = dict(case, x=case["x"][:t].clone())
+        r = weight_copies(w)
+        site = LNSite(ops, I, w, case=c, copies=r)
+        one(site, {"weight_copies": r})
+        del site
+        torch.cuda.empty_cache()
+    return out
+
+
+def copy_bandwidth(mib=1024, reps=10):
+    """A plain device-to-device copy of `mib` MiB, event-timed: bytes read + written per second."""
+    src = torch.ones(mib << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    stream = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    gbs = 2.0 * (mib << 20) / (ms * 1e-3) / 1e9
+    return {"bytes": 2 * (mib << 20), "ms": round(ms, 4), "gbs": round(gbs, 1), "frac_of_spec": round(gbs / PEAK_HBM_GBS, 4)}
+
+
+def cpu_model() -> str:
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def isolated(s, steps):
+    """Each path of a site timed on its own: the deferred kernel, the unfused comparator and the
+    ablations the site supports, alternating over ROUNDS rounds of at least 20 launches; medians
+    and min-max spreads over the rounds."""
+    k = {}
+    # speedups compare like with like: each path timed alone, back to back on its own inputs
+    # (inside the step the kernel follows the other site, whose traffic evicts the caches);
+    # the paths alternate over ROUNDS rounds and each reports its median
+    n = max(20, steps)  # iterations per round (each round: every path, in turn)
+    fis, us, uds, sers, sps, nols, posts, gos = [], [], [], [], [], [], [], []
+    serial = isinstance(s, LNSite) and not s.rms and s.w.K <= 16384
+    on_load = serial and s.on_load_supported()
+    for _ in range(ROUNDS):
+        fis.append(time_steps([s.fused], n, 2)[0][0])
+        us.append(time_steps([s.unfused], n, 2)[0][0])
+        if isinstance(s, LNSite):
+            gos.append(time_steps([s.gemm_only], n, 2)[0][0])
+        if isinstance(s, (SMSite, AttnSite)) and s.w.causal:
+            uds.append(time_steps([s.unfused_dense], max(3, n // 2), 1)[0][0])
+        if serial:
+            sers.append(time_steps([s.serial], n, 2)[0][0])
+        if isinstance(s, DecodeAttnSite):
+            sps.append(time_steps([s.single_pass], n, 2)[0][0])
+        if on_load:
+            nols.append(time_steps([s.norm_on_load], n, 2)[0][0])
+        if isinstance(s, LNSite):
+            posts.append(time_steps([s.post], n, 2)[0][0])
+    fi, u = float(np.median(fis)), float(np.median(us))
+    k["isolated_ms"] = round(fi, 4)
+    k["unfused_ms"] = round(u, 4)
+    k["isolated_spread_ms"] = [round(min(fis), 4), round(max(fis), 4)]  # over the rounds
+    k["unfused_spread_ms"] = [round(min(us), 4), round(max(us), 4)]
+    k["speedup_vs_unfused"] = round(u / fi, 3)
+    if gos:  # the product alone: what deferral adds on top of it
+        go = float(np.median(gos))
+        k["gemm_only_ms"] = round(go, 4)
+        k["deferred_overhead_us"] = round(1e3 * (fi - go), 1)
+    if uds:
+        ud = float(np.median(uds))
+        k["unfused_dense_ms"] = round(ud, 4)
+        k["speedup_vs_unfused_dense"] = round(ud / fi, 3)
+    if sers:  # ablation: statistics from a pre-pass instead of concurrently
+        se = float(np.median(sers))
+        k["serial_stats_ms"] = round(se, 4)
+        k["speedup_vs_serial_stats"] = round(se / fi, 3)
+    if posts:  # post-LN placement: deferred product + normalized rows, against the unfused pair
+        po = float(np.median(posts))
+        k["post_ln_ms"] = round(po, 4)
+        k["post_ln_speedup_vs_unfused"] = round(u / po, 3)
+    if nols:  # ablation: fused without deferral (normalize on load)
+        nl = float(np.median(nols))
+        k["norm_on_load_ms"] = round(nl, 4)
+        k["speedup_vs_norm_on_load"] = round(nl / fi, 3)
+    if sps:  # ablation: no key split (one workgroup per head)
+        sp = float(np.median(sps))
+        k["single_pass_ms"] = round(sp, 4)
+        k["speedup_vs_single_pass"] = round(sp / fi, 3)
+    return k
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -511,7 +689,8 @@ def main():
     sites, wl_name = build_sites(ops, I, args.workload)
     setup_s = time.perf_counter() - t_setup
 
-    per, total = time_steps([s.fused for s in sites], args.steps, args.warmup, args.warm_seconds)
+    fns = [s.fused if args.path == "fused" else s.unfused for s in sites]
+    per, total = time_steps(fns, args.steps, args.warmup, args.warm_seconds)
     if args.calib_copy_mib > 0:
         src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -535,52 +714,7 @@ def main():
         tr = measured_traffic(name, s.w.name)
         k["hbm_traffic_mbytes"] = None if tr is None else round(tr / 1e6, 2)
         if not args.no_unfused:
-            # speedups compare like with like: each path timed alone, back to back on its own inputs
-            # (inside the step the kernel follows the other site, whose traffic evicts the caches);
-            # the two alternate over 5 rounds and each reports its median
-            n = max(20, args.steps)  # iterations per round (each round: every path, in turn)
-            fis, us, uds, sers, sps, nols, posts = [], [], [], [], [], [], []
-            serial = isinstance(s, LNSite) and not s.rms and s.w.K <= 16384
-            on_load = serial and s.on_load_supported()
-            for _ in range(5):
-                fis.append(time_steps([s.fused], n, 2)[0][0])
-                us.append(time_steps([s.unfused], n, 2)[0][0])
-                if isinstance(s, (SMSite, AttnSite)) and s.w.causal:
-                    uds.append(time_steps([s.unfused_dense], max(3, n // 2), 1)[0][0])
-                if serial:
-                    sers.append(time_steps([s.serial], n, 2)[0][0])
-                if isinstance(s, DecodeAttnSite):
-                    sps.append(time_steps([s.single_pass], n, 2)[0][0])
-                if on_load:
-                    nols.append(time_steps([s.norm_on_load], n, 2)[0][0])
-                if isinstance(s, LNSite):
-                    posts.append(time_steps([s.post], n, 2)[0][0])
-            fi, u = float(np.median(fis)), float(np.median(us))
-            k["isolated_ms"] = round(fi, 4)
-            k["unfused_ms"] = round(u, 4)
-            k["isolated_spread_ms"] = [round(min(fis), 4), round(max(fis), 4)]  # over the 5 rounds
-            k["unfused_spread_ms"] = [round(min(us), 4), round(max(us), 4)]
-            k["speedup_vs_unfused"] = round(u / fi, 3)
-            if uds:
-                ud = float(np.median(uds))
-                k["unfused_dense_ms"] = round(ud, 4)
-                k["speedup_vs_unfused_dense"] = round(ud / fi, 3)
-            if sers:  # ablation: statistics from a pre-pass instead of concurrently
-                se = float(np.median(sers))
-                k["serial_stats_ms"] = round(se, 4)
-                k["speedup_vs_serial_stats"] = round(se / fi, 3)
-            if posts:  # post-LN placement: deferred product + normalized rows, against the unfused pair
-                po = float(np.median(posts))
-                k["post_ln_ms"] = round(po, 4)
-                k["post_ln_speedup_vs_unfused"] = round(u / po, 3)
-            if nols:  # ablation: fused without deferral (normalize on load)
-                nl = float(np.median(nols))
-                k["norm_on_load_ms"] = round(nl, 4)
-                k["speedup_vs_norm_on_load"] = round(nl / fi, 3)
-            if sps:  # ablation: no key split (one workgroup per head)
-                sp = float(np.median(sps))
-                k["single_pass_ms"] = round(sp, 4)
-                k["speedup_vs_single_pass"] = round(sp / fi, 3)
+            k.update(isolated(s, args.steps))
         kernels[name] = k
 
     d = sites[dom]
@@ -601,10 +735,17 @@ def main():
                 "unit": "TFLOP/s", "frac": round(ach / pk, 4),
                 "traffic": kernels[dname]["hbm_traffic_mbytes"] and round(kernels[dname]["hbm_traffic_mbytes"] * 1e6)}
 
+    workloads = None
+    if args.workload == "layer" and not args.no_workloads:
+        workloads = workload_entries(ops, I, args.steps)
+    hbm_copy = copy_bandwidth() if args.workload == "layer" else None
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        threads = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))
+        # the host's share of CPU threads for one GPU is 16, whatever the affinity mask shows
+        affinity = len(os.sched_getaffinity(0))
+        threads = args.cpu_threads or min(16, affinity)
         t_cpu, frac_cpu, descs = 0.0, 0.0, []
         extrap = 0.0
         for s in sites:
@@ -627,15 +768,24 @@ def main():
             descs.append(f"{desc} ({dt:.1f} s)")
         cpu = {"value": round(flops / extrap / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
                "sample": "; ".join(descs) + f"; time extrapolated by work to the whole step "
-                         f"({extrap:.1f} s per step on {threads} threads)"}
+                         f"({extrap:.1f} s per step on {threads} threads)",
+               "cpu_model": cpu_model(), "affinity_cores": affinity}
+        # one thread, the whole LayerNorm -> Linear fp32 128 x 768 x 3072 workload
+        small = I.make_ln(I.LN_F32_SMALL)
+        t0 = time.perf_counter()
+        oracle.ln_linear(small["x"], small["gamma"], small["beta"], small["W"], small["bias"], small["eps"],
+                         nthreads=1)
+        dt1 = time.perf_counter() - t0
+        cpu["single_thread"] = {"workload": I.LN_F32_SMALL.name, "s": round(dt1, 3),
+                                "tflops": round(I.LN_F32_SMALL.flops() / dt1 / 1e12, 6)}
 
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(total, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32" if all(getattr(s.w, "dtype", "bf16") == "f32" for s in sites) else "bf16",
         "data": "synthetic",
-        "config": {"workload": wl_name},
-        "roofline": roof, "cpu_baseline": cpu, "kernels": kernels,
+        "config": {"workload": wl_name} if args.path == "fused" else {"workload": wl_name, "path": args.path},
+        "roofline": roof, "cpu_baseline": cpu, "kernels": kernels, "workloads": workloads, "hbm_copy": hbm_copy,
         "frac_mfma_peak_step": round(value / PEAK_BF16_TFLOPS, 4), "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)

@@ -93,11 +93,15 @@ __device__ __forceinline__ int64_t packed_chunk(int64_t nb, int64_t kc, int64_t 
 }
 
 // =============================================================================
-// General main loop: 128x128 (bf16) or 32x64 (fp32) tiles, two LDS stages.
-// Used for problems too small for the 256x256 kernel, for K not a multiple of
-// 64, for fp32, for batched products and for B in [K][N] layout.
+// General main loop: 128x128 (bf16) or 32x64 (fp32) tiles.  Used for problems
+// too small for the 256x256 kernel, for K not a multiple of 64, for fp32, for
+// batched products and for B in [K][N] layout.
+// NST = 2: two LDS stages, the copy of stage s+1 issued while stage s is read.
+// NST > 2 (chunk copies only): a ring of NST stages whose copies run NST-1
+// stages ahead, for tiles whose per-stage matrix work is too short to cover the
+// latency of one copy (the fp32 tiles: 16 fp32 MFMAs per wave and stage).
 // =============================================================================
-template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI>
+template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI, int NST = 2>
 __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
     constexpr int NW = WM * WN;
     constexpr int EPL = elem<T>::per16;  // elements per lane per chunk
@@ -116,8 +120,9 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
     static_assert(A_CH % NW == 0 && B_CH % NW == 0, "every wave issues the same number of chunk copies");
     static_assert(!LN || WN <= KB, "moments split: one k-chunk column per wave column");
     static_assert(!SW || FN % 2 == 0, "gate/up fragment pairs");
+    static_assert(NST == 2 || (NST > 2 && !B_KN), "the deep ring moves whole chunks only");
 
-    __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+    __shared__ __attribute__((aligned(1024))) char smem[NST * STAGE];
     __shared__ float red[LN ? 2 * WN * BM : 1];
     __shared__ float row_mean[LN ? BM : 1], row_rstd[LN ? BM : 1];
 
@@ -143,7 +148,16 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
     const int64_t kend = p.a_causal ? min(K, m0 + BM) : K;
     const int nst = (int)((kend + BK - 1) / BK);
 
-    // ---- global -> LDS staging
+    // ---- global -> LDS staging.  The deep ring issues its copies from inline
+    // assembly (the compiler does not track them, so it adds no wait of its own
+    // for all outstanding copies before the LDS reads of other stages) and counts
+    // its waits by hand: every call issues exactly A_CH / NW + B_CH / NW copies.
+    auto copy = [&](const void* g, char* l) {
+        if constexpr (NST > 2)
+            g2lds16_async(g, lds_addr32(l));
+        else
+            g2lds16(g, lds_ptr(l));
+    };
     auto issue_dma = [&](int s, int buf) {
         char* base = smem + buf * STAGE;
         const int64_t k0 = (int64_t)s * BK;
@@ -153,7 +167,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
             const int mb = c / KB, kb = c % KB;
             const int64_t row = min(m0 + mb * 16 + (lane & 15), M - 1);
             const int64_t kk = min(k0 + kb * KC + (lane >> 4) * EPL, K - EPL);
-            g2lds16(A + row * K + kk, lds_ptr(base + c * kChunkBytes));
+            copy(A + row * K + kk, base + c * kChunkBytes);
         }
         if constexpr (BMODE == BMode::kNK) {
 #pragma unroll
@@ -162,7 +176,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 const int nb = c / KB, kb = c % KB;
                 const int64_t row = min(n0 + nb * 16 + (lane & 15), N - 1);
                 const int64_t kk = min(k0 + kb * KC + (lane >> 4) * EPL, K - EPL);
-                g2lds16(B + row * K + kk, lds_ptr(base + (A_CH + c) * kChunkBytes));
+                copy(B + row * K + kk, base + (A_CH + c) * kChunkBytes);
             }
         }
         if constexpr (BMODE == BMode::kPacked) {
@@ -172,8 +186,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 const int nb = c / KB, kb = c % KB;
                 const int64_t gnb = min(n0 / 16 + nb, p.nblocks - 1);
                 const int64_t gkc = min((int64_t)s * KB + kb, p.kchunks - 1);
-                g2lds16(reinterpret_cast<const char*>(p.B) + packed_chunk(gnb, gkc, p.kchunks, lane),
-                        lds_ptr(base + (A_CH + c) * kChunkBytes));
+                copy(reinterpret_cast<const char*>(p.B) + packed_chunk(gnb, gkc, p.kchunks, lane),
+                     base + (A_CH + c) * kChunkBytes);
             }
         }
     };
@@ -235,15 +249,28 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
 #pragma unroll
     for (int i = 0; i < FM; ++i) s1[i] = s2[i] = 0.f;
 
-    issue_dma(0, 0);
-    kn_load(0);
-    kn_store(0);
-    wait_vm();
-    __syncthreads();
+    constexpr int PER = (A_CH + (B_KN ? 0 : B_CH)) / NW;  // copies per wave per stage
+    if constexpr (NST > 2) {
+        // stages 0 .. NST-2 in flight; stages past the last re-copy the last one into
+        // slots that are never read, so every stage issues the same count
+#pragma unroll
+        for (int j = 0; j < NST - 1; ++j) issue_dma(min(j, nst - 1), j);
+    } else {
+        issue_dma(0, 0);
+        kn_load(0);
+        kn_store(0);
+        wait_vm();
+        __syncthreads();
+    }
 
     for (int s = 0; s < nst; ++s) {
-        const int buf = s & 1;
+        const int buf = NST > 2 ? s % NST : (s & 1);
         const char* base = smem + buf * STAGE;
+        if constexpr (NST > 2) {
+            wait_vmcnt<(NST - 2) * PER>();  // this wave's copies of stage s have landed
+            block_barrier();                // every wave's have, and stage s-1 has been read by all
+            issue_dma(min(s + NST - 1, nst - 1), (s + NST - 1) % NST);  // into the slot of stage s-1
+        }
         u32x4 af[FM][KB], bfr[FN][KB];
 #pragma unroll
         for (int fm = 0; fm < FM; ++fm)
@@ -257,7 +284,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 bfr[fn][kb] = lds_ld16(
                     lds_ptr((char*)base + (A_CH + (wn * FN + fn) * KB + kb) * kChunkBytes + lane * 16));
 
-        if (s + 1 < nst) {
+        if (NST == 2 && s + 1 < nst) {
             issue_dma(s + 1, buf ^ 1);
             kn_load(s + 1);
         }
@@ -309,9 +336,15 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
 #pragma unroll
                 for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma_chunk<T>(af[fm][kb], bfr[fn][kb], acc[fm][fn]);
 
-        if (s + 1 < nst) kn_store(buf ^ 1);
-        wait_vm();
-        __syncthreads();
+        if constexpr (NST == 2) {
+            if (s + 1 < nst) kn_store(buf ^ 1);
+            wait_vm();
+            __syncthreads();
+        }
+    }
+    if constexpr (NST > 2) {
+        wait_vmcnt<0>();  // no copy into LDS may outlive the loop (the epilogue reuses no stage, but
+        block_barrier();  // the workgroup must not exit with copies in flight)
     }
 
     // ---- epilogue
@@ -1160,13 +1193,15 @@ hipError_t launch_swiglu_prepare(const void* Wg, const void* Wu, const void* gam
     return hipGetLastError();
 }
 
-template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI>
+template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI, int NST = 2>
 static hipError_t run_main(const MainArgs& a, int64_t batch, hipStream_t s) {
     const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
     dim3 grid((unsigned)tiles, (unsigned)batch);
-    main_loop_kernel<T, BM, BN, WM, WN, BMODE, EPI><<<grid, WM * WN * kWave, 0, s>>>(a);
+    main_loop_kernel<T, BM, BN, WM, WN, BMODE, EPI, NST><<<grid, WM * WN * kWave, 0, s>>>(a);
     return hipGetLastError();
 }
+// fp32 tiles (32 x 64, 4 waves): a 6-stage ring, 72 KiB of LDS, copies five stages ahead
+constexpr int kF32Stages = 6;
 
 // Mailbox of the shared row moments: 2 words per row, each (call number << 32) | fp32
 // bits of sum x or sum x^2.  One array per GPU, held until the process ends; in host
@@ -1348,7 +1383,7 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
         decode_dispatch<false>(M, a.nblocks, launch);
         return hipGetLastError();
     }
-    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
+    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred, kF32Stages>(a, 1, s);
     if (use_mid_tiles(M, N, K)) return run_pipe<Epi::kLnDeferred, 128>(a, s);
     if (use_big_tiles(M, N, K)) return run_pipe<Epi::kLnDeferred>(a, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
@@ -1407,7 +1442,7 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
             launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 8>, 4, 2);
         return hipGetLastError();
     }
-    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kSwiGlu>(a, 1, s);
+    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kSwiGlu, kF32Stages>(a, 1, s);
     if (use_mid_tiles(M, np, K)) return run_pipe<Epi::kSwiGlu, 128>(a, s);
     if (use_big_tiles(M, np, K)) return run_pipe<Epi::kSwiGlu>(a, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kSwiGlu>(a, 1, s);
@@ -1445,12 +1480,12 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
             decode_dispatch<true>(M, a.nblocks, launch);
             return hipGetLastError();
         }
-        if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);
+        if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kGemm, kF32Stages>(a, 1, s);
         if (use_mid_tiles(M, N, K)) return run_pipe<Epi::kGemm, 128>(a, s);
         if (use_big_tiles(M, N, K)) return run_pipe<Epi::kGemm>(a, s);
         return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);
     }
-    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kNK, Epi::kGemm>(a, batch, s);
+    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kNK, Epi::kGemm, kF32Stages>(a, batch, s);
     if (b_layout == 1) return run_main<__bf16, 128, 128, 2, 2, BMode::kNK, Epi::kGemm>(a, batch, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kKN, Epi::kGemm>(a, batch, s);
 }

@@ -418,11 +418,20 @@ static hipError_t run_softmax_pv(const void* S, const void* V, int64_t BH, int64
 // slots per wave: 80 KiB (d = 64) or 96 KiB (d = 128) of LDS.  Deeper rings
 // measured no faster on the causal 32 x 8192 x 8192, d = 128 workload.
 constexpr int kSmWaves = 8, kSmFrags = 2, kSmStages = 2, kSmPrefetch = 2;
+// Where 256-query blocks would give fewer workgroups than the chip has CUs
+// (12 heads x 512 queries: 24), the work is latency-bound: 2 waves x 1
+// fragment (32 queries per workgroup) spread it over 8x more workgroups, with
+// rings 4 (d = 64, 48 KiB) or 3 (d = 128, 60 KiB) steps deep.
+constexpr int64_t kSmCUs = 256;
 
 hipError_t launch_softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq, int64_t Lk, int64_t d,
                                       int causal, void* out, hipStream_t s) {
-    if (d == 64)
+    const bool small = BH * ((Lq + 255) / 256) < kSmCUs;
+    if (d == 64) {
+        if (small) return run_softmax_pv<64, 2, 1, 4, 4>(S, V, BH, Lq, Lk, causal, out, s);
         return run_softmax_pv<64, kSmWaves, kSmFrags, kSmStages, kSmPrefetch>(S, V, BH, Lq, Lk, causal, out, s);
+    }
+    if (small) return run_softmax_pv<128, 2, 1, 3, 3>(S, V, BH, Lq, Lk, causal, out, s);
     return run_softmax_pv<128, kSmWaves, kSmFrags, kSmStages, kSmPrefetch>(S, V, BH, Lq, Lk, causal, out, s);
 }
 

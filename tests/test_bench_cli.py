@@ -20,3 +20,17 @@ def test_bench_lists_its_workloads():
     assert r.returncode == 0
     for wl in ("layer", "ln_qkv", "causal_softmax_pv", "ffn_decode_t1", "causal_attention", "decode_attention"):
         assert wl in r.stdout
+
+
+def test_bench_weight_copies_cover_the_last_level_cache():
+    # HBM-bound LN shapes rotate through about 1 GB of prepared weights (four times the
+    # 256 MB last-level cache); MFMA-bound shapes use one copy
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2502_17728_amd import inputs as I
+    assert bench.weight_copies(I.ln_ffn_decode(1)) == 3      # 470 MB of W'
+    assert bench.weight_copies(I.ln_ffn_decode(16)) == 3
+    assert bench.weight_copies(I.ln_qkv_tokens(32)) == 10    # 100.7 MB of W'
+    assert bench.weight_copies(I.LN_QKV) == 1
+    assert bench.weight_copies(I.LN_FFN_PREFILL) == 1
+    assert bench.weight_copies(I.LN_F32_SMALL) == 1          # above the fp32 ridge point

@@ -568,7 +568,9 @@ def test_softmax_pv_small_workload(ops):
 
 
 @pytest.mark.parametrize("BH,L,d,causal", [(3, 200, 64, True), (2, 136, 128, False), (2, 8, 64, True),
-                                           (1, 392, 128, True), (5, 64, 64, False), (2, 520, 128, False)])
+                                           (1, 392, 128, True), (5, 64, 64, False), (2, 520, 128, False),
+                                           # enough 256-query blocks to fill the chip: the 8-wave kernel
+                                           (256, 136, 64, True), (128, 264, 128, False), (86, 776, 64, True)])
 def test_softmax_pv_ragged(ops, BH, L, d, causal):
     _sm_check(ops, I.make_sm_case(BH, L, d, causal, seed=L, from_qk=causal))
 
