@@ -110,7 +110,10 @@ DN_API dn_status ln_linear_prepare(const void* W, const void* gamma, const void*
  * not find a peer's sums within 200 us (a peer not resident on a busy GPU)
  * reduces all its rows itself, so the result never depends on scheduling.
  * (DN_MOMENT_WAIT_TICKS in the environment overrides the wait, in 10 ns
- * ticks; 0 makes every workgroup reduce its rows itself.)  A row holding
+ * ticks; 0 makes every workgroup reduce its rows itself.)  A launch recorded
+ * under stream capture (a HIP graph) uses no mailbox: each workgroup reduces
+ * the moments of its rows alongside its first tile, so every replay of the
+ * graph normalizes with its own inputs' statistics.  A row holding
  * NaN or +-inf gives an all-NaN output row; with eps = 0 a row whose fp32
  * one-pass variance is exactly 0 (a constant row whose squares sum exactly)
  * gives NaN, as (x - mean) / 0 does.  |x| >= 2^64 (fp32 overflow of x^2) is

@@ -97,16 +97,17 @@ __device__ __forceinline__ int64_t packed_chunk(int64_t nb, int64_t kc, int64_t 
 // too small for the 256x256 kernel, for K not a multiple of 64, for fp32, for
 // batched products and for B in [K][N] layout.
 // NST = 2: two LDS stages, the copy of stage s+1 issued while stage s is read.
-// NST > 2 (chunk copies only): a ring of NST stages whose copies run NST-1
-// stages ahead, for tiles whose per-stage matrix work is too short to cover the
-// latency of one copy (the fp32 tiles: 16 fp32 MFMAs per wave and stage).
+// NST > 2 (chunk copies only, NST >= 3): a ring of NST stages whose copies run
+// NST-1 stages ahead, with each stage's fragments read while the previous
+// stage's products run, for tiles whose per-stage matrix work is too short to
+// cover the latency of a copy (the fp32 tiles: 16 fp32 MFMAs per wave and stage).
 // =============================================================================
-template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI, int NST = 2>
+template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI, int NST = 2, int KBT = 2>
 __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
     constexpr int NW = WM * WN;
     constexpr int EPL = elem<T>::per16;  // elements per lane per chunk
     constexpr int KC = elem<T>::kchunk;  // k per chunk
-    constexpr int KB = 2;                // chunks per stage along k
+    constexpr int KB = KBT;              // chunks per stage along k
     constexpr int BK = KC * KB;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int FM = WTM / 16, FN = WTN / 16;
@@ -120,7 +121,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
     static_assert(A_CH % NW == 0 && B_CH % NW == 0, "every wave issues the same number of chunk copies");
     static_assert(!LN || WN <= KB, "moments split: one k-chunk column per wave column");
     static_assert(!SW || FN % 2 == 0, "gate/up fragment pairs");
-    static_assert(NST == 2 || (NST > 2 && !B_KN), "the deep ring moves whole chunks only");
+    static_assert(NST == 2 || (NST >= 3 && !B_KN), "the deep ring moves whole chunks only");
 
     __shared__ __attribute__((aligned(1024))) char smem[NST * STAGE];
     __shared__ float red[LN ? 2 * WN * BM : 1];
@@ -250,28 +251,11 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
     for (int i = 0; i < FM; ++i) s1[i] = s2[i] = 0.f;
 
     constexpr int PER = (A_CH + (B_KN ? 0 : B_CH)) / NW;  // copies per wave per stage
-    if constexpr (NST > 2) {
-        // stages 0 .. NST-2 in flight; stages past the last re-copy the last one into
-        // slots that are never read, so every stage issues the same count
-#pragma unroll
-        for (int j = 0; j < NST - 1; ++j) issue_dma(min(j, nst - 1), j);
-    } else {
-        issue_dma(0, 0);
-        kn_load(0);
-        kn_store(0);
-        wait_vm();
-        __syncthreads();
-    }
 
-    for (int s = 0; s < nst; ++s) {
-        const int buf = NST > 2 ? s % NST : (s & 1);
+    // Fragments of the stage in LDS slot `buf` (stage s: zero past K, causal mask), and the
+    // stage's work on them: the row moments (each element once per workgroup) and the MFMAs.
+    auto read_frags = [&](int buf, u32x4(&af)[FM][KB], u32x4(&bfr)[FN][KB]) {
         const char* base = smem + buf * STAGE;
-        if constexpr (NST > 2) {
-            wait_vmcnt<(NST - 2) * PER>();  // this wave's copies of stage s have landed
-            block_barrier();                // every wave's have, and stage s-1 has been read by all
-            issue_dma(min(s + NST - 1, nst - 1), (s + NST - 1) % NST);  // into the slot of stage s-1
-        }
-        u32x4 af[FM][KB], bfr[FN][KB];
 #pragma unroll
         for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -283,12 +267,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
             for (int kb = 0; kb < KB; ++kb)
                 bfr[fn][kb] = lds_ld16(
                     lds_ptr((char*)base + (A_CH + (wn * FN + fn) * KB + kb) * kChunkBytes + lane * 16));
-
-        if (NST == 2 && s + 1 < nst) {
-            issue_dma(s + 1, buf ^ 1);
-            kn_load(s + 1);
-        }
-
+    };
+    auto compute = [&](int s, u32x4(&af)[FM][KB], u32x4(&bfr)[FN][KB]) {
         const int64_t k0 = (int64_t)s * BK;
         if (k0 + BK > K) {  // K tail: zero the lane-chunks past K (their loads were clamped)
 #pragma unroll
@@ -320,7 +300,6 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 }
             }
         }
-
         if constexpr (LN) {  // row moments from the operand registers, each element once per workgroup
 #pragma unroll
             for (int fm = 0; fm < FM; ++fm)
@@ -328,23 +307,75 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 for (int kb = 0; kb < KB; ++kb)
                     if (kb % WN == wn) chunk_moments<T>(af[fm][kb], s1[fm], s2[fm]);
         }
+        if constexpr (sizeof(T) == 4) {
+            // fp32: a chunk is four dependent 16x16x4 products on one accumulator; taking the
+            // chunk's k-slices in the outer loop interleaves the FM x FN independent chains
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+                        for (int fn = 0; fn < FN; ++fn)
+                            acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                __uint_as_float(af[fm][kb][j]), __uint_as_float(bfr[fn][kb][j]), acc[fm][fn], 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+                    for (int fn = 0; fn < FN; ++fn)
+                        acc[fm][fn] = mfma_chunk<T>(af[fm][kb], bfr[fn][kb], acc[fm][fn]);
+        }
+    };
 
+    if constexpr (NST > 2) {
+        // Deep ring.  Stages 0 .. NST-2 are in flight before the loop; iteration s waits for
+        // stage s+1, refills the slot of stage s-1 (read two iterations ago, consumed one ago)
+        // and reads stage s+1's fragments while stage s's products run.  Stages past the last
+        // re-copy the last one into slots that are never read, so every iteration issues the
+        // same count of copies and the waits are exact.
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
+        for (int j = 0; j < NST - 1; ++j) issue_dma(min(j, nst - 1), j);
+        wait_vmcnt<(NST - 2) * PER>();  // stage 0
+        block_barrier();
+        u32x4 af[2][FM][KB], bfr[2][FN][KB];
+        read_frags(0, af[0], bfr[0]);
+        for (int s = 0; s < nst; s += 2) {
 #pragma unroll
-            for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-                for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma_chunk<T>(af[fm][kb], bfr[fn][kb], acc[fm][fn]);
-
-        if constexpr (NST == 2) {
+            for (int h = 0; h < 2; ++h) {  // unrolled by two: the fragment buffers alternate
+                const int ss = s + h;
+                if (ss < nst) {
+                    wait_vmcnt<(NST - 3) * PER>();  // this wave's copies of stage ss+1 have landed
+                    block_barrier();                // every wave's have
+                    issue_dma(min(ss + NST - 1, nst - 1), (ss + NST - 1) % NST);  // slot of stage ss-1
+                    if (ss + 1 < nst) read_frags((ss + 1) % NST, af[h ^ 1], bfr[h ^ 1]);
+                    compute(ss, af[h], bfr[h]);
+                }
+            }
+        }
+        wait_vmcnt<0>();  // no copy into LDS may outlive the workgroup
+    } else {
+        issue_dma(0, 0);
+        kn_load(0);
+        kn_store(0);
+        wait_vm();
+        __syncthreads();
+        for (int s = 0; s < nst; ++s) {
+            const int buf = s & 1;
+            u32x4 af[FM][KB], bfr[FN][KB];
+            read_frags(buf, af, bfr);
+            if (s + 1 < nst) {
+                issue_dma(s + 1, buf ^ 1);
+                kn_load(s + 1);
+            }
+            compute(s, af, bfr);
             if (s + 1 < nst) kn_store(buf ^ 1);
             wait_vm();
             __syncthreads();
         }
-    }
-    if constexpr (NST > 2) {
-        wait_vmcnt<0>();  // no copy into LDS may outlive the loop (the epilogue reuses no stage, but
-        block_barrier();  // the workgroup must not exit with copies in flight)
     }
 
     // ---- epilogue
@@ -1193,15 +1224,17 @@ hipError_t launch_swiglu_prepare(const void* Wg, const void* Wu, const void* gam
     return hipGetLastError();
 }
 
-template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI, int NST = 2>
+template <class T, int BM, int BN, int WM, int WN, BMode BMODE, Epi EPI, int NST = 2, int KBT = 2>
 static hipError_t run_main(const MainArgs& a, int64_t batch, hipStream_t s) {
     const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
     dim3 grid((unsigned)tiles, (unsigned)batch);
-    main_loop_kernel<T, BM, BN, WM, WN, BMODE, EPI, NST><<<grid, WM * WN * kWave, 0, s>>>(a);
+    main_loop_kernel<T, BM, BN, WM, WN, BMODE, EPI, NST, KBT><<<grid, WM * WN * kWave, 0, s>>>(a);
     return hipGetLastError();
 }
-// fp32 tiles (32 x 64, 4 waves): a 6-stage ring, 72 KiB of LDS, copies five stages ahead
-constexpr int kF32Stages = 6;
+// fp32 tiles (32 x 64, 4 waves): 4 chunks (64 k) per stage, a 4-stage ring of 24 KiB stages,
+// copies three stages ahead (LN -> Linear 128 x 768 x 3072: 15.3 us against 17.9 us with
+// 2-chunk stages in a 6-stage ring and 20.5 us with two 2-chunk stages)
+constexpr int kF32Stages = 4, kF32Chunks = 4;
 
 // Mailbox of the shared row moments: 2 words per row, each (call number << 32) | fp32
 // bits of sum x or sum x^2.  One array per GPU, held until the process ends; in host
@@ -1269,9 +1302,14 @@ static hipError_t run_pipe(const MainArgs& args, hipStream_t s) {
     // Shared moments where the workgroups of a row block are co-resident (one round of
     // workgroups: 256 at one per CU, 512 for the 128 x 128 tiles at two per CU) and number
     // at least 4 (then each wave row of a workgroup owns at most one 16-row fragment).
+    // Not under stream capture: a captured launch keeps its call number on every replay, so
+    // a replay could accept words a previous replay left; captured launches reduce their rows
+    // per workgroup instead (each column group on its first tile, as without the exchange).
     a.mom_slots = nullptr;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusActive;
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess) cap = hipStreamCaptureStatusActive;
     if ((EPI == Epi::kLnDeferred || EPI == Epi::kSwiGlu) && !a.row_stats && ngroups >= 4 &&
-        wgs <= (BT == 128 ? 512 : 256) && a.M <= kMomentRows) {
+        wgs <= (BT == 128 ? 512 : 256) && a.M <= kMomentRows && cap == hipStreamCaptureStatusNone) {
         a.mom_slots = moment_mailbox();
         a.mom_call = next_moment_call();
         a.mom_wait_ticks = moment_wait_ticks();
@@ -1383,7 +1421,7 @@ hipError_t launch_ln_linear_deferred(const void* x, const void* packed, int64_t 
         decode_dispatch<false>(M, a.nblocks, launch);
         return hipGetLastError();
     }
-    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred, kF32Stages>(a, 1, s);
+    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kLnDeferred, kF32Stages, kF32Chunks>(a, 1, s);
     if (use_mid_tiles(M, N, K)) return run_pipe<Epi::kLnDeferred, 128>(a, s);
     if (use_big_tiles(M, N, K)) return run_pipe<Epi::kLnDeferred>(a, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kLnDeferred>(a, 1, s);
@@ -1442,7 +1480,7 @@ hipError_t launch_swiglu_deferred(const void* x, const void* packed, int64_t M, 
             launch(ln_decode_bf16_kernel<4, 2, 2, true, false, 8>, 4, 2);
         return hipGetLastError();
     }
-    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kSwiGlu, kF32Stages>(a, 1, s);
+    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kSwiGlu, kF32Stages, kF32Chunks>(a, 1, s);
     if (use_mid_tiles(M, np, K)) return run_pipe<Epi::kSwiGlu, 128>(a, s);
     if (use_big_tiles(M, np, K)) return run_pipe<Epi::kSwiGlu>(a, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kSwiGlu>(a, 1, s);
@@ -1480,12 +1518,12 @@ hipError_t launch_gemm(const void* A, const void* B, const void* bias, int64_t b
             decode_dispatch<true>(M, a.nblocks, launch);
             return hipGetLastError();
         }
-        if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kGemm, kF32Stages>(a, 1, s);
+        if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kPacked, Epi::kGemm, kF32Stages, kF32Chunks>(a, 1, s);
         if (use_mid_tiles(M, N, K)) return run_pipe<Epi::kGemm, 128>(a, s);
         if (use_big_tiles(M, N, K)) return run_pipe<Epi::kGemm>(a, s);
         return run_main<__bf16, 128, 128, 2, 2, BMode::kPacked, Epi::kGemm>(a, 1, s);
     }
-    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kNK, Epi::kGemm, kF32Stages>(a, batch, s);
+    if (dtype == 0) return run_main<float, 32, 64, 2, 2, BMode::kNK, Epi::kGemm, kF32Stages, kF32Chunks>(a, batch, s);
     if (b_layout == 1) return run_main<__bf16, 128, 128, 2, 2, BMode::kNK, Epi::kGemm>(a, batch, s);
     return run_main<__bf16, 128, 128, 2, 2, BMode::kKN, Epi::kGemm>(a, batch, s);
 }

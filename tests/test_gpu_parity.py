@@ -250,6 +250,36 @@ def test_ln_linear_shared_moments_follow_each_call(ops):
     assert torch.equal(oa, oa2)
 
 
+def test_ln_linear_graph_replays_follow_new_inputs(ops):
+    # a deferred LayerNorm product recorded in a HIP graph (a shape that takes the row-moment
+    # exchange when launched directly) and replayed on new contents of the same x buffer: every
+    # replay normalizes with the new rows' statistics; eager work and a synchronization run
+    # between the replays
+    cases = [I.make_ln_case(1024, 512, 4096, "bf16", seed=60 + i, outliers=2, mean_offset=0.5 * i)
+             for i in range(3)]
+    a = cases[0]
+    w = ops.ln_linear_prepare(cuda(a["W"]), cuda(a["gamma"]), cuda(a["beta"]))
+    x = cuda(a["x"])
+    out = torch.empty((1024, 4096), dtype=torch.bfloat16, device="cuda")
+    ops.ln_linear_deferred(x, w, a["eps"], out=out)  # first call outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        ops.ln_linear_deferred(x, w, a["eps"], out=out)
+    for rep in range(2):
+        for c in cases:
+            x.copy_(cuda(c["x"]))
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            eager = ops.ln_linear_deferred(x, w, a["eps"])
+            torch.cuda.synchronize()
+            ref = oracle.ln_linear(c["x"], a["gamma"], a["beta"], a["W"], None, a["eps"])
+            err, err_e = rowwise_rel_err(out.cpu(), ref), rowwise_rel_err(eager.cpu(), ref)
+            print(f"graph replay {rep}: err={err:.3e}, eager err={err_e:.3e}")
+            assert err <= TOL[torch.bfloat16] and err_e <= TOL[torch.bfloat16], (err, err_e)
+
+
 # Non-finite inputs propagate as in the plain definition (Eq. (1)-(2), Eq. (6)): a row holding
 # NaN, +inf or -inf gives an all-NaN output row and leaves every other row untouched; with
 # eps = 0 a constant row (LayerNorm: zero variance) or an all-zero row (RMSNorm) gives 0/0 = NaN.
