@@ -154,23 +154,31 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     // wait counts rely on it) and skipped work costs no memory traffic.
     const int64_t kend_w = causal ? min(kv_end, qw0 + WROWS) : kv_end;  // exclusive, multiple of 8
     const uint64_t s_base = uniform_u64(Sh);
-    uint32_t s_row[S_LD], s_p8[S_LD];
+    uint32_t s_row[S_LD], s_p8[S_LD], s_off[S_LD];
 #pragma unroll
     for (int j = 0; j < S_LD; ++j) {
         const int r = 8 * j + (lane >> 3);
         const int64_t q = qw0 + r < Lq ? qw0 + r : Lq - 1;
         s_row[j] = (uint32_t)(q * Lk * 2);
         s_p8[j] = (uint32_t)(((lane & 7) ^ s_swz(r)) * 8);
+        s_off[j] = s_row[j] + 2 * s_p8[j];
     }
     const uint32_t s_lds = smem_addr + (uint32_t)(NS * V_BYTES + wave * PF * S_SLOT);
     const uint32_t klast = (uint32_t)(kend_w - 8);  // the wave's last 8-key group
-    auto issue_s = [&](int step) {
+    // FAST: no key of the step is clamped (the caller's loop guarantees it), so the step's
+    // offset goes into the scalar base and the lanes' offsets stay fixed
+    auto issue_s = [&](int step, auto fast) {
         const uint32_t dst = s_lds + (uint32_t)((step % PF) * S_SLOT);
         const uint32_t k0 = (uint32_t)step * BKV;
+        if constexpr (decltype(fast)::value) {
 #pragma unroll
-        for (int j = 0; j < S_LD; ++j) {
-            const uint32_t key = k0 + s_p8[j] < klast ? k0 + s_p8[j] : klast;  // a select, no branch
-            g2lds16_async_sb(s_base, s_row[j] + key * 2u, dst + j * kChunkBytes);
+            for (int j = 0; j < S_LD; ++j) g2lds16_async_sb(s_base + 2u * k0, s_off[j], dst + j * kChunkBytes);
+        } else {
+#pragma unroll
+            for (int j = 0; j < S_LD; ++j) {
+                const uint32_t key = k0 + s_p8[j] < klast ? k0 + s_p8[j] : klast;  // a select, no branch
+                g2lds16_async_sb(s_base, s_row[j] + key * 2u, dst + j * kChunkBytes);
+            }
         }
     };
     // fragment reads: lane (i, G) takes row 16f + i, piece 4kc + G (8 keys), the B-operand order
@@ -198,13 +206,23 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     }
     const uint64_t v_base = uniform_u64(Vh);
     const uint32_t vlast = (uint32_t)(Lk - 1);
-    auto issue_v = [&](int step) {
+    uint32_t vc_off[V_INS];
+#pragma unroll
+    for (int j = 0; j < V_INS; ++j) vc_off[j] = v_row[j] * (uint32_t)VROW + v_p16[j];
+    auto issue_v = [&](int step, auto fast) {  // FAST: every row of the step exists
         const uint32_t base = smem_addr + (uint32_t)((step % NS) * V_BYTES);
         const uint32_t k0 = (uint32_t)step * BKV;
+        if constexpr (decltype(fast)::value) {
 #pragma unroll
-        for (int j = 0; j < V_INS; ++j) {
-            const uint32_t key = k0 + v_row[j] < vlast ? k0 + v_row[j] : vlast;  // rows past Lk clamp onto the last
-            g2lds16_async_sb(v_base, key * (uint32_t)VROW + v_p16[j], base + (uint32_t)((wave + j * NW) * kChunkBytes));
+            for (int j = 0; j < V_INS; ++j)
+                g2lds16_async_sb(v_base + (uint64_t)k0 * VROW, vc_off[j], base + (uint32_t)((wave + j * NW) * kChunkBytes));
+        } else {
+#pragma unroll
+            for (int j = 0; j < V_INS; ++j) {
+                const uint32_t key = k0 + v_row[j] < vlast ? k0 + v_row[j] : vlast;  // rows past Lk clamp onto the last
+                g2lds16_async_sb(v_base, key * (uint32_t)VROW + v_p16[j],
+                                 base + (uint32_t)((wave + j * NW) * kChunkBytes));
+            }
         }
     };
 
@@ -308,10 +326,10 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     // of step 0 computed in iteration -1.
 #pragma unroll
     for (int j = -AHEAD; j < -1; ++j) {
-        if (j + NS - 1 >= 0) issue_v(j + NS - 1);
-        if (j + 1 + PF >= 0) issue_s(j + 1 + PF);
+        if (j + NS - 1 >= 0) issue_v(j + NS - 1, std::false_type{});
+        if (j + 1 + PF >= 0) issue_s(j + 1 + PF, std::false_type{});
     }
-    issue_v(NS - 2);
+    issue_v(NS - 2, std::false_type{});
     wait_vmcnt_asm<(PF - 1) * S_LD>();  // S(0) is complete once only the later S copies may remain
     u32x4 pf[QW][2];
     float alpha[QW];
@@ -323,7 +341,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
         numerators(sc, pf, alpha);
     }
     raised = false;  // the partial sums are still zero: nothing to rescale
-    issue_s(PF);     // into the slot step 0 vacated
+    issue_s(PF, std::false_type{});  // into the slot step 0 vacated
 
     // Iteration s: the products of step s (V(s) from the ring, numerators
     // computed one iteration earlier) and, independent of them, the numerators
@@ -334,11 +352,14 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     // two numerator buffers used in turn: the loop is unrolled by two so that
     // neither is ever copied
     u32x4 pf2[QW][2];
-    auto iteration = [&](int s, u32x4(&pcur)[QW][2], u32x4(&pnext)[QW][2]) {
+    // FAST: the copies this iteration issues need no clamping and step s+1 is not an edge
+    // step (both follow from the bound of the loop that passes it, see below).
+    auto iteration = [&](int s, u32x4(&pcur)[QW][2], u32x4(&pnext)[QW][2], auto fast) {
+        constexpr bool FAST = decltype(fast)::value;
         wait_vmcnt_asm<WAIT_N>();  // S(s+1) and this wave's V copies of step s are complete
         wait_lgkm0();              // this wave's LDS reads of step s-1 are complete
         block_barrier();
-        issue_v(s + NS - 1);  // into the slot step s-1 vacated
+        issue_v(s + NS - 1, fast);  // into the slot step s-1 vacated
         if (__any(raised)) {
 #pragma unroll
             for (int f = 0; f < QW; ++f) {
@@ -349,7 +370,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
         }
         u32x4 sc[QW][2];
         read_s(s + 1, sc);
-        if (is_edge(s + 1)) mask_scores(s + 1, sc);
+        if (!FAST && is_edge(s + 1)) mask_scores(s + 1, sc);
         const char* vb = smem + (s % NS) * V_BYTES;
         // V^T fragments of key chunk kc (A operand): two transposing reads of 4 keys per d block
         auto read_v = [&](int kc, u32x4(&vf)[DB]) {
@@ -372,7 +393,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
             u32x4 vf[DB];
             read_v(0, vf);
             raised = numerators(sc, pnext, alpha);
-            issue_s(s + 1 + PF);  // the slot of S(s+1) has been read
+            issue_s(s + 1 + PF, fast);  // the slot of S(s+1) has been read
             products(0, vf);
         }
         {
@@ -380,10 +401,33 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
             read_v(1, vf);
             products(1, vf);
         }
+        // The next step's numerators are consumed in the next iteration, which the loop's
+        // exit test may skip; without these uses the compiler sinks their exponentials past
+        // that test, out of this block and away from the products they should run beside.
+#pragma unroll
+        for (int f = 0; f < QW; ++f) {
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) asm volatile("" ::"v"(pnext[f][kc]));
+            asm volatile("" ::"v"(alpha[f]));
+        }
     };
-    for (int s = 0; s < nsteps; s += 2) {
-        iteration(s, pf, pf2);
-        if (s + 1 < nsteps) iteration(s + 1, pf2, pf);
+    // Iterations s < fast_end issue only unclamped copies: the S copy of step s+1+PF lies
+    // wholly before the wave's last 8-key group, (s+1+PF+1)·64 - 8 <= klast, and the V copy
+    // of step s+NS-1 wholly inside the keys, (s+NS)·64 - 1 <= vlast.  Then step s+1 lies
+    // wholly before the wave's first query (PF >= 1) and before the end: not an edge step.
+    const int64_t a_s = (int64_t)klast + 8 - BKV, a_v = (int64_t)vlast + 1 - BKV;
+    int fast_end = nsteps;
+    fast_end = a_s < 0 ? 0 : min(fast_end, (int)(a_s / BKV) - PF);
+    fast_end = a_v < 0 ? 0 : min(fast_end, (int)(a_v / BKV) - NS + 2);
+    fast_end = __builtin_amdgcn_readfirstlane(max(fast_end, 0));
+    int s = 0;
+    for (; s + 1 < fast_end; s += 2) {  // both iterations of the pair run: no exit test between them
+        iteration(s, pf, pf2, std::true_type{});
+        iteration(s + 1, pf2, pf, std::true_type{});
+    }
+    for (; s < nsteps; s += 2) {
+        iteration(s, pf, pf2, std::false_type{});
+        if (s + 1 < nsteps) iteration(s + 1, pf2, pf, std::false_type{});
     }
     wait_vmcnt_asm<0>();  // no copy into LDS may outlive the workgroup
 
