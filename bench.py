@@ -66,13 +66,9 @@ KERNEL_SOURCES = {"softmax_pv_deferred": ("softmax_pv.hip", "dn_device.hpp"),
                   "rms_swiglu_deferred": ("ln_gemm.hip", "dn_device.hpp")}
 TRAFFIC = {
     ("softmax_pv_deferred", "causal_softmax_pv_bf16_32x8192x8192_d128"): {
-        "sha256": ("e46caf2ff7e623fd557409ac5dcb54a94b8139090cd828cf9c656322269fcf42",
+        "sha256": ("dfea4bf89541f7e6c430cb4992f64612a4548b3c0034efc22c769ab24f62aaff",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 1151405, "fetch_scale": 1.99992, "write_kib": 66182, "write_scale": 1.0},
-    ("softmax_pv_deferred", "softmax_pv_bf16_12x512x512_d64"): {
-        "sha256": ("e46caf2ff7e623fd557409ac5dcb54a94b8139090cd828cf9c656322269fcf42",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 3648, "fetch_scale": 1.99990, "write_kib": 768, "write_scale": 1.0},
+        "fetch_kib": 1151338, "fetch_scale": 1.99988, "write_kib": 66245, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
         "sha256": ("9319e05eaf13fc87cd250397763647052a2293a02a7041bd93c7949d6e3a7ea5",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
@@ -90,14 +86,14 @@ TRAFFIC = {
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
         "fetch_kib": 6228, "fetch_scale": 1.99990, "write_kib": 1536, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
-        "sha256": ("76dc4fc2b2825ebd51688a01e9472cb45cd21d7dbf8e43ec98ab907f8cf91adf",
-                   "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 134669, "fetch_scale": 1.99993, "write_kib": 65536, "write_scale": 1.0},
+        "sha256": ("5526e2ed23dd4cd303791dd3c8321b273869027224059114d5e02fdb98ac51d1",
+                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
+        "fetch_kib": 133530, "fetch_scale": 1.99991, "write_kib": 65536, "write_scale": 1.0},
     # the split kernel and the merge kernel together (530515 + 145 KiB read, 266 + 64 KiB written)
     ("attention_decode_deferred", "decode_attention_bf16_256x1x8192_d128"): {
-        "sha256": ("76dc4fc2b2825ebd51688a01e9472cb45cd21d7dbf8e43ec98ab907f8cf91adf",
-                   "c5b8ebce4ee91abda916790fb6cc88a60ca33c792a330c08054503dc1aea3a2b"),
-        "fetch_kib": 530660, "fetch_scale": 1.99993, "write_kib": 330, "write_scale": 1.0},
+        "sha256": ("5526e2ed23dd4cd303791dd3c8321b273869027224059114d5e02fdb98ac51d1",
+                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
+        "fetch_kib": 530660, "fetch_scale": 1.99989, "write_kib": 330, "write_scale": 1.0},
 }
 
 

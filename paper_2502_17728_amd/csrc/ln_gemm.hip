@@ -268,9 +268,12 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 bfr[fn][kb] = lds_ld16(
                     lds_ptr((char*)base + (A_CH + (wn * FN + fn) * KB + kb) * kChunkBytes + lane * 16));
     };
-    auto compute = [&](int s, u32x4(&af)[FM][KB], u32x4(&bfr)[FN][KB]) {
+    // TAIL: the stage may reach past K (only the last one can).  MOM: 0 -- the moments of the
+    // chunks whose index matches the wave column (each element once per workgroup); 1 -- of
+    // every chunk (the deep ring gives them all to wave column 0); 2 -- none.
+    auto compute = [&](int s, u32x4(&af)[FM][KB], u32x4(&bfr)[FN][KB], auto tail, auto mom) {
         const int64_t k0 = (int64_t)s * BK;
-        if (k0 + BK > K) {  // K tail: zero the lane-chunks past K (their loads were clamped)
+        if (decltype(tail)::value && k0 + BK > K) {  // K tail: zero the lane-chunks past K (their loads were clamped)
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb) {
                 if (k0 + kb * KC + (lane >> 4) * EPL >= K) {
@@ -300,12 +303,13 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 }
             }
         }
-        if constexpr (LN) {  // row moments from the operand registers, each element once per workgroup
+        constexpr int MOM = decltype(mom)::value;
+        if constexpr (LN && MOM < 2) {  // row moments from the operand registers, each element once per workgroup
 #pragma unroll
             for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
                 for (int kb = 0; kb < KB; ++kb)
-                    if (kb % WN == wn) chunk_moments<T>(af[fm][kb], s1[fm], s2[fm]);
+                    if (MOM == 1 || kb % WN == wn) chunk_moments<T>(af[fm][kb], s1[fm], s2[fm]);
         }
         if constexpr (sizeof(T) == 4) {
             // fp32: a chunk is four dependent 16x16x4 products on one accumulator; taking the
@@ -336,27 +340,44 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
         // stage s+1, refills the slot of stage s-1 (read two iterations ago, consumed one ago)
         // and reads stage s+1's fragments while stage s's products run.  Stages past the last
         // re-copy the last one into slots that are never read, so every iteration issues the
-        // same count of copies and the waits are exact.
+        // same count of copies and the waits are exact.  Only the last stage can reach past K,
+        // and the row moments go to wave column 0 alone (a uniform choice made once, outside
+        // the loop), so the loop body has no branch: its products, fragment reads and moment
+        // arithmetic form one block that the scheduler interleaves.
+        auto deep = [&](auto mom) {
 #pragma unroll
-        for (int j = 0; j < NST - 1; ++j) issue_dma(min(j, nst - 1), j);
-        wait_vmcnt<(NST - 2) * PER>();  // stage 0
-        block_barrier();
-        u32x4 af[2][FM][KB], bfr[2][FN][KB];
-        read_frags(0, af[0], bfr[0]);
-        for (int s = 0; s < nst; s += 2) {
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {  // unrolled by two: the fragment buffers alternate
-                const int ss = s + h;
-                if (ss < nst) {
-                    wait_vmcnt<(NST - 3) * PER>();  // this wave's copies of stage ss+1 have landed
-                    block_barrier();                // every wave's have
-                    issue_dma(min(ss + NST - 1, nst - 1), (ss + NST - 1) % NST);  // slot of stage ss-1
-                    if (ss + 1 < nst) read_frags((ss + 1) % NST, af[h ^ 1], bfr[h ^ 1]);
-                    compute(ss, af[h], bfr[h]);
-                }
+            for (int j = 0; j < NST - 1; ++j) issue_dma(min(j, nst - 1), j);
+            wait_vmcnt<(NST - 2) * PER>();  // stage 0
+            block_barrier();
+            u32x4 af[2][FM][KB], bfr[2][FN][KB];
+            read_frags(0, af[0], bfr[0]);
+            auto body = [&](int ss, auto h, auto tail) {
+                constexpr int H = decltype(h)::value;
+                wait_vmcnt<(NST - 3) * PER>();  // this wave's copies of stage ss+1 have landed
+                block_barrier();                // every wave's have
+                issue_dma(min(ss + NST - 1, nst - 1), (ss + NST - 1) % NST);  // slot of stage ss-1
+                if (!decltype(tail)::value || ss + 1 < nst) read_frags((ss + 1) % NST, af[H ^ 1], bfr[H ^ 1]);
+                compute(ss, af[H], bfr[H], tail, mom);
+            };
+            using h0 = std::integral_constant<int, 0>;
+            using h1 = std::integral_constant<int, 1>;
+            int ss = 0;
+            for (; ss + 2 <= nst - 1; ss += 2) {  // stages before the last: no tail, no exit test inside
+                body(ss, h0{}, std::false_type{});
+                body(ss + 1, h1{}, std::false_type{});
             }
-        }
-        wait_vmcnt<0>();  // no copy into LDS may outlive the workgroup
+            if (ss < nst - 1) {
+                body(ss, h0{}, std::false_type{});
+                body(ss + 1, h1{}, std::true_type{});
+            } else {
+                body(ss, h0{}, std::true_type{});
+            }
+            wait_vmcnt<0>();  // no copy into LDS may outlive the workgroup
+        };
+        if (LN && __builtin_amdgcn_readfirstlane(wn) == 0)
+            deep(std::integral_constant<int, 1>{});
+        else
+            deep(std::integral_constant<int, 2>{});
     } else {
         issue_dma(0, 0);
         kn_load(0);
@@ -371,7 +392,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
                 issue_dma(s + 1, buf ^ 1);
                 kn_load(s + 1);
             }
-            compute(s, af, bfr);
+            compute(s, af, bfr, std::true_type{}, std::integral_constant<int, 0>{});
             if (s + 1 < nst) kn_store(buf ^ 1);
             wait_vm();
             __syncthreads();

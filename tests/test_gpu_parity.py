@@ -505,6 +505,31 @@ def _swiglu_check(ops, case, rows=None):
     return h
 
 
+def test_rms_swiglu_graph_replays_follow_new_inputs(ops):
+    # the gated product recorded in a HIP graph (a shape whose direct launches exchange row
+    # moments between workgroups) and replayed on new contents of the same x buffer
+    cases = [I.make_swiglu_case(1024, 512, 2048, "bf16", seed=70 + i, outliers=2) for i in range(3)]
+    a = cases[0]
+    w = ops.swiglu_prepare(cuda(a["Wg"]), cuda(a["Wu"]), cuda(a["gamma"]))
+    x = cuda(a["x"])
+    out = torch.empty((1024, 2048), dtype=torch.bfloat16, device="cuda")
+    ops.rms_swiglu_deferred(x, w, a["eps"], out=out)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        ops.rms_swiglu_deferred(x, w, a["eps"], out=out)
+    for rep in range(2):
+        for c in cases:
+            x.copy_(cuda(c["x"]))
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            ref = oracle.rms_swiglu(c["x"], a["gamma"], a["Wg"], a["Wu"], a["eps"])
+            err = rowwise_rel_err(out.cpu(), ref)
+            print(f"swiglu graph replay {rep}: err={err:.3e}")
+            assert err <= TOL[torch.bfloat16], err
+
+
 @pytest.mark.parametrize("M,K,N", [(37, 104, 72), (1, 8, 8), (130, 256, 200)])
 def test_rms_swiglu_f32_ragged(ops, M, K, N):
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "f32", seed=M))
