@@ -93,24 +93,31 @@ __device__ __forceinline__ uint2 lds_tr16(const char* p) {
 }
 }  // namespace sm
 
-template <int D, int NW, int QW, int NS, int PF>
+// KSP > 1 (non-causal only): the workgroup's NW waves are KSP groups of NW / KSP query
+// waves; group g walks the g-th of KSP equal runs of key steps, and the groups' partial
+// sums are merged in LDS at the end (Eq. (8) over key ranges, each with its own reference
+// maximum) -- for grids too small to fill the chip, where the steps one wave walks in
+// sequence set the time.
+template <int D, int NW, int QW, int NS, int PF, int KSP = 1>
 __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __restrict__ S,
                                                          const __bf16* __restrict__ V, int BH,
                                                          int64_t Lq, int64_t Lk, int causal, int nqb,
                                                          __bf16* __restrict__ out) {
     using namespace sm;
-    constexpr int BQ = NW * QW * 16;       // queries per workgroup (QW 16-query fragments per wave)
+    constexpr int NQW = NW / KSP;          // waves per key group (one per 16 x QW queries)
+    constexpr int BQ = NQW * QW * 16;      // queries per workgroup (QW 16-query fragments per wave)
     constexpr int BKV = 64;                // keys per step
     constexpr int VROW = D * 2;            // bytes per V row
     constexpr int V_BYTES = BKV * VROW;    // one V ring slot
-    constexpr int V_INS = V_BYTES / kChunkBytes / NW;  // V copies per wave per step
+    constexpr int V_INS = V_BYTES / kChunkBytes / NQW;  // V copies per wave per step
     constexpr int WROWS = QW * 16;         // score rows per wave
     constexpr int S_SLOT = WROWS * BKV * 2;  // one step of a wave's scores
     constexpr int S_LD = WROWS / 8;        // S copies per wave per step (8 rows x 128 B each)
     constexpr int VPR = VROW / 16;         // 16-byte pieces per V row
     constexpr int VRPI = kChunkBytes / VROW;  // V rows per copy instruction
     constexpr int DB = D / 16;
-    static_assert(V_BYTES % (kChunkBytes * NW) == 0, "V tile split evenly over the waves");
+    static_assert(V_BYTES % (kChunkBytes * NQW) == 0, "V tile split evenly over the waves");
+    static_assert(KSP >= 1 && NW % KSP == 0, "key groups of equal size");
     static_assert(NS >= 2 && NS <= 4 && PF >= 2 && PF >= NS - 2 && PF <= NS, "ring depths the counts assume");
     // Memory-op order per iteration j: [top] V copies of step j+NS-1, [middle] S copies of step
     // j+1+PF.  At the top of iteration s the wave needs S(s+1) and V(s); the ops issued after each:
@@ -119,7 +126,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     constexpr int WAIT_N = AFTER_S < AFTER_V ? AFTER_S : AFTER_V;
     constexpr int AHEAD = PF + 1 > NS - 1 ? PF + 1 : NS - 1;  // prologue length
 
-    __shared__ __attribute__((aligned(1024))) char smem[NS * V_BYTES + NW * PF * S_SLOT];
+    __shared__ __attribute__((aligned(1024))) char smem[KSP * NS * V_BYTES + NW * PF * S_SLOT];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -129,13 +136,18 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     const int qb = causal ? (nqb - 1 - t % nqb) : (t % nqb);
     const int64_t q0 = (int64_t)qb * BQ;
     const int64_t kv_end = causal ? min(Lk, q0 + BQ) : Lk;
-    const int nsteps = (int)((kv_end + BKV - 1) / BKV);
+    // key group: waves kg * NQW .. kg * NQW + NQW - 1 walk global steps gs0 .. gs0 + nsteps - 1;
+    // keys from kv_end_g on are masked for the group (the last group: kv_end)
+    const int qg = wave % NQW, kg = wave / NQW;
+    const int nsteps = (int)((((kv_end + BKV - 1) / BKV) + KSP - 1) / KSP);
+    const int gs0 = kg * nsteps;
+    const int64_t kv_end_g = min(kv_end, (int64_t)(gs0 + nsteps) * BKV);
 
     const __bf16* Sh = S + (int64_t)h * Lq * Lk;
     const __bf16* Vh = V + (int64_t)h * Lk * D;
     __bf16* Oh = out + (int64_t)h * Lq * D;
 
-    const int64_t qw0 = q0 + wave * WROWS;  // first query of this wave
+    const int64_t qw0 = q0 + qg * WROWS;  // first query of this wave
     const int G = lane >> 4, i = lane & 15;
     int64_t qrow[QW];
 #pragma unroll
@@ -163,13 +175,13 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
         s_p8[j] = (uint32_t)(((lane & 7) ^ s_swz(r)) * 8);
         s_off[j] = s_row[j] + 2 * s_p8[j];
     }
-    const uint32_t s_lds = smem_addr + (uint32_t)(NS * V_BYTES + wave * PF * S_SLOT);
+    const uint32_t s_lds = smem_addr + (uint32_t)(KSP * NS * V_BYTES + wave * PF * S_SLOT);
     const uint32_t klast = (uint32_t)(kend_w - 8);  // the wave's last 8-key group
     // FAST: no key of the step is clamped (the caller's loop guarantees it), so the step's
     // offset goes into the scalar base and the lanes' offsets stay fixed
     auto issue_s = [&](int step, auto fast) {
         const uint32_t dst = s_lds + (uint32_t)((step % PF) * S_SLOT);
-        const uint32_t k0 = (uint32_t)step * BKV;
+        const uint32_t k0 = (uint32_t)(gs0 + step) * BKV;
         if constexpr (decltype(fast)::value) {
 #pragma unroll
             for (int j = 0; j < S_LD; ++j) g2lds16_async_sb(s_base + 2u * k0, s_off[j], dst + j * kChunkBytes);
@@ -185,7 +197,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     int s_rd[2];
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) s_rd[kc] = i * 128 + (((4 * kc + G) ^ s_swz(i)) << 4);
-    const char* s_ring = smem + NS * V_BYTES + wave * PF * S_SLOT;
+    const char* s_ring = smem + KSP * NS * V_BYTES + wave * PF * S_SLOT;
     auto read_s = [&](int step, u32x4(&r)[QW][2]) {
         const char* b = s_ring + (step % PF) * S_SLOT;
 #pragma unroll
@@ -200,7 +212,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     uint32_t v_row[V_INS], v_p16[V_INS];
 #pragma unroll
     for (int j = 0; j < V_INS; ++j) {
-        const int r = (wave + j * NW) * VRPI + lane / VPR;
+        const int r = (qg + j * NQW) * VRPI + lane / VPR;
         v_row[j] = (uint32_t)r;
         v_p16[j] = (uint32_t)(((lane % VPR) ^ v_swz<D>(r)) * 16);
     }
@@ -210,18 +222,18 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
 #pragma unroll
     for (int j = 0; j < V_INS; ++j) vc_off[j] = v_row[j] * (uint32_t)VROW + v_p16[j];
     auto issue_v = [&](int step, auto fast) {  // FAST: every row of the step exists
-        const uint32_t base = smem_addr + (uint32_t)((step % NS) * V_BYTES);
-        const uint32_t k0 = (uint32_t)step * BKV;
+        const uint32_t base = smem_addr + (uint32_t)((kg * NS + step % NS) * V_BYTES);
+        const uint32_t k0 = (uint32_t)(gs0 + step) * BKV;
         if constexpr (decltype(fast)::value) {
 #pragma unroll
             for (int j = 0; j < V_INS; ++j)
-                g2lds16_async_sb(v_base + (uint64_t)k0 * VROW, vc_off[j], base + (uint32_t)((wave + j * NW) * kChunkBytes));
+                g2lds16_async_sb(v_base + (uint64_t)k0 * VROW, vc_off[j], base + (uint32_t)((qg + j * NQW) * kChunkBytes));
         } else {
 #pragma unroll
             for (int j = 0; j < V_INS; ++j) {
                 const uint32_t key = k0 + v_row[j] < vlast ? k0 + v_row[j] : vlast;  // rows past Lk clamp onto the last
                 g2lds16_async_sb(v_base, key * (uint32_t)VROW + v_p16[j],
-                                 base + (uint32_t)((wave + j * NW) * kChunkBytes));
+                                 base + (uint32_t)((qg + j * NQW) * kChunkBytes));
             }
         }
     };
@@ -298,10 +310,10 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     // bf16 scores are replaced by -inf (0xff80), two per word.  A step wholly
     // above a wave's queries, or past the last step, is masked entirely.
     auto mask_scores = [&](int step, u32x4(&sc)[QW][2]) {
-        const int64_t k0 = (int64_t)step * BKV;
+        const int64_t k0 = (int64_t)(gs0 + step) * BKV;
 #pragma unroll
         for (int f = 0; f < QW; ++f) {
-            const int64_t last = causal ? (qrow[f] < kv_end - 1 ? qrow[f] : kv_end - 1) : kv_end - 1;
+            const int64_t last = causal ? (qrow[f] < kv_end - 1 ? qrow[f] : kv_end - 1) : kv_end_g - 1;
             const int64_t rel = last - k0;  // last kept key, relative to the step
             const int lim = rel < 0 ? -1 : (rel > BKV ? BKV : (int)rel);
 #pragma unroll
@@ -314,9 +326,9 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
                 }
         }
     };
-    const int qw0i = (int)qw0, kv_endi = (int)kv_end;  // positions fit 32 bits (Lq * Lk <= 2^31)
+    const int qw0i = (int)qw0, kv_endi = (int)kv_end_g;  // positions fit 32 bits (Lq * Lk <= 2^31)
     auto is_edge = [&](int step) {
-        const int k0 = step * BKV;
+        const int k0 = (gs0 + step) * BKV;
         return (causal && k0 + BKV - 1 > qw0i) || k0 + BKV > kv_endi;
     };
 
@@ -371,7 +383,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
         u32x4 sc[QW][2];
         read_s(s + 1, sc);
         if (!FAST && is_edge(s + 1)) mask_scores(s + 1, sc);
-        const char* vb = smem + (s % NS) * V_BYTES;
+        const char* vb = smem + (kg * NS + s % NS) * V_BYTES;  // this key group's V ring
         // V^T fragments of key chunk kc (A operand): two transposing reads of 4 keys per d block
         auto read_v = [&](int kc, u32x4(&vf)[DB]) {
 #pragma unroll
@@ -411,14 +423,17 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
             asm volatile("" ::"v"(alpha[f]));
         }
     };
-    // Iterations s < fast_end issue only unclamped copies: the S copy of step s+1+PF lies
-    // wholly before the wave's last 8-key group, (s+1+PF+1)·64 - 8 <= klast, and the V copy
-    // of step s+NS-1 wholly inside the keys, (s+NS)·64 - 1 <= vlast.  Then step s+1 lies
-    // wholly before the wave's first query (PF >= 1) and before the end: not an edge step.
+    // Iterations s < fast_end (local steps; global step = gs0 + local) issue only unclamped
+    // copies and mask nothing: the S copy of step s+1+PF lies wholly before the wave's last
+    // 8-key group, (s+1+PF+1)·64 - 8 <= klast, the V copy of step s+NS-1 wholly inside the
+    // keys, (s+NS)·64 - 1 <= vlast, and step s+1 is no edge step: (s+1)·64 + 63 <= the wave's
+    // first query (causal) and (s+2)·64 <= kv_end_g.
     const int64_t a_s = (int64_t)klast + 8 - BKV, a_v = (int64_t)vlast + 1 - BKV;
+    const int64_t a_e = min(causal ? (int64_t)qw0i - (BKV - 1) : (int64_t)kv_endi, (int64_t)kv_endi - BKV);
     int fast_end = nsteps;
-    fast_end = a_s < 0 ? 0 : min(fast_end, (int)(a_s / BKV) - PF);
-    fast_end = a_v < 0 ? 0 : min(fast_end, (int)(a_v / BKV) - NS + 2);
+    fast_end = a_s < 0 ? 0 : min(fast_end, (int)(a_s / BKV) - PF - gs0);
+    fast_end = a_v < 0 ? 0 : min(fast_end, (int)(a_v / BKV) - NS + 2 - gs0);
+    fast_end = a_e < 0 ? 0 : min(fast_end, (int)(a_e / BKV) - gs0);
     fast_end = __builtin_amdgcn_readfirstlane(max(fast_end, 0));
     int s = 0;
     for (; s + 1 < fast_end; s += 2) {  // both iterations of the pair run: no exit test between them
@@ -430,6 +445,44 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
         if (s + 1 < nsteps) iteration(s + 1, pf2, pf, std::false_type{});
     }
     wait_vmcnt_asm<0>();  // no copy into LDS may outlive the workgroup
+
+    if constexpr (KSP > 1) {
+        // Merge of the key groups (KSP = 2): group 1 leaves its partial products, its row sum
+        // and its reference maximum in LDS (the rings are idle now), group 0 rescales both to
+        // the larger reference, out = (acc0 2^(m0-m) + acc1 2^(m1-m)) / (l0 2^(m0-m) + l1 2^(m1-m)).
+        // A group without any unmasked key has m = -inf and contributes nothing.
+        static_assert(KSP == 2, "two key groups");
+        constexpr int NF = QW * (DB * 4 + 2);  // floats per lane
+        float* xch = reinterpret_cast<float*>(smem) + (qg * kWave + lane) * NF;
+        wait_lgkm0();
+        block_barrier();  // every wave is done with the rings
+        if (kg == 1) {
+#pragma unroll
+            for (int f = 0; f < QW; ++f) {
+#pragma unroll
+                for (int b = 0; b < DB; ++b)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) xch[f * (DB * 4 + 2) + b * 4 + e] = acc[f][b][e];
+                xch[f * (DB * 4 + 2) + DB * 4] = accl[f][0];
+                xch[f * (DB * 4 + 2) + DB * 4 + 1] = mref[f];
+            }
+        }
+        __syncthreads();
+        if (kg == 1) return;
+#pragma unroll
+        for (int f = 0; f < QW; ++f) {
+            const float m1 = xch[f * (DB * 4 + 2) + DB * 4 + 1], l1 = xch[f * (DB * 4 + 2) + DB * 4];
+            const float m = mref[f] > m1 ? mref[f] : m1;
+            const float a0 = mref[f] == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(mref[f] - m);
+            const float a1 = m1 == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m1 - m);
+#pragma unroll
+            for (int b = 0; b < DB; ++b)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    acc[f][b][e] = __builtin_fmaf(acc[f][b][e], a0, xch[f * (DB * 4 + 2) + b * 4 + e] * a1);
+            accl[f][0] = __builtin_fmaf(accl[f][0], a0, l1 * a1);
+        }
+    }
 
     // ---- epilogue: the single deferred division, one rounding to bf16
 #pragma unroll
@@ -447,14 +500,14 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     }
 }
 
-template <int D, int NW, int QW, int NS, int PF>
+template <int D, int NW, int QW, int NS, int PF, int KSP = 1>
 static hipError_t run_softmax_pv(const void* S, const void* V, int64_t BH, int64_t Lq, int64_t Lk, int causal,
                                  void* out, hipStream_t s) {
-    constexpr int BQ = NW * QW * 16;
+    constexpr int BQ = NW / KSP * QW * 16;
     const int nqb = (int)((Lq + BQ - 1) / BQ);
     dim3 grid((unsigned)(BH * nqb));
-    softmax_pv_kernel<D, NW, QW, NS, PF><<<grid, NW * 64, 0, s>>>((const __bf16*)S, (const __bf16*)V, (int)BH, Lq,
-                                                                  Lk, causal, nqb, (__bf16*)out);
+    softmax_pv_kernel<D, NW, QW, NS, PF, KSP><<<grid, NW * 64, 0, s>>>((const __bf16*)S, (const __bf16*)V, (int)BH,
+                                                                       Lq, Lk, causal, nqb, (__bf16*)out);
     return hipGetLastError();
 }
 
@@ -471,10 +524,17 @@ constexpr int64_t kSmCUs = 256;
 hipError_t launch_softmax_pv_deferred(const void* S, const void* V, int64_t BH, int64_t Lq, int64_t Lk, int64_t d,
                                       int causal, void* out, hipStream_t s) {
     const bool small = BH * ((Lq + 255) / 256) < kSmCUs;
+    // small and non-causal with more than one key step: two key groups per workgroup, each
+    // walking half the steps with 2-deep rings, merged in LDS (12 x 512 x 512, d64, graph
+    // replays: 6.8 us unsplit, 5.4 us split; 3- and 4-deep rings 5.7-6.0 us, one query wave
+    // per group 6.3-6.5 us)
+    const bool split = small && !causal && Lk > 64;
     if (d == 64) {
+        if (split) return run_softmax_pv<64, 4, 1, 2, 2, 2>(S, V, BH, Lq, Lk, causal, out, s);
         if (small) return run_softmax_pv<64, 2, 1, 4, 4>(S, V, BH, Lq, Lk, causal, out, s);
         return run_softmax_pv<64, kSmWaves, kSmFrags, kSmStages, kSmPrefetch>(S, V, BH, Lq, Lk, causal, out, s);
     }
+    if (split) return run_softmax_pv<128, 4, 1, 2, 2, 2>(S, V, BH, Lq, Lk, causal, out, s);
     if (small) return run_softmax_pv<128, 2, 1, 3, 3>(S, V, BH, Lq, Lk, causal, out, s);
     return run_softmax_pv<128, kSmWaves, kSmFrags, kSmStages, kSmPrefetch>(S, V, BH, Lq, Lk, causal, out, s);
 }
