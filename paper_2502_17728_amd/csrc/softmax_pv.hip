@@ -35,9 +35,10 @@
 // vmcnt values.
 //
 // Schedule.  Iteration s issues the products of step s (numerators computed in
-// iteration s-1) and computes the numerators of step s+1: independent work in
-// one basic block, which the compiler interleaves, so the exponentials of one
-// step run beside the matrix instructions of the previous one.
+// iteration s-1) and computes the numerators of step s+1: independent work,
+// which the compiler interleaves, so the exponentials of one step run beside
+// the matrix instructions of the previous one (only the rare rise of a
+// reference maximum branches off).
 #include <type_traits>
 
 #include "dn_device.hpp"
@@ -138,7 +139,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     const int64_t kv_end = causal ? min(Lk, q0 + BQ) : Lk;
     // key group: waves kg * NQW .. kg * NQW + NQW - 1 walk global steps gs0 .. gs0 + nsteps - 1;
     // keys from kv_end_g on are masked for the group (the last group: kv_end)
-    const int qg = wave % NQW, kg = wave / NQW;
+    const int qg = KSP == 1 ? wave : wave % NQW, kg = KSP == 1 ? 0 : wave / NQW;
     const int nsteps = (int)((((kv_end + BKV - 1) / BKV) + KSP - 1) / KSP);
     const int gs0 = kg * nsteps;
     const int64_t kv_end_g = min(kv_end, (int64_t)(gs0 + nsteps) * BKV);
@@ -198,8 +199,8 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) s_rd[kc] = i * 128 + (((4 * kc + G) ^ s_swz(i)) << 4);
     const char* s_ring = smem + KSP * NS * V_BYTES + wave * PF * S_SLOT;
-    auto read_s = [&](int step, u32x4(&r)[QW][2]) {
-        const char* b = s_ring + (step % PF) * S_SLOT;
+    auto read_s = [&](int slot, u32x4(&r)[QW][2]) {
+        const char* b = s_ring + slot * S_SLOT;
 #pragma unroll
         for (int f = 0; f < QW; ++f)
 #pragma unroll
@@ -270,37 +271,52 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     // Masked keys arrive as -inf scores (mask_scores) and yield zeros.
     auto numerators = [&](const u32x4(&sc)[QW][2], u32x4(&pfo)[QW][2], float(&alpha)[QW]) {
         bool raised = false;
+        float sv[QW][2][8], tmax[QW];
+        bool want = false;  // some lane's own scores would raise its query's reference
 #pragma unroll
         for (int f = 0; f < QW; ++f) {
-            float sv[2][8];
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
                 const uint32_t w[4] = {sc[f][kc].x, sc[f][kc].y, sc[f][kc].z, sc[f][kc].w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    sv[kc][2 * e] = bf_lo(w[e]);
-                    sv[kc][2 * e + 1] = bf_hi(w[e]);
+                    sv[f][kc][2 * e] = bf_lo(w[e]);
+                    sv[f][kc][2 * e + 1] = bf_hi(w[e]);
                 }
             }
-            // balanced max tree over the lane's 16 scores, then across the 4 lanes of the query
-            const float m0 = max3f(sv[0][0], sv[0][1], sv[0][2]), m1 = max3f(sv[0][3], sv[0][4], sv[0][5]);
-            const float m2 = max3f(sv[0][6], sv[0][7], sv[1][0]), m3 = max3f(sv[1][1], sv[1][2], sv[1][3]);
-            const float m4 = max3f(sv[1][4], sv[1][5], sv[1][6]);
-            const float tmax = max3f(max3f(m0, m1, m2), max3f(m3, m4, sv[1][7]), m0);
-            const float tmax2 = max_lane_groups(tmax) * kLog2e;
-            const bool raise = tmax2 > mref[f] + 8.0f;
-            const float mnew = raise ? tmax2 : mref[f];
-            // the select keeps -inf - -inf out of exp2 for rows that have not started
-            alpha[f] = __builtin_amdgcn_exp2f(raise ? mref[f] - mnew : 0.f);
-            mref[f] = mnew;
-            raised |= raise;
-            const float nb = mnew == -__builtin_inff() ? 0.f : -mnew;
+            const float m0 = max3f(sv[f][0][0], sv[f][0][1], sv[f][0][2]), m1 = max3f(sv[f][0][3], sv[f][0][4], sv[f][0][5]);
+            const float m2 = max3f(sv[f][0][6], sv[f][0][7], sv[f][1][0]), m3 = max3f(sv[f][1][1], sv[f][1][2], sv[f][1][3]);
+            const float m4 = max3f(sv[f][1][4], sv[f][1][5], sv[f][1][6]);
+            tmax[f] = max3f(max3f(m0, m1, m2), max3f(m3, m4, sv[f][1][7]), m0);
+            want |= tmax[f] * kLog2e > mref[f] + 8.0f;
+        }
+        // The reference rises when the query's maximum over its 4 lanes exceeds it by more
+        // than 8; that holds exactly when one of the lanes' own maxima does (scaling by
+        // log2e keeps the order), so the cross-lane maximum is formed only in the rare
+        // steps where some lane of the wave asks for it.
+        if (__any(want)) {
+#pragma unroll
+            for (int f = 0; f < QW; ++f) {
+                const float tmax2 = max_lane_groups(tmax[f]) * kLog2e;
+                const bool raise = tmax2 > mref[f] + 8.0f;
+                const float mnew = raise ? tmax2 : mref[f];
+                alpha[f] = __builtin_amdgcn_exp2f(raise ? mref[f] - mnew : 0.f);
+                mref[f] = mnew;
+                raised |= raise;
+            }
+        } else {
+#pragma unroll
+            for (int f = 0; f < QW; ++f) alpha[f] = 1.f;
+        }
+#pragma unroll
+        for (int f = 0; f < QW; ++f) {
+            const float nb = mref[f] == -__builtin_inff() ? 0.f : -mref[f];
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[kc][2 * e], kLog2e, nb));
-                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[kc][2 * e + 1], kLog2e, nb));
+                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[f][kc][2 * e], kLog2e, nb));
+                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[f][kc][2 * e + 1], kLog2e, nb));
                     pfo[f][kc][e] = pack_bf16(p0, p1);
                 }
         }
@@ -365,9 +381,15 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     // neither is ever copied
     u32x4 pf2[QW][2];
     // FAST: the copies this iteration issues need no clamping and step s+1 is not an edge
-    // step (both follow from the bound of the loop that passes it, see below).
-    auto iteration = [&](int s, u32x4(&pcur)[QW][2], u32x4(&pnext)[QW][2], auto fast) {
+    // step (both follow from the bound of the loop that passes it, see below).  PAR = s % 2:
+    // the loops run iterations in pairs from step 0, so with two-slot rings the slots each
+    // iteration reads are known at compile time and their offsets go into the LDS reads'
+    // immediate fields.
+    auto iteration = [&](int s, u32x4(&pcur)[QW][2], u32x4(&pnext)[QW][2], auto fast, auto par) {
         constexpr bool FAST = decltype(fast)::value;
+        constexpr int PAR = decltype(par)::value;
+        const int vslot = NS == 2 ? PAR : s % NS;               // V(s)
+        const int sslot = PF == 2 ? PAR ^ 1 : (s + 1) % PF;     // S(s+1)
         wait_vmcnt_asm<WAIT_N>();  // S(s+1) and this wave's V copies of step s are complete
         wait_lgkm0();              // this wave's LDS reads of step s-1 are complete
         block_barrier();
@@ -381,9 +403,9 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
             }
         }
         u32x4 sc[QW][2];
-        read_s(s + 1, sc);
+        read_s(sslot, sc);
         if (!FAST && is_edge(s + 1)) mask_scores(s + 1, sc);
-        const char* vb = smem + (kg * NS + s % NS) * V_BYTES;  // this key group's V ring
+        const char* vb = smem + (kg * NS + vslot) * V_BYTES;  // this key group's V ring
         // V^T fragments of key chunk kc (A operand): two transposing reads of 4 keys per d block
         auto read_v = [&](int kc, u32x4(&vf)[DB]) {
 #pragma unroll
@@ -436,13 +458,15 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
     fast_end = a_e < 0 ? 0 : min(fast_end, (int)(a_e / BKV) - gs0);
     fast_end = __builtin_amdgcn_readfirstlane(max(fast_end, 0));
     int s = 0;
+    using even = std::integral_constant<int, 0>;
+    using odd = std::integral_constant<int, 1>;
     for (; s + 1 < fast_end; s += 2) {  // both iterations of the pair run: no exit test between them
-        iteration(s, pf, pf2, std::true_type{});
-        iteration(s + 1, pf2, pf, std::true_type{});
+        iteration(s, pf, pf2, std::true_type{}, even{});
+        iteration(s + 1, pf2, pf, std::true_type{}, odd{});
     }
     for (; s < nsteps; s += 2) {
-        iteration(s, pf, pf2, std::false_type{});
-        if (s + 1 < nsteps) iteration(s + 1, pf2, pf, std::false_type{});
+        iteration(s, pf, pf2, std::false_type{}, even{});
+        if (s + 1 < nsteps) iteration(s + 1, pf2, pf, std::false_type{}, odd{});
     }
     wait_vmcnt_asm<0>();  // no copy into LDS may outlive the workgroup
 

@@ -399,9 +399,13 @@ def test_ln_linear_norm_on_load_rejects_small_shapes(ops):
     assert e.value.status == 2  # DN_ERR_UNSUPPORTED: the ablation runs on the large tiles only
 
 
+# (1024, 512, 4096): 128 x 128 pipelined tiles whose workgroups exchange row moments;
+# (4104, 320, 4096): 256 x 256 tiles exchanging them; (100, 1024, 520): 8 decode fragments
 @pytest.mark.parametrize("M,K,N,dtype,norm", [(37, 104, 72, "f32", "layernorm"), (257, 1024, 264, "bf16", "layernorm"),
                                               (5, 1024, 520, "bf16", "layernorm"), (50, 1024, 520, "bf16", "layernorm"),
-                                              (4104, 320, 4096, "bf16", "layernorm"),
+                                              (100, 1024, 520, "bf16", "layernorm"),
+                                              (4104, 320, 4096, "bf16", "layernorm"), (1024, 512, 4096, "bf16", "layernorm"),
+                                              (1024, 512, 4096, "bf16", "rms"),
                                               (300, 512, 200, "bf16", "rms"), (3, 8200, 64, "bf16", "rms")])
 def test_linear_deferred_post(ops, M, K, N, dtype, norm):
     # post-LN placement: the deferred product and the normalized rows (the residual branch) from
@@ -430,6 +434,27 @@ def test_linear_deferred_post(ops, M, K, N, dtype, norm):
     var = (xd * xd).mean(1) if rms else xd.var(1)
     np.testing.assert_allclose(sd[:, 0], mean, rtol=1e-4, atol=1e-5)
     np.testing.assert_allclose(sd[:, 1], 1 / np.sqrt(var + case["eps"]), rtol=1e-4)
+
+
+def test_linear_deferred_post_qkv_workload_statistics(ops):
+    # the row statistics the LN -> QKV workload's kernel reduces (4096 x 4096 x 12288, the
+    # bench's launch configuration: 256 x 256 tiles, moments shared between the 16 column
+    # groups of each row block), exported and checked on every row: a share of the moments
+    # lost or counted twice shifts a row's mean far beyond this bound, where it can hide
+    # inside the bf16 tolerance of the outputs
+    w = I.LN_QKV
+    case = I.make_ln(w)
+    g, b = cuda(case["gamma"]), cuda(case["beta"])
+    wp = ops.ln_linear_prepare(cuda(case["W"]), g, b, cuda(case["bias"]))
+    out, y, st = ops.linear_deferred_post(cuda(case["x"]), wp, g, b, case["eps"])
+    torch.cuda.synchronize()
+    sd = st.cpu().double().reshape(w.M, 2).numpy()
+    del out, wp
+    xd = oracle.to_f64(case["x"])
+    np.testing.assert_allclose(sd[:, 0], xd.mean(1), rtol=1e-4, atol=1e-5)
+    np.testing.assert_allclose(sd[:, 1], 1 / np.sqrt(xd.var(1) + case["eps"]), rtol=1e-4)
+    yref = oracle.layernorm(case["x"], case["gamma"], case["beta"], case["eps"], nthreads=ORACLE_THREADS)
+    assert rowwise_rel_err(y.cpu(), yref) <= TOL[torch.bfloat16] / 4
 
 
 def test_linear_deferred_post_deterministic(ops):
@@ -707,6 +732,25 @@ def test_softmax_pv_key_groups_merge(ops):
     out = _sm_check(ops, case, rows=[r for r in range(400) if r != 205])
     assert torch.isnan(out[1, 5].float()).all()
     assert torch.equal(out[1, 6].cpu(), case["V"][1, 150])
+
+
+@pytest.mark.parametrize("BH,L,d,causal", [(256, 264, 128, True), (2, 520, 64, False), (3, 392, 128, True)])
+def test_softmax_pv_reference_rises_mid_row(ops, BH, L, d, causal):
+    # scores that climb along the keys (the reference maximum rises step after step, the partial
+    # sums rescaled each time), fall, stay flat, or jump once late in the row (a single lane's
+    # keys ask for the rise while the others do not), on the 8-wave, split and small kernels
+    case = I.make_sm_case(BH, L, d, causal, seed=BH + L)
+    g = torch.Generator().manual_seed(BH * L)
+    S = case["S"].float()
+    slopes = torch.tensor([0.0, 0.05, 0.2, -0.05])[torch.randint(0, 4, (BH, L, 1), generator=g)]
+    S = S + slopes * torch.arange(L, dtype=torch.float32)
+    spike_q = torch.randint(0, L, (BH, 8), generator=g)
+    for h in range(BH):
+        for q in spike_q[h].tolist():
+            k = q if causal else int(torch.randint(0, L, (1,), generator=g))
+            S[h, q, k] += 30.0
+    case["S"] = S.to(torch.bfloat16)
+    _sm_check(ops, case)
 
 
 def test_softmax_pv_deterministic(ops):
