@@ -508,7 +508,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
 // middle of stage s (when every wave has finished reading stage s), so it has
 // a whole stage of MFMA time to land.
 // =============================================================================
-constexpr int kSgMfma = 0x008, kSgDsRead = 0x100;
+constexpr int kSgValu = 0x002, kSgMfma = 0x008, kSgDsRead = 0x100;
 
 // xh = x r + nb for the 8 bf16 of a fragment chunk, rounded once to bf16.
 __device__ __forceinline__ u32x4 normalize_chunk(const u32x4& a, float r, float nb) {
@@ -666,15 +666,24 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
 #pragma unroll
             for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+        // Shared moments: the wave's owned fragment for k-half h == wn, re-read from the
+        // stage in LDS (one fragment read per stage), summed into (ms1, ms2).
+        float ms1 = 0.f, ms2 = 0.f;
         // MFMAs on (fa, fb) -- and, on the group's first tile, the owned rows'
         // moments from the same fa registers -- with the next half's fragment
         // reads (already issued) interleaved by the scheduler.  OWN < 0: no moments.
-        auto compute = [&](auto own, u32x4(&fa)[FM], u32x4(&fb)[FN]) {
+        // SLICE: the shared-moment share of the stage (ms, read before the stage's
+        // barrier) is reduced by VALU instructions placed between the later MFMAs,
+        // where they fill issue slots beside the matrix pipe instead of running
+        // after the last MFMA and delaying the next barrier.
+        auto compute = [&](auto own, u32x4(&fa)[FM], u32x4(&fb)[FN], auto slice, const u32x4& ms) {
             constexpr int OWN = decltype(own)::value;
+            constexpr bool SLICE = decltype(slice)::value;
             if constexpr (LN && OWN >= 0) {
 #pragma unroll
                 for (int i = 0; i < FMW; ++i) chunk_moments<__bf16>(fa[OWN * FMW + i], s1[i], s2[i]);
             }
+            if constexpr (SLICE) chunk_moments<__bf16>(ms, ms1, ms2);
             if constexpr (NOL) {
 #pragma unroll
                 for (int fm = 0; fm < FM; ++fm) fa[fm] = normalize_chunk(fa[fm], nl_r[fm], nl_b[fm]);
@@ -686,12 +695,12 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
 #pragma unroll
             for (int i = 0; i < NMF; ++i) {
                 __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
-                if (i < NRD) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
+                if (i < NRD)
+                    __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
+                else if (SLICE && i < NRD + 12)
+                    __builtin_amdgcn_sched_group_barrier(kSgValu, 2, 0);
             }
         };
-        // Shared moments: the wave's owned fragment for k-half h == wn, re-read from the
-        // stage in LDS (one fragment read per stage) next to the first half's MFMAs.
-        float ms1 = 0.f, ms2 = 0.f;
         const int mr = wm * WTM + max(own_fm, 0) * 16 + (lane & 15);
         const int mrow = mr * 128 + (((wn * 4 + (lane >> 4)) ^ a_swz(mr)) << 4);
         auto run = [&](auto own, auto slice) {
@@ -704,21 +713,21 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
                 wait_vmcnt<0>();
             }
             block_barrier();
-            u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN], ms;
+            u32x4 fa0[FM], fb0[FN], fa1[FM], fb1[FN], ms = {0u, 0u, 0u, 0u};
             read(0, 0, fa0, fb0);
             for (int s = 0; s < nst; ++s) {
                 read(s, 1, fa1, fb1);
                 // the owned fragment's k-half wn of stage s, read (like every read of stage s)
-                // before the barrier after which stage s + 2 overwrites the buffer
+                // before the barrier after which stage s + 2 overwrites the buffer, and reduced
+                // beside the MFMAs of stage s's second half
                 if (SLICE) ms = lds_ld16(lds_ptr(smem + (s & 1) * STAGE + mrow));
-                compute(own, fa0, fb0);
-                if (SLICE) chunk_moments<__bf16>(ms, ms1, ms2);
+                compute(own, fa0, fb0, std::false_type{}, ms);
                 wait_vmcnt<0>();  // this wave's copies of stage s+1 have landed
                 wait_lgkm0();     // this wave's reads of stage s are complete
                 block_barrier();
                 if (s + 2 < nst) issue(s + 2);  // into the buffer stage s just vacated
                 read(s + 1, 0, fa0, fb0);       // past the end this reads stale data that is never used
-                compute(own, fa1, fb1);
+                compute(own, fa1, fb1, slice, ms);
             }
         };
         const bool moments = LN && !NOL && tt == 0 && !p.row_stats;
