@@ -126,9 +126,10 @@ def parse():
                              "decode_attention", "decode_attention_gqa"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
-    ap.add_argument("--path", default="fused", choices=["fused", "unfused"],
-                    help="what the timed steps run: the deferred kernels (default) or the unfused "
-                         "comparators (for profiling them on their own)")
+    ap.add_argument("--path", default="fused", choices=["fused", "unfused", "library"],
+                    help="what the timed steps run: the deferred kernels (default), the unfused "
+                         "comparators, or (LN workloads) the plain product from the vendor library "
+                         "-- for profiling each on its own")
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip the other named workloads (timed on their own after the layer step)")
     ap.add_argument("--cpu-threads", type=int, default=None)
@@ -176,6 +177,9 @@ class LNSite:
         # nothing), so both paths run the same weight layout and MFMA main loop
         one = torch.ones(w.K, dtype=W.dtype, device="cuda")
         self.Wpks = [ops.ln_linear_prepare(W, one) for _ in range(copies)]
+        # vendor-library reference for the plain product (hipBLASLt through torch), on
+        # MFMA-bound bf16 shapes: W^T stored [N][K], the layout the library runs fastest
+        self.Wt = W.t().contiguous() if self.library_supported() else None
         del W
         self.copies, self.it = copies, 0
         self.y = torch.empty_like(self.x)
@@ -214,6 +218,17 @@ class LNSite:
     def gemm_only(self):
         # the product alone on the same packed weights: no statistics, no normalization
         self.ops.gemm(self.x, self.Wpks[self._next()], self.bias, out=self.out.view(1, self.w.M, self.w.N))
+
+    def library_supported(self):
+        return self.w.dtype == "bf16" and self.w.M > 128
+
+    def library(self):
+        # the same plain product (x . W + bias, bf16 out) from the vendor library: a reference for
+        # what the chip's own GEMM reaches on this shape, not part of the deferred path
+        if self.bias is None:
+            torch.matmul(self.x, self.Wt.t(), out=self.out)
+        else:
+            torch.addmm(self.bias, self.x, self.Wt.t(), out=self.out)
 
     def unfused(self):
         if self.rms:
@@ -660,7 +675,7 @@ def isolated(s, steps):
     # (inside the step the kernel follows the other site, whose traffic evicts the caches);
     # the paths alternate over ROUNDS rounds and each reports its median
     n = max(20, steps)  # iterations per round (each round: every path, in turn)
-    fis, us, uds, sers, sps, nols, posts, gos = [], [], [], [], [], [], [], []
+    fis, us, uds, sers, sps, nols, posts, gos, libs = [], [], [], [], [], [], [], [], []
     serial = isinstance(s, LNSite) and not s.rms and s.w.K <= 16384
     on_load = serial and s.on_load_supported()
     # kernels whose roofline floor is a few microseconds are timed from graph replays
@@ -673,6 +688,8 @@ def isolated(s, steps):
     paths = [(fis, s.fused, n), (us, s.unfused, n)]
     if isinstance(s, LNSite):
         paths.append((gos, s.gemm_only, n))
+        if s.library_supported():
+            paths.append((libs, s.library, n))
     if isinstance(s, (SMSite, AttnSite)) and s.w.causal:
         paths.append((uds, s.unfused_dense, max(3, n // 2)))
     if serial:
@@ -697,6 +714,10 @@ def isolated(s, steps):
         go = float(np.median(gos))
         k["gemm_only_ms"] = round(go, 4)
         k["deferred_overhead_us"] = round(1e3 * (fi - go), 1)
+    if libs:  # reference: the plain product from the vendor library (no normalization)
+        lb = float(np.median(libs))
+        k["library_gemm_ms"] = round(lb, 4)
+        k["library_gemm_tflops"] = round(s.flops() / (lb * 1e-3) / 1e12, 2)
     if uds:
         ud = float(np.median(uds))
         k["unfused_dense_ms"] = round(ud, 4)
@@ -736,7 +757,12 @@ def main():
     sites, wl_name = build_sites(ops, I, args.workload)
     setup_s = time.perf_counter() - t_setup
 
-    fns = [s.fused if args.path == "fused" else s.unfused for s in sites]
+    if args.path == "library" and not all(isinstance(s, LNSite) and s.library_supported() for s in sites):
+        print("--path library runs the plain bf16 product of an LN workload with more than 128 rows",
+              file=sys.stderr)
+        sys.exit(2)
+    fns = [{"fused": s.fused, "unfused": s.unfused, "library": getattr(s, "library", None)}[args.path]
+           for s in sites]
     per, total = time_steps(fns, args.steps, args.warmup, args.warm_seconds)
     if args.calib_copy_mib > 0:
         src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
