@@ -246,7 +246,9 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
         for (int b = 0; b < DB; ++b) acc[f][b] = f32x4{0.f, 0.f, 0.f, 0.f};
         accl[f] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const u32x4 ones = {0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
+    u32x4 ones = {0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
+    // opaque to the compiler, which would otherwise rebuild the constant in every iteration
+    asm volatile("" : "+v"(ones));
 
     // Lane-constant LDS offsets of the V^T fragments.  The V swizzle depends
     // only on bits of (8G + (i >> 2)), which the chunk (kc) and half offsets
