@@ -133,12 +133,24 @@ def test_ln_linear_bf16_large_tiles(ops, M, K, N):
     _ln_check(ops, case)
 
 
+# K >= 8192 on the 256x256 loop, one tile per workgroup and the row moments shared between the
+# column groups of each row block: (2100, 8256, 4200) ragged M and N over 9 x 17 tiles,
+# (2048, 8192, 4096) 8 x 16; every 7th row (all 16-row fragments of every row block) against the
+# oracle
+@pytest.mark.parametrize("M,K,N,norm", [(2100, 8256, 4200, "layernorm"), (2048, 8192, 4096, "layernorm"),
+                                        (2100, 8256, 4200, "rms")])
+def test_norm_linear_bf16_long_k(ops, M, K, N, norm):
+    case = I.make_ln_case(M, K, N, "bf16", seed=M % 91, outliers=3, norm=norm)
+    _ln_check(ops, case, rows=np.arange(0, M, 7))
+
+
 @pytest.mark.parametrize("M,K,N,layout", [(4104, 320, 4096, 2), (4104, 264, 4096, 2), (4104, 264, 4096, 1),
-                                           (300, 136, 264, 2), (257, 512, 1032, 2)])
+                                           (300, 136, 264, 2), (257, 512, 1032, 2), (2100, 8256, 4200, 2)])
 def test_gemm_large(ops, M, K, N, layout):
     # layout 2 (packed weights, gamma = 1) with K % 64 == 0 runs the pipelined loop, on
-    # 256 x 256 tiles at 4104 rows and on 128 x 128 tiles at 257 x 1032 (27 tiles);
-    # K = 264 and K = 136 run the two-stage 128 x 128 loop
+    # 256 x 256 tiles at 4104 rows and at 2100 x 4200 with K = 8256 (every 7th row checked) and
+    # on 128 x 128 tiles at 257 x 1032 (27 tiles); K = 264 and K = 136 run the two-stage
+    # 128 x 128 loop
     g = torch.Generator().manual_seed(5)
     A = torch.randn(M, K, generator=g).to(torch.bfloat16)
     B = torch.randn(K, N, generator=g).to(torch.bfloat16)
@@ -148,8 +160,9 @@ def test_gemm_large(ops, M, K, N, layout):
     else:
         Bd = cuda(B.t().contiguous())
     C = ops.gemm(cuda(A), Bd, cuda(bias), b_layout=layout)
-    ref = oracle.to_f64(A) @ oracle.to_f64(B) + oracle.to_f64(bias)
-    assert rowwise_rel_err(C.cpu(), ref) <= TOL[torch.bfloat16]
+    rows = torch.arange(0, M, 7) if K > 4096 else torch.arange(M)
+    ref = oracle.to_f64(A[rows]) @ oracle.to_f64(B) + oracle.to_f64(bias)
+    assert rowwise_rel_err(C.cpu()[rows], ref) <= TOL[torch.bfloat16]
 
 
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 520), (5, 8200, 264), (16, 512, 72), (3, 8, 8), (17, 1024, 520),
@@ -457,6 +470,26 @@ def test_linear_deferred_post_qkv_workload_statistics(ops):
     assert rowwise_rel_err(y.cpu(), yref) <= TOL[torch.bfloat16] / 4
 
 
+def test_linear_deferred_post_long_k_statistics(ops):
+    # the statistics exported by the 256 x 256 kernel at K = 8192 with the row moments shared
+    # between 16 column groups: every row's (mean, rstd) against the definition, the product on
+    # every 7th row
+    M, K, N = 2048, 8192, 4096
+    case = I.make_ln_case(M, K, N, "bf16", seed=17, outliers=2)
+    g, b = cuda(case["gamma"]), cuda(case["beta"])
+    wp = ops.ln_linear_prepare(cuda(case["W"]), g, b, cuda(case["bias"]))
+    out, y, st = ops.linear_deferred_post(cuda(case["x"]), wp, g, b, case["eps"])
+    torch.cuda.synchronize()
+    sd = st.cpu().double().reshape(M, 2).numpy()
+    xd = oracle.to_f64(case["x"])
+    np.testing.assert_allclose(sd[:, 0], xd.mean(1), rtol=1e-4, atol=1e-5)
+    np.testing.assert_allclose(sd[:, 1], 1 / np.sqrt(xd.var(1) + case["eps"]), rtol=1e-4)
+    rows = np.arange(0, M, 7)
+    ref = oracle.norm_linear_matmul(case["x"][torch.as_tensor(rows)], case["gamma"], case["beta"],
+                                    oracle.to_f64(case["W"]), case["bias"], case["eps"], nthreads=ORACLE_THREADS)
+    assert rowwise_rel_err(out.cpu()[torch.as_tensor(rows)], ref) <= TOL[torch.bfloat16]
+
+
 def test_linear_deferred_post_deterministic(ops):
     case = I.make_ln_case(4104, 320, 4096, "bf16", seed=23)
     g, b = cuda(case["gamma"]), cuda(case["beta"])
@@ -576,11 +609,12 @@ def test_rms_swiglu_bf16_decode_shapes(ops, M, K, N):
     _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M * 3 + 1, outliers=4))
 
 
-@pytest.mark.parametrize("M,K,N", [(4000, 544, 2056), (4000, 520, 2056)])
+@pytest.mark.parametrize("M,K,N", [(4000, 544, 2056), (4000, 520, 2056), (2100, 8256, 2104)])
 def test_rms_swiglu_bf16_large_tiles(ops, M, K, N):
     # 2 x 2056 packed columns: 16 x 17 tiles of 256 x 256 (pipelined loop, ragged M and N); K = 520
-    # takes the 128 x 128 loop
-    _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M % 83, outliers=3))
+    # takes the 128 x 128 loop; K = 8256 runs 129 stages (every 7th row checked)
+    _swiglu_check(ops, I.make_swiglu_case(M, K, N, "bf16", seed=M % 83, outliers=3),
+                  rows=np.arange(0, M, 7) if K > 4096 else None)
 
 
 def test_rms_swiglu_prefill_workload_all_rows(ops):
