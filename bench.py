@@ -66,25 +66,29 @@ KERNEL_SOURCES = {"softmax_pv_deferred": ("softmax_pv.hip", "dn_device.hpp"),
                   "rms_swiglu_deferred": ("ln_gemm.hip", "dn_device.hpp")}
 TRAFFIC = {
     ("softmax_pv_deferred", "causal_softmax_pv_bf16_32x8192x8192_d128"): {
-        "sha256": ("dfea4bf89541f7e6c430cb4992f64612a4548b3c0034efc22c769ab24f62aaff",
+        "sha256": ("5d36d8e80b87248baf0d9311b8d248c71c8ab87536efaf3cdd55c651dcca055b",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 1151338, "fetch_scale": 1.99988, "write_kib": 66245, "write_scale": 1.0},
+        "fetch_kib": 1150884, "fetch_scale": 1.99988, "write_kib": 66369, "write_scale": 1.0},
+    ("softmax_pv_deferred", "softmax_pv_bf16_12x512x512_d64"): {
+        "sha256": ("5d36d8e80b87248baf0d9311b8d248c71c8ab87536efaf3cdd55c651dcca055b",
+                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
+        "fetch_kib": 3676, "fetch_scale": 1.99989, "write_kib": 768, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("9319e05eaf13fc87cd250397763647052a2293a02a7041bd93c7949d6e3a7ea5",
+        "sha256": ("34843ce91948397e0bf88b9bf11f34fc22648f628037f3dd52620c2f4fb99da3",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 300537, "fetch_scale": 1.99991, "write_kib": 108674, "write_scale": 1.0},
+        "fetch_kib": 300556, "fetch_scale": 1.99990, "write_kib": 108674, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_8192x8192x28672"): {
-        "sha256": ("9319e05eaf13fc87cd250397763647052a2293a02a7041bd93c7949d6e3a7ea5",
+        "sha256": ("34843ce91948397e0bf88b9bf11f34fc22648f628037f3dd52620c2f4fb99da3",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 2775738, "fetch_scale": 1.99993, "write_kib": 469250, "write_scale": 1.0},
+        "fetch_kib": 2775771, "fetch_scale": 1.99991, "write_kib": 469250, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("9319e05eaf13fc87cd250397763647052a2293a02a7041bd93c7949d6e3a7ea5",
+        "sha256": ("34843ce91948397e0bf88b9bf11f34fc22648f628037f3dd52620c2f4fb99da3",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 229661, "fetch_scale": 1.99988, "write_kib": 56, "write_scale": 1.0},
+        "fetch_kib": 229664, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_linear_f32_128x768x3072"): {
-        "sha256": ("9319e05eaf13fc87cd250397763647052a2293a02a7041bd93c7949d6e3a7ea5",
+        "sha256": ("34843ce91948397e0bf88b9bf11f34fc22648f628037f3dd52620c2f4fb99da3",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 6228, "fetch_scale": 1.99990, "write_kib": 1536, "write_scale": 1.0},
+        "fetch_kib": 6286, "fetch_scale": 1.99989, "write_kib": 1536, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
         "sha256": ("5526e2ed23dd4cd303791dd3c8321b273869027224059114d5e02fdb98ac51d1",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
