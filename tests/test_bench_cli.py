@@ -34,3 +34,26 @@ def test_bench_weight_copies_cover_the_last_level_cache():
     assert bench.weight_copies(I.LN_QKV) == 1
     assert bench.weight_copies(I.LN_FFN_PREFILL) == 1
     assert bench.weight_copies(I.LN_F32_SMALL) == 1          # above the fp32 ridge point
+
+
+def test_bench_paths_and_traffic_table():
+    # the timed step can run the deferred kernels, the unfused comparators or (for profiling)
+    # the vendor library's plain product; every stored traffic figure names the sources it
+    # was counted on, and a figure taken on other sources reads as unknown
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--help"], capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0 and "library" in r.stdout and "unfused" in r.stdout
+    sys.path.insert(0, ROOT)
+    import bench
+    for (kernel, workload), t in bench.TRAFFIC.items():
+        assert kernel in bench.KERNEL_SOURCES
+        assert len(t["sha256"]) == len(bench.KERNEL_SOURCES[kernel])
+        assert t["fetch_kib"] > 0 and 1.9 < t["fetch_scale"] < 2.1 and t["write_scale"] == 1.0
+    saved = dict(bench.TRAFFIC)
+    try:
+        key = next(iter(bench.TRAFFIC))
+        bench.TRAFFIC[key] = dict(bench.TRAFFIC[key], sha256=("0" * 64,) * len(bench.TRAFFIC[key]["sha256"]))
+        assert bench.measured_traffic(*key) is None
+    finally:
+        bench.TRAFFIC.clear()
+        bench.TRAFFIC.update(saved)
