@@ -787,6 +787,22 @@ def test_softmax_pv_reference_rises_mid_row(ops, BH, L, d, causal):
     _sm_check(ops, case)
 
 
+@pytest.mark.parametrize("BH,L,d,causal", [(256, 264, 128, True), (2, 520, 64, False), (3, 392, 128, True)])
+def test_softmax_pv_nonfinite_scores(ops, BH, L, d, causal):
+    # a NaN score and a +inf score (kept keys) each make their row all NaN, as the plain
+    # definition does (exp(s - m) with m = +inf gives inf - inf); the other rows are unaffected
+    # (8-wave, split and small kernels)
+    case = I.make_sm_case(BH, L, d, causal, seed=L + d)
+    S = case["S"]
+    S[0, 5, 3] = float("nan")
+    S[0, 150, 100] = float("inf")
+    S[BH - 1, L - 1, L // 2] = float("nan")
+    out = _sm_check(ops, case)
+    for h, q in ((0, 5), (0, 150), (BH - 1, L - 1)):
+        assert torch.isnan(out[h, q].float()).all()
+    assert not torch.isnan(out[0, 4].float()).any()
+
+
 def test_softmax_pv_deterministic(ops):
     case = I.make_sm_case(2, 296, 128, True, seed=6)
     S, V = cuda(case["S"]), cuda(case["V"])
