@@ -923,6 +923,29 @@ def test_attention_decode_shapes(ops, BH, Lq, Lk, d):
     _decode_check(ops, I.make_decode_case(BH, Lq, Lk, d, seed=Lk + Lq))
 
 
+@pytest.mark.parametrize("causal", [True, False])
+def test_attention_nonfinite_inputs(ops, causal):
+    # a NaN in a query row makes that row NaN; a NaN in a key row makes NaN every row that
+    # keeps that key (causal: the rows at or after it), as the plain definition does
+    case = I.make_qkv_case(2, 300, 128, causal, seed=31)
+    case["Q"][0, 10, 7] = float("nan")
+    case["K"][1, 200, 3] = float("nan")
+    out = _attn_check(ops, case)
+    assert torch.isnan(out[0, 10].float()).all()
+    assert torch.isnan(out[1, 299].float()).all()
+    if causal:  # the rows before key 200 do not keep it
+        assert not torch.isnan(out[1, 199].float()).any()
+
+
+def test_attention_decode_nonfinite_inputs(ops):
+    # split keys and the merge: a NaN key row poisons its head's rows only
+    case = I.make_decode_case(4, 2, 3000, 128, seed=13)
+    case["K"][2, 1234, 5] = float("nan")
+    out = _decode_check(ops, case)
+    assert torch.isnan(out[2].float()).all()
+    assert not torch.isnan(out[1].float()).any()
+
+
 def test_attention_decode_matches_single_pass(ops):
     # the split + merge against the single-pass kernel on the same inputs: both bf16 outputs
     # of the same exact quantity, so they agree to twice the bf16 output rounding
