@@ -1307,18 +1307,18 @@ static uint32_t moment_wait_ticks() {
     return e ? (uint32_t)strtoul(e, nullptr, 10) : 20000u;
 }
 
-template <Epi EPI, int BT = 256>
-static hipError_t run_pipe(const MainArgs& args, hipStream_t s) {
-    MainArgs a = args;
-    const int64_t tm = (a.M + BT - 1) / BT, tn = (a.N + BT - 1) / BT;
-    // deferred LN: each workgroup takes `group` column tiles of one row block and
-    // reduces the row moments once, on its first tile.  With one workgroup per CU
-    // the run takes about ceil(workgroups / 256) * group tile times; take the
-    // group that minimises that, and of equal ones the largest (fewest moment
-    // reductions).  384 tiles: group 2 (192 workgroups, 2 tile times) instead of
-    // group 1 (384 workgroups, also 2 tile times, twice the moment work).
+// Workgroups for tm x tn tiles.  Deferred LN: each workgroup takes `group` column
+// tiles of one row block and reduces the row moments once, on its first tile.
+// With one workgroup per CU the run takes about ceil(workgroups / 256) * group
+// tile times; take the group that minimises that, and of equal ones the largest
+// (fewest moment reductions).  384 tiles: group 2 (192 workgroups, 2 tile times)
+// instead of group 1 (384 workgroups, also 2 tile times, twice the moment work).
+struct TilePlan {
+    int64_t group, ngroups, wgs, times;
+};
+static TilePlan plan_tiles(int64_t tm, int64_t tn, bool grouped) {
     int64_t group = 1;
-    if (EPI != Epi::kGemm) {
+    if (grouped) {
         int64_t best = -1;
         for (int64_t g = 1; g <= tn; ++g) {
             const int64_t span = (tm * ((tn + g - 1) / g) + 255) / 256 * g;
@@ -1329,6 +1329,30 @@ static hipError_t run_pipe(const MainArgs& args, hipStream_t s) {
         }
     }
     const int64_t ngroups = (tn + group - 1) / group, wgs = tm * ngroups;
+    return TilePlan{group, ngroups, wgs, (wgs + 255) / 256 * group};
+}
+
+// 256 x 192 tiles where they fill the chip in fewer 256 x 256-tile times: a narrow
+// tile costs about kNarrowCost of a square one (three quarters of the MACs, a
+// little more operand traffic per MAC).  4096 x 4096 -> 6144: 512 narrow tiles in
+// two full rounds instead of 384 square ones in 1.5; 1024 x 4096 -> 12288: 256
+// instead of 192 on 256 CUs.
+constexpr double kNarrowCost = 0.8;
+
+template <Epi EPI, int BT = 256>
+static hipError_t run_pipe(const MainArgs& args, hipStream_t s) {
+    MainArgs a = args;
+    const int64_t tm = (a.M + BT - 1) / BT, tn = (a.N + BT - 1) / BT;
+    TilePlan plan = plan_tiles(tm, tn, EPI != Epi::kGemm);
+    bool narrow = false;
+    if constexpr (BT == 256) {
+        const TilePlan nplan = plan_tiles(tm, (a.N + 191) / 192, EPI != Epi::kGemm);
+        if ((double)nplan.times * kNarrowCost < (double)plan.times) {
+            plan = nplan;
+            narrow = true;
+        }
+    }
+    const int64_t group = plan.group, ngroups = plan.ngroups, wgs = plan.wgs;
     // Shared moments where the workgroups of a row block are co-resident (one round of
     // workgroups: 256 at one per CU, 512 for the 128 x 128 tiles at two per CU) and number
     // at least 4 (then each wave row of a workgroup owns at most one 16-row fragment).
@@ -1346,6 +1370,8 @@ static hipError_t run_pipe(const MainArgs& args, hipStream_t s) {
     }
     if constexpr (BT == 128)  // 4 waves of 64 x 64, 64 KiB of LDS: two workgroups per CU
         pipe_kernel<EPI, 2, 2, 128, 128><<<dim3((unsigned)wgs), 4 * kWave, 0, s>>>(a, (int)group);
+    else if (narrow)  // 8 waves of 64 x 96
+        pipe_kernel<EPI, 4, 2, 256, 192><<<dim3((unsigned)wgs), 8 * kWave, 0, s>>>(a, (int)group);
     else
         pipe_kernel<EPI, 4, 2><<<dim3((unsigned)wgs), 8 * kWave, 0, s>>>(a, (int)group);
     return hipGetLastError();
