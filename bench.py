@@ -74,21 +74,25 @@ TRAFFIC = {
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
         "fetch_kib": 3676, "fetch_scale": 1.99989, "write_kib": 768, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("34843ce91948397e0bf88b9bf11f34fc22648f628037f3dd52620c2f4fb99da3",
+        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 300556, "fetch_scale": 1.99990, "write_kib": 108674, "write_scale": 1.0},
+        "fetch_kib": 300435, "fetch_scale": 1.99993, "write_kib": 108674, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_8192x8192x28672"): {
-        "sha256": ("34843ce91948397e0bf88b9bf11f34fc22648f628037f3dd52620c2f4fb99da3",
+        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 2775771, "fetch_scale": 1.99991, "write_kib": 469250, "write_scale": 1.0},
+        "fetch_kib": 2775759, "fetch_scale": 1.99989, "write_kib": 469250, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("34843ce91948397e0bf88b9bf11f34fc22648f628037f3dd52620c2f4fb99da3",
+        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 229664, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
+        "fetch_kib": 229685, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_linear_f32_128x768x3072"): {
-        "sha256": ("34843ce91948397e0bf88b9bf11f34fc22648f628037f3dd52620c2f4fb99da3",
+        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 6286, "fetch_scale": 1.99989, "write_kib": 1536, "write_scale": 1.0},
+        "fetch_kib": 6297, "fetch_scale": 1.99993, "write_kib": 1536, "write_scale": 1.0},
+    ("rms_linear_deferred", "rms_qkv_bf16_4096x4096x6144"): {
+        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
+                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
+        "fetch_kib": 164217, "fetch_scale": 1.99988, "write_kib": 49281, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
         "sha256": ("5526e2ed23dd4cd303791dd3c8321b273869027224059114d5e02fdb98ac51d1",
                    "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
