@@ -66,42 +66,42 @@ KERNEL_SOURCES = {"softmax_pv_deferred": ("softmax_pv.hip", "dn_device.hpp"),
                   "rms_swiglu_deferred": ("ln_gemm.hip", "dn_device.hpp")}
 TRAFFIC = {
     ("softmax_pv_deferred", "causal_softmax_pv_bf16_32x8192x8192_d128"): {
-        "sha256": ("5d36d8e80b87248baf0d9311b8d248c71c8ab87536efaf3cdd55c651dcca055b",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 1150884, "fetch_scale": 1.99988, "write_kib": 66369, "write_scale": 1.0},
+        "sha256": ("8348feaf7e161752c3966e3a1e5f5235f20f8403ef203d36c1487a1565ffb446",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 1131128, "fetch_scale": 1.99988, "write_kib": 65962, "write_scale": 1.0},
     ("softmax_pv_deferred", "softmax_pv_bf16_12x512x512_d64"): {
-        "sha256": ("5d36d8e80b87248baf0d9311b8d248c71c8ab87536efaf3cdd55c651dcca055b",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 3676, "fetch_scale": 1.99989, "write_kib": 768, "write_scale": 1.0},
+        "sha256": ("8348feaf7e161752c3966e3a1e5f5235f20f8403ef203d36c1487a1565ffb446",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 3676, "fetch_scale": 1.99990, "write_kib": 768, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 300435, "fetch_scale": 1.99993, "write_kib": 108674, "write_scale": 1.0},
+        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 300433, "fetch_scale": 1.99993, "write_kib": 108674, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_8192x8192x28672"): {
-        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 2775759, "fetch_scale": 1.99989, "write_kib": 469250, "write_scale": 1.0},
+        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 2775748, "fetch_scale": 1.99993, "write_kib": 469250, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 229685, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
+        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 238155, "fetch_scale": 1.99989, "write_kib": 56, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_linear_f32_128x768x3072"): {
-        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 6297, "fetch_scale": 1.99993, "write_kib": 1536, "write_scale": 1.0},
+        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 6296, "fetch_scale": 1.99990, "write_kib": 1536, "write_scale": 1.0},
     ("rms_linear_deferred", "rms_qkv_bf16_4096x4096x6144"): {
-        "sha256": ("43a0820b0f6cf2c0eb9ca81dc72265462f2f66ca88c1a994294287718667c295",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 164217, "fetch_scale": 1.99988, "write_kib": 49281, "write_scale": 1.0},
+        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 164201, "fetch_scale": 1.99993, "write_kib": 49281, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
-        "sha256": ("5526e2ed23dd4cd303791dd3c8321b273869027224059114d5e02fdb98ac51d1",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 133530, "fetch_scale": 1.99991, "write_kib": 65536, "write_scale": 1.0},
-    # the split kernel and the merge kernel together (530515 + 145 KiB read, 266 + 64 KiB written)
+        "sha256": ("8268a1d5d523228fa454e8d27778b1f368a67909143927d354b7b682fd1aeee2",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 133264, "fetch_scale": 1.99991, "write_kib": 65536, "write_scale": 1.0},
+    # the split kernel and the merge kernel together (527283 + 145 KiB read, 264 + 64 KiB written)
     ("attention_decode_deferred", "decode_attention_bf16_256x1x8192_d128"): {
-        "sha256": ("5526e2ed23dd4cd303791dd3c8321b273869027224059114d5e02fdb98ac51d1",
-                   "77f7f20f4fed0ca3b1d7d0274580e7636579197745fdb08d12465534e86116f3"),
-        "fetch_kib": 530660, "fetch_scale": 1.99989, "write_kib": 330, "write_scale": 1.0},
+        "sha256": ("8268a1d5d523228fa454e8d27778b1f368a67909143927d354b7b682fd1aeee2",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 527428, "fetch_scale": 1.99992, "write_kib": 328, "write_scale": 1.0},
 }
 
 

@@ -81,7 +81,9 @@ __device__ __forceinline__ uint2 lds_tr16(const char* p) {
 }
 }  // namespace fa
 
-template <int D, int NW, int QW, int NS, int BKV>
+// STREAM: every key/value row is read by one workgroup only (decode), so the copies
+// carry the non-temporal hint; prefill workgroups share them through L2.
+template <int D, int NW, int QW, int NS, int BKV, bool STREAM = false>
 __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __restrict__ Q,
                                                             const __bf16* __restrict__ K,
                                                             const __bf16* __restrict__ V, int64_t Lq,
@@ -165,8 +167,13 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
         for (int j = 0; j < T_INS; ++j) {
             const uint32_t key = k0 + c_row[j] < last ? k0 + c_row[j] : last;  // a select, no branch
             const uint32_t dst = base + (uint32_t)((wave + j * NW) * kChunkBytes);
-            g2lds16_async_sb(k_base, key * (uint32_t)ROW + k_p16[j], dst);
-            g2lds16_async_sb(v_base, key * (uint32_t)ROW + v_p16[j], dst + TILE);
+            if constexpr (STREAM) {
+                g2lds16_stream_sb(k_base, key * (uint32_t)ROW + k_p16[j], dst);
+                g2lds16_stream_sb(v_base, key * (uint32_t)ROW + v_p16[j], dst + TILE);
+            } else {
+                g2lds16_async_sb(k_base, key * (uint32_t)ROW + k_p16[j], dst);
+                g2lds16_async_sb(v_base, key * (uint32_t)ROW + v_p16[j], dst + TILE);
+            }
         }
     };
 
@@ -410,12 +417,12 @@ static hipError_t run_attention_decode(const void* Q, const void* K, const void*
     int64_t kchunk;
     attention_decode_split(BH, Lk, D, &nsplit, &kchunk);
     if (nsplit == 1) {  // enough heads to fill the chip: one pass, the division in the kernel's epilogue
-        attention_kernel<D, 1, 1, kDecNS, kDecBKV><<<dim3((unsigned)BH), 64, 0, s>>>(
+        attention_kernel<D, 1, 1, kDecNS, kDecBKV, true><<<dim3((unsigned)BH), 64, 0, s>>>(
             (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, 0, scale * fa::kLog2e, 1, 1, Lk,
             nullptr, (__bf16*)out, 1);
         return hipGetLastError();
     }
-    attention_kernel<D, 1, 1, kDecNS, kDecBKV><<<dim3((unsigned)(BH * nsplit)), 64, 0, s>>>(
+    attention_kernel<D, 1, 1, kDecNS, kDecBKV, true><<<dim3((unsigned)(BH * nsplit)), 64, 0, s>>>(
         (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Lq, Lk, 0, scale * fa::kLog2e, 1, nsplit, kchunk,
         part, nullptr, 1);
     const int64_t rows = BH * Lq;

@@ -153,11 +153,25 @@ __device__ __forceinline__ void g2lds16_async_sb(uint64_t sbase, uint32_t offset
                  : "memory", "m0");
 }
 
+// Streaming form, for bytes one launch reads exactly once (a score matrix, a decode
+// key/value cache): the non-temporal hint keeps them from evicting lines that other
+// workgroups re-read from L2.  Not for data shared between workgroups.
+__device__ __forceinline__ void g2lds16_stream_sb(uint64_t sbase, uint32_t offset, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2 nt"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(offset), "s"(sbase)
+                 : "memory", "m0");
+}
+
 __device__ __forceinline__ uint32_t lds_addr32(const void* p) {
     return (uint32_t)(uintptr_t)(const DN_LDS void*)p;
 }
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+// register load with the non-temporal hint (read-once streams, as above)
+__device__ __forceinline__ u32x4 ld16_stream(const void* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 
 __device__ __forceinline__ u32x4 lds_ld16(const DN_LDS void* p) {
     return *reinterpret_cast<const DN_LDS u32x4*>(p);

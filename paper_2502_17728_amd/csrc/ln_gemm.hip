@@ -1027,7 +1027,7 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
             const int64_t cl = ok ? cc : c_end - 1;
             const int64_t kk = cl * 32 + (lane >> 4) * 8;
 #pragma unroll
-            for (int q = 0; q < NC; ++q) b[u][q] = ld16(wr[q] + cl * kWave * 16);  // zero-padded past K
+            for (int q = 0; q < NC; ++q) b[u][q] = ld16_stream(wr[q] + cl * kWave * 16);  // zero-padded past K
 #pragma unroll
             for (int f = 0; f < MT; ++f) {
                 const u32x4 xv = ld16(xr[f] + min(kk, K - 8));  // K % 8 == 0

@@ -25,7 +25,8 @@
 // Scores are private to a wave, so each wave streams its own rows into a
 // ring of PF LDS slots that only it reads: global->LDS copies of whole
 // 128-byte lines (8 rows per instruction), 16-byte pieces XOR-swizzled so that
-// the fragment reads are bank-conflict free, and no barrier.  V is shared by
+// the fragment reads are bank-conflict free, and no barrier; S is read once, so
+// its copies carry the non-temporal hint and leave L2 to V.  V is shared by
 // all waves and goes through an NS-slot ring with one barrier per step; it
 // stays in its row-major [key][d] layout, pieces XOR-swizzled per key row, and
 // the V^T operand -- eight consecutive keys of one d per lane -- is read with
@@ -185,12 +186,12 @@ __global__ __launch_bounds__(NW * 64) void softmax_pv_kernel(const __bf16* __res
         const uint32_t k0 = (uint32_t)(gs0 + step) * BKV;
         if constexpr (decltype(fast)::value) {
 #pragma unroll
-            for (int j = 0; j < S_LD; ++j) g2lds16_async_sb(s_base + 2u * k0, s_off[j], dst + j * kChunkBytes);
+            for (int j = 0; j < S_LD; ++j) g2lds16_stream_sb(s_base + 2u * k0, s_off[j], dst + j * kChunkBytes);
         } else {
 #pragma unroll
             for (int j = 0; j < S_LD; ++j) {
                 const uint32_t key = k0 + s_p8[j] < klast ? k0 + s_p8[j] : klast;  // a select, no branch
-                g2lds16_async_sb(s_base, s_row[j] + key * 2u, dst + j * kChunkBytes);
+                g2lds16_stream_sb(s_base, s_row[j] + key * 2u, dst + j * kChunkBytes);
             }
         }
     };
