@@ -74,25 +74,25 @@ TRAFFIC = {
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
         "fetch_kib": 3676, "fetch_scale": 1.99990, "write_kib": 768, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 300433, "fetch_scale": 1.99993, "write_kib": 108674, "write_scale": 1.0},
+        "fetch_kib": 298905, "fetch_scale": 1.99989, "write_kib": 110379, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_8192x8192x28672"): {
-        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 2775748, "fetch_scale": 1.99993, "write_kib": 469250, "write_scale": 1.0},
+        "fetch_kib": 2768548, "fetch_scale": 1.99989, "write_kib": 481478, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 238155, "fetch_scale": 1.99989, "write_kib": 56, "write_scale": 1.0},
+        "fetch_kib": 238158, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_linear_f32_128x768x3072"): {
-        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 6296, "fetch_scale": 1.99990, "write_kib": 1536, "write_scale": 1.0},
+        "fetch_kib": 6296, "fetch_scale": 1.99993, "write_kib": 1536, "write_scale": 1.0},
     ("rms_linear_deferred", "rms_qkv_bf16_4096x4096x6144"): {
-        "sha256": ("858fe5507524d1cd42153b006a2658382b65bd185f8c87ec6658f84c15d8728e",
+        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 164201, "fetch_scale": 1.99993, "write_kib": 49281, "write_scale": 1.0},
+        "fetch_kib": 164194, "fetch_scale": 1.99992, "write_kib": 52818, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
         "sha256": ("8268a1d5d523228fa454e8d27778b1f368a67909143927d354b7b682fd1aeee2",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),

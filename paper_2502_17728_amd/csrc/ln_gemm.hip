@@ -509,6 +509,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void main_loop_kernel(MainArgs p) {
 // a whole stage of MFMA time to land.
 // =============================================================================
 constexpr int kSgValu = 0x002, kSgMfma = 0x008, kSgDsRead = 0x100;
+// cache-policy operand of the buffer stores: non-temporal
+constexpr int kStoreStream = 2;
 
 // xh = x r + nb for the 8 bf16 of a fragment chunk, rounded once to bf16.
 __device__ __forceinline__ u32x4 normalize_chunk(const u32x4& a, float r, float nb) {
@@ -897,20 +899,30 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
         // tile's first element: the row offset of each (fm, i) is a scalar
         // (soffset), the lane's offset in the tile a fixed 32-bit VGPR and the
         // fragment column an immediate, so no 64-bit row addresses stay live.
-        // (The host keeps 256 rows of the output below 2^31 bytes.)
+        // (The host keeps 256 rows of the output below 2^31 bytes.)  Every store
+        // carries the non-temporal policy: the output goes to HBM while the
+        // matrix cores still run, instead of staying dirty in the caches for
+        // the next kernel to write back when its own traffic evicts it.
         auto store_tile = [&](__bf16* base, int64_t ldc, int vo, auto col_value, auto ncol) {
             const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
             constexpr int NCOL = decltype(ncol)::value;
 #pragma unroll
-            for (int fm = 0; fm < FM; ++fm)
+            for (int fm = 0; fm < FM; ++fm) {
+                // a fragment's values first, then its stores back to back: the
+                // pieces of each output line reach L2 close together
+                unsigned short hv[4][NCOL];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int f = 0; f < NCOL; ++f) hv[i][f] = __builtin_bit_cast(unsigned short, (__bf16)col_value(fm, f, i));
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int so = __builtin_amdgcn_readfirstlane((fm * 16 + i) * (int)ldc * 2);
 #pragma unroll
                     for (int f = 0; f < NCOL; ++f)
-                        __builtin_amdgcn_raw_buffer_store_b16(
-                            __builtin_bit_cast(unsigned short, (__bf16)col_value(fm, f, i)), rc, vo + f * 32, so, 0);
+                        __builtin_amdgcn_raw_buffer_store_b16(hv[i][f], rc, vo + f * 32, so, kStoreStream);
                 }
+            }
         };
         // A ragged tile checks each store against the rows and columns left.
         auto store_edge = [&](__bf16* base, int64_t ldc, int64_t rows_left, int64_t cols_left, int col0,
@@ -928,7 +940,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void pipe_kernel(MainArgs p, int gro
                         if (rl < rows_left && col < cols_left)
                             __builtin_amdgcn_raw_buffer_store_b16(
                                 __builtin_bit_cast(unsigned short, (__bf16)col_value(fm, f, i)), rc,
-                                (rl * (int)ldc + col) * 2, 0, 0);
+                                (rl * (int)ldc + col) * 2, 0, kStoreStream);
                     }
                 }
         };
