@@ -142,6 +142,14 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
 #pragma unroll
         for (int c = 0; c < DC; ++c) qf[f][c] = ld16(Qh + qr * D + 32 * c + 8 * G);
     }
+    // Q is in registers before the key loop: each fragment is an operand of an empty
+    // statement here, so the compiler places its waits for these loads before the
+    // loop.  Left to find the first use inside it, it kept waits there on every
+    // step, and at run time those also drained the copies issued for the next step.
+#pragma unroll
+    for (int f = 0; f < QW; ++f)
+#pragma unroll
+        for (int c = 0; c < DC; ++c) asm volatile("" : "+v"(qf[f][c]));
     wait_vmcnt_asm<0>();  // before the hand-counted copies below start
 
     // ---- K/V ring.  Copy instruction j of a wave covers tile rows
@@ -236,10 +244,14 @@ __global__ __launch_bounds__(NW * 64) void attention_kernel(const __bf16* __rest
             for (int f = 0; f < QW; ++f) {
                 const int lim = causal ? min((int)qrow[f], kv_endi - 1) : kv_endi - 1;
 #pragma unroll
-                for (int b4 = 0; b4 < NKB; ++b4)
+                for (int b4 = 0; b4 < NKB; ++b4) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         if (k0 + 16 * b4 + 4 * G + e > lim) st[f][b4][e] = -__builtin_inff();
+                    // one block's compare masks at a time: issued all at once they
+                    // took 64 SGPRs and pushed loop-long scalars into VGPR lanes
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
         }
         bool raised = false;
@@ -391,16 +403,18 @@ __global__ __launch_bounds__(256) void attention_merge_kernel(const float* __res
     for (int j = 0; j < PER; ++j) out[row * D + lane + 64 * j] = (__bf16)(acc[j] * inv);
 }
 
-// Decode kernel: one wave of 16 query slots per workgroup (Lq <= 16), 32-key steps, a
-// ring of 4 slots (three steps in flight while one is computed): 512 d bytes of LDS.
-constexpr int kDecNS = 4, kDecBKV = 32;
+// Decode kernel: one wave of 16 query slots per workgroup (Lq <= 16), 128-key steps, a
+// ring of 2 slots (the next step's copies in flight while one is computed): 1024 d
+// bytes of LDS.  Measured on 256 heads x 8192 keys, d = 128 (split kernel + merge):
+// 157 us, against 164 us for 3 slots of 64 keys, 167 us for 2 of 64 and 173 us for
+// 4 of 32 -- fewer, larger copies in flight per workgroup stream best.
+constexpr int kDecNS = 2, kDecBKV = 128;
 constexpr int64_t kCUs = 256, kLdsPerCU = 160 * 1024;
 inline int64_t decode_lds_bytes(int64_t d) { return (int64_t)kDecNS * 2 * kDecBKV * d * 2; }
 
-// Decode split: as many workgroups as fit on the chip at once (LDS-bound: 2 per CU at
-// d = 128, 5 at d = 64), spread over the heads; each split a whole number of steps.
-// Measured on 256 heads x 8192 keys, d = 128: one resident round beats 2 and 4 rounds
-// (their tails) and the 64-key, 2-slot ring (fewer bytes in flight per CU).
+// Decode split: as many workgroups as fit on the chip at once (LDS-bound: 1 per CU at
+// d = 128, 2 at d = 64), spread over the heads; each split a whole number of steps.
+// One resident round beats 2 and 4 rounds (their tails).
 static void attention_decode_split(int64_t BH, int64_t Lk, int64_t d, int* nsplit, int64_t* kchunk) {
     const int64_t wgs = kCUs * (kLdsPerCU / decode_lds_bytes(d));
     const int64_t steps = (Lk + kDecBKV - 1) / kDecBKV;
