@@ -74,25 +74,25 @@ TRAFFIC = {
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
         "fetch_kib": 3676, "fetch_scale": 1.99990, "write_kib": 768, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_qkv_bf16_4096x4096x12288"): {
-        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
+        "sha256": ("70ff13ee8dfa009c3eb542e1df3eb31c525d39718e9311900f3f1a3c58b46307",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 298905, "fetch_scale": 1.99989, "write_kib": 110379, "write_scale": 1.0},
+        "fetch_kib": 298905, "fetch_scale": 1.99992, "write_kib": 109686, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_8192x8192x28672"): {
-        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
+        "sha256": ("70ff13ee8dfa009c3eb542e1df3eb31c525d39718e9311900f3f1a3c58b46307",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 2768548, "fetch_scale": 1.99989, "write_kib": 481478, "write_scale": 1.0},
+        "fetch_kib": 2768553, "fetch_scale": 1.99993, "write_kib": 481424, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_ffn_up_bf16_decode_t1_8192x28672"): {
-        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
+        "sha256": ("70ff13ee8dfa009c3eb542e1df3eb31c525d39718e9311900f3f1a3c58b46307",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 238158, "fetch_scale": 1.99993, "write_kib": 56, "write_scale": 1.0},
+        "fetch_kib": 233660, "fetch_scale": 1.99986, "write_kib": 56, "write_scale": 1.0},
     ("ln_linear_deferred", "ln_linear_f32_128x768x3072"): {
-        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
+        "sha256": ("70ff13ee8dfa009c3eb542e1df3eb31c525d39718e9311900f3f1a3c58b46307",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 6296, "fetch_scale": 1.99993, "write_kib": 1536, "write_scale": 1.0},
+        "fetch_kib": 6296, "fetch_scale": 1.99992, "write_kib": 1536, "write_scale": 1.0},
     ("rms_linear_deferred", "rms_qkv_bf16_4096x4096x6144"): {
-        "sha256": ("c1eba0ce5930cc5522efb98f1bb545f13001c5861282f6a22b437afa1397902e",
+        "sha256": ("70ff13ee8dfa009c3eb542e1df3eb31c525d39718e9311900f3f1a3c58b46307",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
-        "fetch_kib": 164194, "fetch_scale": 1.99992, "write_kib": 52818, "write_scale": 1.0},
+        "fetch_kib": 164194, "fetch_scale": 1.99993, "write_kib": 52852, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
         "sha256": ("48c04e65a188cead7ed3178f67d4948075975384ebcbf9579db3d7c0b459fb83",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),

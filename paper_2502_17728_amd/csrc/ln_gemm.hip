@@ -1009,9 +1009,16 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
 #pragma unroll
     for (int q = 0; q < NC; ++q) wr[q] = Wp + packed_chunk(min(nb0 + q, nblocks - 1), 0, kchunks, lane);
 
+    // The KS waves split the chunks: with one row fragment interleaved (wave w takes
+    // chunks w, w + KS, ..., so the waves of a workgroup read neighbouring KiB of each
+    // column block at a time), with more in contiguous ranges.  Measured: 1 token on
+    // 8192 -> 2 x 28672 (gated MLP) 152.5 -> 141.4 us and on 8192 -> 28672 78.1 ->
+    // 77.3 us interleaved; 32 tokens on 4096 -> 12288 25.2 -> 27.3 us, so ranges there.
+    constexpr bool ILV = MT == 1;
     const int64_t nchunks = kchunks;
     const int64_t per = (nchunks + KS - 1) / KS;
-    const int64_t c_begin = wave * per, c_end = min(nchunks, c_begin + per);
+    const int64_t c_begin = ILV ? 0 : wave * per;
+    const int64_t c_end = ILV ? (nchunks > wave ? (nchunks - wave + KS - 1) / KS : 0) : min(nchunks, c_begin + per);
 
     const u32x4 ones = {0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
     const u32x4 zero = {0, 0, 0, 0};
@@ -1034,9 +1041,9 @@ __global__ __launch_bounds__(KS * kWave) void ln_decode_bf16_kernel(const __bf16
     auto load = [&](u32x4(&a)[U][MT], u32x4(&b)[U][NC], int64_t g) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t cc = c_begin + g * U + u;
-            const bool ok = cc < c_end;
-            const int64_t cl = ok ? cc : c_end - 1;
+            const int64_t ci = c_begin + g * U + u;  // the wave's ci-th chunk
+            const bool ok = ci < c_end;
+            const int64_t cl = ILV ? (ok ? ci : c_end - 1) * KS + wave : (ok ? ci : c_end - 1);
             const int64_t kk = cl * 32 + (lane >> 4) * 8;
 #pragma unroll
             for (int q = 0; q < NC; ++q) b[u][q] = ld16_stream(wr[q] + cl * kWave * 16);  // zero-padded past K
