@@ -94,12 +94,12 @@ TRAFFIC = {
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
         "fetch_kib": 164194, "fetch_scale": 1.99993, "write_kib": 52852, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
-        "sha256": ("48c04e65a188cead7ed3178f67d4948075975384ebcbf9579db3d7c0b459fb83",
+        "sha256": ("7a22d31fdb1a62b1da07e531c37abb39162f3075d1df416b61aae2ba1f2a525e",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
         "fetch_kib": 144248, "fetch_scale": 1.99991, "write_kib": 65536, "write_scale": 1.0},
     # 256 heads fill the chip with one workgroup per head: no key split, no merge kernel
     ("attention_decode_deferred", "decode_attention_bf16_256x1x8192_d128"): {
-        "sha256": ("48c04e65a188cead7ed3178f67d4948075975384ebcbf9579db3d7c0b459fb83",
+        "sha256": ("7a22d31fdb1a62b1da07e531c37abb39162f3075d1df416b61aae2ba1f2a525e",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
         "fetch_kib": 524463, "fetch_scale": 1.99990, "write_kib": 64, "write_scale": 1.0},
 }

@@ -325,8 +325,8 @@ DN_API dn_status attention_decode_deferred(const void* Q, const void* K, const v
  * with no workspace argument.  The key-range partials go to a 12 MiB device
  * array that the library holds on each GPU it runs on until the process ends;
  * no call allocates or frees memory.  Every request attention_decode_deferred
- * accepts fits it (the partials stay below 10.6 MiB at d = 64 and 8.3 MiB at
- * d = 128); a request that would not gives DN_ERR_UNSUPPORTED.  The array
+ * accepts fits it (the partials stay below 4.25 MiB at d = 64 and 4.125 MiB
+ * at d = 128); a request that would not gives DN_ERR_UNSUPPORTED.  The array
  * keeps the last call's partials, which every call overwrites before it reads
  * them; calls that overlap on one GPU (concurrent streams) share it and race.
  * Arguments, layout, grouped-query use and status codes as

@@ -405,7 +405,7 @@ __global__ __launch_bounds__(256) void attention_merge_kernel(const float* __res
 
 // Decode kernel: one wave of 16 query slots per workgroup (Lq <= 16), 128-key steps, a
 // ring of 2 slots (the next step's copies in flight while one is computed): 1024 d
-// bytes of LDS.  Measured on 256 heads x 8192 keys, d = 128 (split kernel + merge):
+// bytes of LDS.  Measured on 256 heads x 8192 keys, d = 128, per call:
 // 157 us, against 164 us for 3 slots of 64 keys, 167 us for 2 of 64 and 173 us for
 // 4 of 32 -- fewer, larger copies in flight per workgroup stream best.
 constexpr int kDecNS = 2, kDecBKV = 128;
@@ -460,9 +460,9 @@ hipError_t launch_attention_decode(const void* Q, const void* K, const void* V, 
 // ---------------------------------------------------------------------------
 // Allocation-free decode: the per-split partials go to a file-scope device array
 // instead of a caller workspace.  Every valid call fits it: with nsplit > 1 the
-// heads number fewer than the resident workgroups W (1280 at d = 64, 512 at
+// heads number fewer than the resident workgroups W (512 at d = 64, 256 at
 // d = 128), so BH * nsplit < 2 W and the partials take less than
-// 2 W * 16 * (d + 4) * 4 bytes -- 10.6 MiB at d = 64, 8.3 MiB at d = 128.
+// 2 W * 16 * (d + 4) * 4 bytes -- 4.25 MiB at d = 64, 4.125 MiB at d = 128.
 // In host code `scratch` names a host-side stand-in; its device address (one
 // copy per GPU) is looked up once per device with hipGetSymbolAddress and only
 // that address is passed to kernels.
