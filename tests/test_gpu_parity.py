@@ -916,10 +916,11 @@ def _decode_check(ops, case, heads=None):
 
 @pytest.mark.parametrize("BH,Lq,Lk,d", [(1, 1, 1, 64), (3, 1, 100, 128), (2, 4, 8200, 128), (5, 16, 8192, 64),
                                         (1, 7, 70001, 128), (2048, 1, 130, 64), (8, 3, 64, 128),
-                                        (600, 2, 3000, 128)])
+                                        (600, 2, 3000, 128), (255, 1, 4100, 128), (511, 2, 1000, 64)])
 def test_attention_decode_shapes(ops, BH, Lq, Lk, d):
     # single key; ragged caches (not whole steps); splits of one step and of many steps (one head,
-    # long cache); enough heads for a single pass without the merge; partial query tiles
+    # long cache); enough heads for a single pass without the merge; partial query tiles; one head
+    # short of a full resident round (255 at d = 128, 511 at d = 64: two ranges per head)
     _decode_check(ops, I.make_decode_case(BH, Lq, Lk, d, seed=Lk + Lq))
 
 
