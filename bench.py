@@ -93,6 +93,10 @@ TRAFFIC = {
         "sha256": ("70ff13ee8dfa009c3eb542e1df3eb31c525d39718e9311900f3f1a3c58b46307",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
         "fetch_kib": 164194, "fetch_scale": 1.99993, "write_kib": 52852, "write_scale": 1.0},
+    ("rms_swiglu_deferred", "rms_swiglu_bf16_decode_t1_8192x28672"): {
+        "sha256": ("70ff13ee8dfa009c3eb542e1df3eb31c525d39718e9311900f3f1a3c58b46307",
+                   "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
+        "fetch_kib": 459121, "fetch_scale": 1.99994, "write_kib": 56, "write_scale": 1.0},
     ("attention_deferred", "causal_attention_bf16_32x8192x8192_d128"): {
         "sha256": ("7a22d31fdb1a62b1da07e531c37abb39162f3075d1df416b61aae2ba1f2a525e",
                    "ac9c5fe92ec45f657c9519fcd8d54a4977d6a85897f645cae15b69abf72ca89a"),
